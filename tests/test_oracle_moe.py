@@ -1,0 +1,188 @@
+"""Pins for the routed half of the oracle: the hard dispatch (Section 2), the shared-decoder
+expert forward with the multilabel softmax loss (Section 2; Section 4.1, Eq. 3) and its
+gradients.
+
+Independent checks: numpy's stable argsort, scipy's logsumexp, PyTorch CPU fp64 autograd
+(per-sample expert selection + cross_entropy with probability targets), central finite
+differences, the closed form for a zero decoder, and the hand-worked loss fixture."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+from scipy.special import logsumexp
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _case(seed, n=40, d=6, h=9, o=5, V=13, K=3, empty=None, max_tags=4):
+    rs = np.random.default_rng(seed)
+    X = rs.normal(size=(n, d))
+    a = rs.integers(0, K, n).astype(np.int32)
+    if empty is not None:
+        a[a == empty] = (empty + 1) % K
+    W1 = rs.normal(size=(K, h, d)) / np.sqrt(d)
+    b1 = rs.normal(size=(K, h)) * 0.3
+    W2 = rs.normal(size=(K, o, h)) / np.sqrt(h)
+    b2 = rs.normal(size=(K, o)) * 0.3
+    D = rs.normal(size=(V, o)) / np.sqrt(o)
+    bD = rs.normal(size=V) * 0.3
+    cnt = rs.integers(1, max_tags + 1, n)
+    tags = [rs.choice(V, c, replace=False) for c in cnt]
+    row_ptr = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int32)
+    tag = np.concatenate(tags).astype(np.int32)
+    return dict(X=X, a=a, W1=W1, b1=b1, W2=W2, b2=b2, D=D, bD=bD, row_ptr=row_ptr, tag=tag)
+
+
+def _fwd(orc, c, **kw):
+    return orc.moe_forward(c["X"], c["a"], c["W1"], c["b1"], c["W2"], c["b2"], c["D"], c["bD"],
+                           c["row_ptr"], c["tag"], **kw)
+
+
+def _bwd(orc, c, f, **kw):
+    return orc.moe_backward(c["X"], c["a"], c["W1"], c["W2"], c["D"], c["bD"], c["row_ptr"],
+                            c["tag"], f["H1"], f["H"], f["lse"], **kw)
+
+
+# ------------------------------------------------------------------ dispatch
+
+@pytest.mark.parametrize("n,K", [(0, 3), (1, 1), (1000, 7), (513, 64)])
+def test_dispatch_is_stable_sort(orc, n, K):
+    rs = np.random.default_rng(n + K)
+    e = rs.integers(0, K, n).astype(np.int32)
+    if n > 10:
+        e[e == 2] = 3  # force an empty bucket
+    counts, offsets, perm, inv = orc.dispatch(e, K)
+    assert np.array_equal(perm, np.argsort(e, kind="stable"))
+    assert np.array_equal(counts, np.bincount(e, minlength=K))
+    assert offsets[0] == 0 and offsets[-1] == n
+    assert np.array_equal(np.diff(offsets), counts)
+    assert np.array_equal(inv[perm], np.arange(n))
+    assert np.array_equal(perm[inv], np.arange(n))
+    # combine(dispatch(rows)) is the identity
+    rows = rs.normal(size=(n, 3))
+    assert np.array_equal(rows[perm][inv], rows)
+
+
+# ------------------------------------------------------------------ forward
+
+def test_loss_golden(orc):
+    g = json.load(open(os.path.join(GOLD, "loss_tiny.json")))
+    # One expert whose output is exactly h: d = h = o = 1, W1 = W2 = 1, x = h > 0.
+    X = np.array([[g["h"]], [g["h"]]])
+    one = np.ones((1, 1, 1))
+    D = np.array(g["D"], float)
+    row_ptr = np.array(g["row_ptr"], np.int32)
+    tag = np.array(g["tag"], np.int32)
+    f = orc.moe_forward(X, np.zeros(2, np.int32), one, None, one, None, D, None, row_ptr, tag,
+                        want_probs=True)
+    np.testing.assert_allclose(f["lse"], g["lse"], rtol=1e-14)
+    np.testing.assert_allclose(f["loss"], g["loss"], rtol=1e-14)
+    np.testing.assert_allclose(f["probs"][0], g["probs"], rtol=1e-14)
+    b = orc.moe_backward(X, np.zeros(2, np.int32), one, one, D, None, row_ptr, tag,
+                         f["H1"], f["H"], f["lse"])
+    dl = np.array(g["dlogits"])
+    # dbD is the batch sum of dloss/dlogits; dD = sum_i dlogits_i * h
+    np.testing.assert_allclose(b["dbD"], dl.sum(axis=0), rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(b["dD"][:, 0], dl.sum(axis=0) * g["h"], rtol=1e-13, atol=1e-15)
+
+
+def test_zero_decoder_gives_log_v(orc):
+    c = _case(1, V=37)
+    c["D"] = np.zeros_like(c["D"])
+    c["bD"] = np.zeros_like(c["bD"])
+    f = _fwd(orc, c, want_probs=True)
+    np.testing.assert_allclose(f["loss"], np.log(37.0), rtol=1e-15)
+    np.testing.assert_allclose(f["probs"], 1.0 / 37.0, rtol=1e-14)
+    b = _bwd(orc, c, f)
+    n = c["X"].shape[0]
+    # g = (1/V - y)/n: closed form for dbD
+    y = np.zeros((n, 37))
+    for i in range(n):
+        t = c["tag"][c["row_ptr"][i]:c["row_ptr"][i + 1]]
+        y[i, t] = 1.0 / len(t)
+    np.testing.assert_allclose(b["dbD"], ((1.0 / 37.0) - y).sum(axis=0) / n, atol=1e-15)
+
+
+def test_softmax_rows_and_lse(orc):
+    c = _case(2, V=50)
+    f = _fwd(orc, c, want_probs=True)
+    np.testing.assert_allclose(f["probs"].sum(axis=1), 1.0, rtol=1e-13)
+    logits = f["H"] @ c["D"].T + c["bD"]
+    np.testing.assert_allclose(f["lse"], logsumexp(logits, axis=1), rtol=1e-13)
+    assert np.isclose(f["loss_mean"], f["loss"].mean(), rtol=1e-14)
+
+
+def _torch_loss(c, store_mask=None):
+    """The same model written with PyTorch ops (fp64 CPU) for autograd."""
+    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=k not in ("row_ptr", "tag", "a"))
+         for k, v in c.items() if k not in ("row_ptr", "tag", "a")}
+    a = torch.tensor(c["a"], dtype=torch.long)
+    z = torch.einsum("nhd,nd->nh", t["W1"][a], t["X"]) + t["b1"][a]
+    h1 = torch.relu(z)
+    y = torch.einsum("noh,nh->no", t["W2"][a], h1) + t["b2"][a]
+    logits = y @ t["D"].T + t["bD"]
+    n, V = logits.shape
+    target = torch.zeros(n, V, dtype=torch.float64)
+    for i in range(n):
+        tg = c["tag"][c["row_ptr"][i]:c["row_ptr"][i + 1]]
+        target[i, torch.tensor(tg, dtype=torch.long)] = 1.0 / len(tg)
+    loss = torch.nn.functional.cross_entropy(logits, target)  # mean over the batch
+    loss.backward()
+    return t, loss, h1, y
+
+
+@pytest.mark.parametrize("K,empty", [(1, None), (3, None), (4, 2)])
+def test_matches_torch_autograd(orc, K, empty):
+    c = _case(3 + K, K=K, empty=empty)
+    f = _fwd(orc, c)
+    b = _bwd(orc, c, f)
+    t, loss, h1, y = _torch_loss(c)
+    assert np.isclose(f["loss_mean"], loss.item(), rtol=1e-12)
+    np.testing.assert_allclose(f["H1"], h1.detach().numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(f["H"], y.detach().numpy(), rtol=1e-12, atol=1e-13)
+    for k in ("W1", "b1", "W2", "b2", "D", "bD", "X"):
+        np.testing.assert_allclose(b["d" + k], t[k].grad.numpy(), rtol=1e-10, atol=1e-13,
+                                   err_msg=k)
+    if empty is not None:
+        for k in ("dW1", "db1", "dW2", "db2"):
+            assert np.all(b[k][empty] == 0.0)
+
+
+def test_finite_differences(orc):
+    """Central differences of loss_mean on the fp64 oracle itself (h = 1e-6)."""
+    c = _case(11, n=12, d=4, h=6, o=3, V=7, K=2, max_tags=3)
+    # keep pre-activations away from the ReLU kink so the loss is smooth at the probe points
+    f = _fwd(orc, c)
+    b = _bwd(orc, c, f)
+    rs = np.random.default_rng(0)
+    eps = 1e-6
+
+    def loss_at(cc):
+        return _fwd(orc, cc)["loss_mean"]
+
+    for key, gkey in (("W1", "dW1"), ("b1", "db1"), ("W2", "dW2"), ("b2", "db2"),
+                      ("D", "dD"), ("bD", "dbD"), ("X", "dX")):
+        for _ in range(4):
+            idx = tuple(rs.integers(0, s) for s in c[key].shape)
+            cp = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in c.items()}
+            cm = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in c.items()}
+            cp[key][idx] += eps
+            cm[key][idx] -= eps
+            fd = (loss_at(cp) - loss_at(cm)) / (2 * eps)
+            an = b[gkey][idx]
+            assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (key, idx, fd, an)
+
+
+def test_store_rounding_points(orc):
+    """With bf16 storage the hidden activations and outputs are bf16 values and dX too."""
+    c = _case(12)
+    f = _fwd(orc, c, store="bf16")
+    for k in ("H1", "H"):
+        np.testing.assert_array_equal(orc.round_store(f[k], "bf16"), f[k])
+    b = _bwd(orc, c, f, store="bf16")
+    np.testing.assert_array_equal(orc.round_store(b["dX"], "bf16"), b["dX"])
+    f64 = _fwd(orc, c, store="f64")
+    # the stored H differs from the unrounded one by at most half a bf16 ulp chain
+    assert np.max(np.abs(f["H"] - f64["H"])) < 0.05
