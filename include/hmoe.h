@@ -1,0 +1,174 @@
+/*
+ * hmoe.h -- C ABI of the hard mixture-of-experts hot path on MI355X (gfx950).
+ *
+ * Method: Gross, Ranzato & Szlam, "Hard Mixtures of Experts for Large Scale Weakly
+ * Supervised Vision" (arXiv 1704.06363).  A K-means gater over feature vectors picks exactly
+ * one expert per sample (Section 2, Eq. 2); each expert is trained on its own share of the
+ * data; in the shared-decoder variant (Section 2, shared-decoder figure) every expert feeds
+ * one decoder D whose outputs go through the multilabel softmax loss of Section 4.1, Eq. 3.
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns all memory.
+ *     The library allocates nothing and keeps no state between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Every call is
+ *     asynchronous on that stream and performs no host synchronisation.
+ *   - Scratch memory comes from the caller through (ws, ws_bytes); the matching *_workspace()
+ *     call returns the number of bytes needed (0 is a valid answer; ws may then be NULL).
+ *   - Matrices are row-major.  Real tensors are HMOE_F32 (float) or HMOE_BF16 (bfloat16,
+ *     round-to-nearest-even on store); accumulation is always fp32 or wider.
+ *   - Row widths (d, d_hid, d_out, vocab for the decoder) must be multiples of 8 and device
+ *     pointers 16-byte aligned, else HMOE_ESHAPE.  n may be 0 (nothing is launched).
+ *     Indices are int32 (n < 2^31); 1 <= K <= 4096.
+ *   - Return value: HMOE_OK (0) or a negative code; argument errors are detected before any
+ *     launch and described by hmoe_last_error() (thread-local).  Launch failures return
+ *     HMOE_EHIP.  Faults inside kernels surface at the caller's next synchronisation.
+ */
+#ifndef HMOE_H_
+#define HMOE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HMOE_VERSION 1
+
+enum {
+  HMOE_OK = 0,
+  HMOE_EINVAL = -1,     /* NULL required pointer, negative size, K out of range */
+  HMOE_EDTYPE = -2,     /* unknown dtype */
+  HMOE_ESHAPE = -3,     /* width not a multiple of 8, misaligned pointer */
+  HMOE_EWORKSPACE = -4, /* ws_bytes smaller than the *_workspace() answer */
+  HMOE_EHIP = -5        /* a HIP launch or runtime call failed */
+};
+
+typedef enum { HMOE_F32 = 0, HMOE_BF16 = 1 } hmoe_dtype_t;
+
+/* Message for the last error on this thread ("" if none). */
+const char* hmoe_last_error(void);
+/* HMOE_VERSION of the library. */
+int hmoe_version(void);
+
+/* ------------------------------------------------------------------ gater (K-means) */
+
+/* Nearest-centroid assignment, Section 2, Eq. 2: assign[i] = argmin_k |X_i - C_k|^2 with
+ * ties going to the lowest k; min_dist[i] (optional) = that squared distance.
+ *   X [n x d] and C [K x d] in dtype dt (a bf16 gater multiplies bf16 centres).
+ *   The distance is computed as |c|^2 - 2 x.c + |x|^2 with fp32 accumulation (MFMA).
+ *   assign: int32[n] out.  min_dist: float[n] out or NULL. */
+size_t hmoe_kmeans_assign_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt);
+int hmoe_kmeans_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C,
+                       int32_t K, int32_t* assign, float* min_dist, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* Lloyd's K-means on the gater features (Section 2; K = 50 centres in Section 4.2) for a
+ * fixed number of iterations: for t < n_iter: assign against C_t, J_t = sum of min
+ * distances, C_{t+1} = mean of each cluster (empty clusters reseeded when reseed_empty:
+ * in ascending id order each takes the farthest remaining sample whose cluster has more
+ * than one member; an empty cluster that finds none keeps its centre); then a final assign
+ * against C_T and J_T.
+ *   init_uniforms: device double[K] in [0,1) -> k-means++ seeding (first centre row
+ *     floor(u0*n), then the first row whose running sum of D^2 exceeds u_t * total);
+ *     NULL -> C already holds the initial centres.
+ *   C: float[K x d] in/out (fp32 master copy; a bf16 fit assigns against bf16(C)).
+ *   assign: int32[n] out (final assignment).  min_dist: float[n] out or NULL.
+ *   counts: int32[K] out or NULL.  objective: double[n_iter+1] out or NULL.
+ *   init_idx: int32[K] out or NULL (k-means++ picks).  K <= n is required. */
+size_t hmoe_kmeans_fit_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt);
+int hmoe_kmeans_fit(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K,
+                    int32_t n_iter, const double* init_uniforms, int32_t reseed_empty,
+                    float* C, int32_t* assign, float* min_dist, int32_t* counts,
+                    double* objective, int32_t* init_idx, void* ws, size_t ws_bytes,
+                    void* stream);
+
+/* One Lloyd centre update (Section 2), also usable over data streamed in chunks.
+ *   mode HMOE_UPDATE_FULL: zero sums/counts, accumulate this X, reseed (if reseed_empty)
+ *     and write C.  HMOE_UPDATE_ACCUMULATE: add this chunk to sums/counts only.
+ *     HMOE_UPDATE_FINALIZE: write C = sums / counts (X, assign unused; no reseeding).
+ *   assign: int32[n] (in; rewritten for reseeded rows).  min_dist: float[n], required when
+ *     reseeding (the "farthest" key).  sums: double[K x d] accumulator.  counts:
+ *     int64[K] accumulator.  C: float[K x d] in (kept for clusters left empty) / out. */
+enum { HMOE_UPDATE_FULL = 0, HMOE_UPDATE_ACCUMULATE = 1, HMOE_UPDATE_FINALIZE = 2 };
+size_t hmoe_kmeans_update_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt);
+int hmoe_kmeans_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K,
+                       int32_t* assign, const float* min_dist, double* sums, int64_t* counts,
+                       float* C, int32_t mode, int32_t reseed_empty, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------ hard routing */
+
+/* Hard partition of a batch by expert (Section 2: each expert sees its own share of the
+ * data, no balancing): a stable counting sort.
+ *   expert: int32[n], 0 <= e < K (out-of-range ids are an error caught on the device:
+ *     counts then do not sum to n).
+ *   counts int32[K], offsets int32[K+1] (exclusive scan), perm int32[n] (slot -> sample),
+ *   inv int32[n] (sample -> slot).
+ *   rows [n x w] (dtype dt) and rows_sorted [n x w]: optional; when rows is non-NULL,
+ *   rows_sorted[p] = rows[perm[p]].  w must be a multiple of 8. */
+size_t hmoe_moe_dispatch_workspace(int64_t n, int32_t K);
+int hmoe_moe_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* counts,
+                      int32_t* offsets, int32_t* perm, int32_t* inv, const void* rows,
+                      void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/* Row gather out[r] = in[index[r]] for r < n (rows of w elements of dtype dt).  With
+ * index = inv it combines expert-ordered rows back to sample order; with perm it
+ * dispatches.  in and out must not overlap. */
+int hmoe_permute_rows(const void* in, void* out, const int32_t* index, int64_t n, int32_t w,
+                      hmoe_dtype_t dt, void* stream);
+
+/* ------------------------------------------------------------------ experts + decoder */
+
+/* Parameters of K expert MLPs and the shared decoder (Section 2, shared-decoder figure).
+ *   W1 [K][d_hid][d_in], b1 [K][d_hid], W2 [K][d_out][d_hid], b2 [K][d_out],
+ *   D [vocab][d_out], bD [vocab]; all in dtype dt; biases may be NULL (no bias). */
+typedef struct {
+  int32_t K, d_in, d_hid, d_out, vocab;
+  hmoe_dtype_t dt;
+  const void *W1, *b1, *W2, *b2, *D, *bD;
+} hmoe_moe_params_t;
+
+/* Multilabel targets as CSR: sample i has the distinct positive tags
+ * tag[row_ptr[i] .. row_ptr[i+1]) (at least one); the target puts mass 1/|P_i| on each
+ * (Section 4.1, Eq. 3, with the indicator spread uniformly over the positives). */
+typedef struct {
+  const int32_t* row_ptr; /* int32[n+1] */
+  const int32_t* tag;     /* int32[nnz], 0 <= tag < vocab */
+} hmoe_labels_t;
+
+/* Forward pass of the shared-decoder hard mixture with the loss of Eq. 3.
+ *   X_sorted [n x d_in]: samples in expert order (from hmoe_moe_dispatch), offsets int32[K+1],
+ *   perm int32[n] (slot -> sample).
+ *   H1_sorted [n x d_hid] out: relu(W1_e x + b1_e) in expert order (saved for backward).
+ *   H [n x d_out] out: expert outputs W2_e h1 + b2_e in SAMPLE order (the combine).
+ *   lse float[n] out: log-sum-exp of the V logits D H_i + bD.
+ *   loss float[n] out: lse_i - mean of the logits of the positive tags.
+ *   loss_mean float[1] out: mean over the batch. */
+size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n);
+int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
+                     const int32_t* offsets, const int32_t* perm, const hmoe_labels_t* y,
+                     void* H1_sorted, void* H, float* lse, float* loss, float* loss_mean,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Backward pass: gradients of loss_mean (the 1/n is included) with respect to every expert
+ * and decoder parameter, and optionally the input features.  The gater is fixed (Section
+ * 2.2), so nothing flows to the centres.  With p = softmax(D H_i + bD), y_i the target:
+ *   g = (p - y)/n; dbD = sum g; dD = g^T H; dH = g D; per expert e: db2 = sum dH,
+ *   dW2 = dH^T H1, dZ = (dH W2) * [H1 > 0]; db1 = sum dZ; dW1 = dZ^T X; dX = dZ W1.
+ *   Inputs are the forward's saved tensors (H1_sorted, H, lse) and inv int32[n].
+ *   dW1, db1, dW2, db2, dD, dbD: float out (overwritten; experts without samples get 0);
+ *   db1, db2, dbD may be NULL.  dX [n x d_in] in dtype dt, SAMPLE order, or NULL. */
+int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
+                      const int32_t* offsets, const int32_t* perm, const int32_t* inv,
+                      const hmoe_labels_t* y, const void* H1_sorted, const void* H,
+                      const float* lse, float* dW1, float* db1, float* dW2, float* db2,
+                      float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
+                      void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HMOE_H_ */

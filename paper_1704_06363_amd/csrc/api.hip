@@ -1,0 +1,277 @@
+// api.hip -- the extern "C" entry points of include/hmoe.h: argument validation, workspace
+// checks and dispatch to the launchers.  Host code only.
+#include <string.h>
+
+#include "launch.hpp"
+
+namespace hmoe {
+
+static thread_local char g_err[512];
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+void clear_error() { g_err[0] = 0; }
+
+static int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+static int check_dtype(hmoe_dtype_t dt) {
+  if (dt != HMOE_F32 && dt != HMOE_BF16) return fail(HMOE_EDTYPE, "unknown dtype %d", (int)dt);
+  return HMOE_OK;
+}
+
+static int check_width(const char* name, int64_t w) {
+  if (w <= 0 || w % 8 != 0) return fail(HMOE_ESHAPE, "%s = %lld must be a positive multiple of 8", name, (long long)w);
+  return HMOE_OK;
+}
+
+static int check_ptr(const char* name, const void* p, bool need_align = true) {
+  if (!p) return fail(HMOE_EINVAL, "%s is NULL", name);
+  if (need_align && !aligned16(p)) return fail(HMOE_ESHAPE, "%s is not 16-byte aligned", name);
+  return HMOE_OK;
+}
+
+static int check_k(int32_t K) {
+  if (K < 1 || K > 4096) return fail(HMOE_EINVAL, "K = %d outside [1, 4096]", K);
+  return HMOE_OK;
+}
+
+static int check_n(int64_t n) {
+  if (n < 0 || n >= (int64_t(1) << 31)) return fail(HMOE_EINVAL, "n = %lld outside [0, 2^31)", (long long)n);
+  return HMOE_OK;
+}
+
+static int check_ws(size_t need, size_t have, const void* ws) {
+  if (need > 0 && (have < need || ws == nullptr))
+    return fail(HMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", have, need);
+  return HMOE_OK;
+}
+
+}  // namespace hmoe
+
+using namespace hmoe;
+
+extern "C" {
+
+const char* hmoe_last_error(void) { return g_err; }
+
+int hmoe_version(void) { return HMOE_VERSION; }
+
+size_t hmoe_kmeans_assign_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt) {
+  (void)d;
+  (void)dt;
+  if (n < 0 || K < 1) return 0;
+  return assign_ws(n, K);
+}
+
+int hmoe_kmeans_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K,
+                       int32_t* assign, float* min_dist, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_k(K));
+  HMOE_TRY(check_width("d", d));
+  HMOE_TRY(check_ptr("C", C));
+  if (n > 0) {
+    HMOE_TRY(check_ptr("X", X));
+    HMOE_TRY(check_ptr("assign", assign, false));
+  }
+  HMOE_TRY(check_ws(assign_ws(n, K), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_assign(X, dt, n, d, C, K, assign, min_dist, w, (hipStream_t)stream);
+}
+
+size_t hmoe_kmeans_fit_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt) {
+  if (n < 0 || K < 1 || d < 1) return 0;
+  return fit_ws_bytes(n, d, K, dt);
+}
+
+int hmoe_kmeans_fit(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K, int32_t n_iter,
+                    const double* init_uniforms, int32_t reseed_empty, float* C, int32_t* assign, float* min_dist,
+                    int32_t* counts, double* objective, int32_t* init_idx, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_k(K));
+  HMOE_TRY(check_width("d", d));
+  if (n < K) return fail(HMOE_EINVAL, "k-means needs n >= K (n = %lld, K = %d)", (long long)n, K);
+  if (n_iter < 0) return fail(HMOE_EINVAL, "n_iter = %d is negative", n_iter);
+  HMOE_TRY(check_ptr("X", X));
+  HMOE_TRY(check_ptr("C", C));
+  HMOE_TRY(check_ptr("assign", assign, false));
+  HMOE_TRY(check_ws(fit_ws_bytes(n, d, K, dt), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_fit(X, dt, n, d, K, n_iter, init_uniforms, reseed_empty, C, assign, min_dist, counts, objective,
+                    init_idx, w, (hipStream_t)stream);
+}
+
+size_t hmoe_kmeans_update_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt) {
+  (void)dt;
+  if (n < 0 || K < 1 || d < 1) return 0;
+  return update_ws_bytes(n, d, K);
+}
+
+int hmoe_kmeans_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K, int32_t* assign,
+                       const float* min_dist, double* sums, int64_t* counts, float* C, int32_t mode,
+                       int32_t reseed_empty, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_k(K));
+  HMOE_TRY(check_width("d", d));
+  if (mode != HMOE_UPDATE_FULL && mode != HMOE_UPDATE_ACCUMULATE && mode != HMOE_UPDATE_FINALIZE)
+    return fail(HMOE_EINVAL, "unknown update mode %d", mode);
+  HMOE_TRY(check_ptr("sums", sums, false));
+  HMOE_TRY(check_ptr("counts", counts, false));
+  if (mode != HMOE_UPDATE_ACCUMULATE) HMOE_TRY(check_ptr("C", C, false));
+  if (mode != HMOE_UPDATE_FINALIZE && n > 0) {
+    HMOE_TRY(check_ptr("X", X));
+    HMOE_TRY(check_ptr("assign", assign, false));
+    if (mode == HMOE_UPDATE_FULL && reseed_empty) HMOE_TRY(check_ptr("min_dist", min_dist, false));
+  }
+  HMOE_TRY(check_ws(update_ws_bytes(n, d, K), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_update(X, dt, n, d, K, assign, min_dist, sums, counts, C, mode, reseed_empty, w,
+                       (hipStream_t)stream);
+}
+
+size_t hmoe_moe_dispatch_workspace(int64_t n, int32_t K) {
+  if (n < 0 || K < 1) return 0;
+  return dispatch_ws(n, K);
+}
+
+int hmoe_moe_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* counts, int32_t* offsets, int32_t* perm,
+                      int32_t* inv, const void* rows, void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* ws,
+                      size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_k(K));
+  HMOE_TRY(check_ptr("counts", counts, false));
+  HMOE_TRY(check_ptr("offsets", offsets, false));
+  if (n > 0) {
+    HMOE_TRY(check_ptr("expert", expert, false));
+    HMOE_TRY(check_ptr("perm", perm, false));
+    HMOE_TRY(check_ptr("inv", inv, false));
+  }
+  if (rows && n > 0) {
+    HMOE_TRY(check_dtype(dt));
+    HMOE_TRY(check_width("w", w));
+    HMOE_TRY(check_ptr("rows", rows));
+    HMOE_TRY(check_ptr("rows_sorted", rows_sorted));
+  }
+  HMOE_TRY(check_ws(dispatch_ws(n, K), ws_bytes, ws));
+  Workspace wsp(ws, ws_bytes);
+  hipStream_t st = (hipStream_t)stream;
+  HMOE_TRY(launch_dispatch(expert, n, K, counts, offsets, perm, inv, wsp, st));
+  if (rows && n > 0) HMOE_TRY(launch_permute(rows, rows_sorted, perm, n, w, dt, st));
+  return HMOE_OK;
+}
+
+int hmoe_permute_rows(const void* in, void* out, const int32_t* index, int64_t n, int32_t w, hmoe_dtype_t dt,
+                      void* stream) {
+  clear_error();
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_width("w", w));
+  if (n == 0) return HMOE_OK;
+  HMOE_TRY(check_ptr("in", in));
+  HMOE_TRY(check_ptr("out", out));
+  HMOE_TRY(check_ptr("index", index, false));
+  return launch_permute(in, out, index, n, w, dt, (hipStream_t)stream);
+}
+
+static int check_params(const hmoe_moe_params_t* p) {
+  if (!p) return fail(HMOE_EINVAL, "params is NULL");
+  HMOE_TRY(check_dtype(p->dt));
+  HMOE_TRY(check_k(p->K));
+  HMOE_TRY(check_width("d_in", p->d_in));
+  HMOE_TRY(check_width("d_hid", p->d_hid));
+  HMOE_TRY(check_width("d_out", p->d_out));
+  HMOE_TRY(check_width("vocab", p->vocab));
+  if ((int64_t)p->d_hid > 8192 || (int64_t)p->d_out > 8192)
+    return fail(HMOE_ESHAPE, "d_hid and d_out are limited to 8192");
+  HMOE_TRY(check_ptr("W1", p->W1));
+  HMOE_TRY(check_ptr("W2", p->W2));
+  HMOE_TRY(check_ptr("D", p->D));
+  return HMOE_OK;
+}
+
+size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n) {
+  if (!p || n < 0) return 0;
+  return moe_ws_bytes(p, n);
+}
+
+int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
+                     const int32_t* perm, const hmoe_labels_t* y, void* H1_sorted, void* H, float* lse, float* loss,
+                     float* loss_mean, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_params(p));
+  HMOE_TRY(check_n(n));
+  if (n == 0) return HMOE_OK;
+  HMOE_TRY(check_ptr("X_sorted", X_sorted));
+  HMOE_TRY(check_ptr("offsets", offsets, false));
+  HMOE_TRY(check_ptr("perm", perm, false));
+  if (!y) return fail(HMOE_EINVAL, "labels are NULL");
+  HMOE_TRY(check_ptr("labels.row_ptr", y->row_ptr, false));
+  HMOE_TRY(check_ptr("labels.tag", y->tag, false));
+  HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
+  HMOE_TRY(check_ptr("H", H));
+  HMOE_TRY(check_ptr("lse", lse, false));
+  HMOE_TRY(check_ptr("loss", loss, false));
+  HMOE_TRY(check_ptr("loss_mean", loss_mean, false));
+  HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_moe_forward(p, n, X_sorted, offsets, perm, y, H1_sorted, H, lse, loss, loss_mean, w,
+                            (hipStream_t)stream);
+}
+
+int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
+                      const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1_sorted,
+                      const void* H, const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD,
+                      float* dbD, void* dX, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_params(p));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_ptr("dW1", dW1, false));
+  HMOE_TRY(check_ptr("dW2", dW2, false));
+  HMOE_TRY(check_ptr("dD", dD, false));
+  if (n == 0) {
+    // empty batch: every gradient is zero
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t K = p->K, d = p->d_in, h = p->d_hid, o = p->d_out, V = p->vocab;
+    HMOE_TRY(hip_check(hipMemsetAsync(dW1, 0, sizeof(float) * K * h * d, st), "zero dW1"));
+    HMOE_TRY(hip_check(hipMemsetAsync(dW2, 0, sizeof(float) * K * o * h, st), "zero dW2"));
+    HMOE_TRY(hip_check(hipMemsetAsync(dD, 0, sizeof(float) * V * o, st), "zero dD"));
+    if (db1) HMOE_TRY(hip_check(hipMemsetAsync(db1, 0, sizeof(float) * K * h, st), "zero db1"));
+    if (db2) HMOE_TRY(hip_check(hipMemsetAsync(db2, 0, sizeof(float) * K * o, st), "zero db2"));
+    if (dbD) HMOE_TRY(hip_check(hipMemsetAsync(dbD, 0, sizeof(float) * V, st), "zero dbD"));
+    return HMOE_OK;
+  }
+  HMOE_TRY(check_ptr("X_sorted", X_sorted));
+  HMOE_TRY(check_ptr("offsets", offsets, false));
+  HMOE_TRY(check_ptr("perm", perm, false));
+  HMOE_TRY(check_ptr("inv", inv, false));
+  if (!y) return fail(HMOE_EINVAL, "labels are NULL");
+  HMOE_TRY(check_ptr("labels.row_ptr", y->row_ptr, false));
+  HMOE_TRY(check_ptr("labels.tag", y->tag, false));
+  HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
+  HMOE_TRY(check_ptr("H", H));
+  HMOE_TRY(check_ptr("lse", lse, false));
+  if (dX) HMOE_TRY(check_ptr("dX", dX));
+  HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_moe_backward(p, n, X_sorted, offsets, perm, inv, y, H1_sorted, H, lse, dW1, db1, dW2, db2, dD, dbD,
+                             dX, w, (hipStream_t)stream);
+}
+
+}  // extern "C"

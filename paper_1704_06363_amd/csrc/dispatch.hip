@@ -1,0 +1,235 @@
+// dispatch.hip -- hard routing: a stable counting sort of the batch by expert id (Section 2:
+// each expert gets its own share of the data), and row gathers for dispatch / combine.
+//
+// Three passes over the int32 ids, all fixed-size blocks of 1024 ids (4 waves x 4 chunks of
+// 64 lanes):
+//   hist    per-wave bucket counts via ballot-built peer masks (lanes with the same id),
+//           summed into block_counts[b][k];
+//   colscan per expert, exclusive prefix of block_counts over blocks -> counts[k];
+//   offsets exclusive scan of counts (one block);
+//   scatter recomputes the peer masks and writes each id's slot = offsets[k] + earlier blocks
+//           + earlier waves + earlier chunks + rank among earlier peer lanes: the order of
+//           equal ids is the sample order, so the permutation is unique.
+#include "launch.hpp"
+#include "primitives.hpp"
+
+namespace hmoe {
+
+constexpr int kIdsPerBlock = 1024;
+
+// Peer mask: the valid lanes whose id equals this lane's id (ids < 2^bits).
+__device__ __forceinline__ uint64_t peer_mask(int id, bool valid, int bits) {
+  uint64_t m = __ballot(valid);
+  for (int b = 0; b < bits; ++b) {
+    const bool bit = (id >> b) & 1;
+    const uint64_t on = __ballot(valid && bit);
+    m &= bit ? on : ~on;
+  }
+  return m;
+}
+
+__device__ __forceinline__ int lane_rank(uint64_t peers) {
+  const int l = threadIdx.x & 63;
+  const uint64_t lt = l == 0 ? 0ull : (~0ull >> (64 - l));
+  return __popcll(peers & lt);
+}
+
+__device__ __forceinline__ void wave_hist(const int32_t* __restrict__ e, int64_t n, int K, int bits,
+                                          int32_t* __restrict__ hist_w, int32_t* __restrict__ err) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int c = 0; c < 4; ++c) {
+    const int64_t i = (int64_t)blockIdx.x * kIdsPerBlock + w * 256 + c * 64 + l;
+    int id = i < n ? e[i] : -1;
+    bool valid = i < n;
+    if (valid && (id < 0 || id >= K)) {
+      if (err) atomicOr(err, 1);
+      valid = false;
+    }
+    const uint64_t peers = peer_mask(valid ? id : 0, valid, bits);
+    if (valid && lane_rank(peers) == 0) atomicAdd(&hist_w[id], (int32_t)__popcll(peers));
+  }
+}
+
+__global__ void __launch_bounds__(256) k_dispatch_hist(const int32_t* __restrict__ e, int64_t n, int K,
+                                                       int bits, int32_t* __restrict__ block_counts,
+                                                       int32_t* __restrict__ err) {
+  extern __shared__ int32_t hist[];  // [4][K]
+  for (int k = threadIdx.x; k < 4 * K; k += 256) hist[k] = 0;
+  __syncthreads();
+  wave_hist(e, n, K, bits, hist + (threadIdx.x >> 6) * K, err);
+  __syncthreads();
+  for (int k = threadIdx.x; k < K; k += 256)
+    block_counts[(int64_t)blockIdx.x * K + k] = hist[k] + hist[K + k] + hist[2 * K + k] + hist[3 * K + k];
+}
+
+__global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ block_counts, int nb, int K,
+                                                          int32_t* __restrict__ counts) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= K) return;
+  int32_t run = 0;
+  for (int b = 0; b < nb; ++b) {
+    const int32_t t = block_counts[(int64_t)b * K + k];
+    block_counts[(int64_t)b * K + k] = run;
+    run += t;
+  }
+  counts[k] = run;
+}
+
+__global__ void __launch_bounds__(1024) k_dispatch_offsets(const int32_t* __restrict__ counts, int K,
+                                                           int32_t* __restrict__ offsets) {
+  __shared__ int32_t sh[17];
+  const int per = (K + 1023) / 1024;
+  const int k0 = threadIdx.x * per;
+  int32_t s = 0;
+  for (int q = 0; q < per; ++q)
+    if (k0 + q < K) s += counts[k0 + q];
+  int32_t total;
+  int32_t ex = block_excl_scan<int32_t>(s, sh, &total);
+  for (int q = 0; q < per; ++q)
+    if (k0 + q < K) {
+      offsets[k0 + q] = ex;
+      ex += counts[k0 + q];
+    }
+  if (threadIdx.x == 0) offsets[K] = total;
+}
+
+__global__ void __launch_bounds__(256) k_dispatch_scatter(const int32_t* __restrict__ e, int64_t n, int K,
+                                                          int bits, const int32_t* __restrict__ block_base,
+                                                          const int32_t* __restrict__ offsets,
+                                                          int32_t* __restrict__ perm,
+                                                          int32_t* __restrict__ inv) {
+  extern __shared__ int32_t hist[];  // [4][K] -> per-wave running slot
+  for (int k = threadIdx.x; k < 4 * K; k += 256) hist[k] = 0;
+  __syncthreads();
+  const int w = threadIdx.x >> 6;
+  wave_hist(e, n, K, bits, hist + w * K, nullptr);
+  __syncthreads();
+  for (int k = threadIdx.x; k < K; k += 256) {
+    int32_t run = offsets[k] + block_base[(int64_t)blockIdx.x * K + k];
+    for (int q = 0; q < 4; ++q) {
+      const int32_t t = hist[q * K + k];
+      hist[q * K + k] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  int32_t* slot_w = hist + w * K;
+  const int l = threadIdx.x & 63;
+  for (int c = 0; c < 4; ++c) {
+    const int64_t i = (int64_t)blockIdx.x * kIdsPerBlock + w * 256 + c * 64 + l;
+    int id = i < n ? e[i] : -1;
+    const bool valid = i < n && id >= 0 && id < K;
+    const uint64_t peers = peer_mask(valid ? id : 0, valid, bits);
+    if (valid) {
+      const int rank = lane_rank(peers);
+      const int32_t slot = slot_w[id] + rank;
+      perm[slot] = (int32_t)i;
+      inv[i] = slot;
+      // every peer has read slot_w[id] above (same wave, program order) before the leader
+      // advances it for the next chunk
+      if (rank == 0) atomicAdd(&slot_w[id], (int32_t)__popcll(peers));
+    } else if (i < n) {
+      inv[i] = -1;
+    }
+  }
+}
+
+static int id_bits(int K) {
+  int b = 0;
+  while ((1 << b) < K) ++b;
+  return b;
+}
+
+size_t dispatch_ws(int64_t n, int32_t K) {
+  Workspace ws(nullptr, 0);
+  const int64_t nb = cdiv(n, kIdsPerBlock);
+  ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * K);
+  return ws.off;
+}
+
+int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int32_t* offsets,
+                    int32_t* perm, int32_t* inv, Workspace& ws, hipStream_t st) {
+  const int64_t nb = cdiv(n, kIdsPerBlock);
+  int32_t* bc = ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * K);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  const int bits = id_bits(K);
+  const size_t lds = 4 * (size_t)K * sizeof(int32_t);
+  if (nb > 0) {
+    hipLaunchKernelGGL(k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
+                       (int32_t*)nullptr);
+    HMOE_TRY(launch_check("dispatch hist"));
+  }
+  hipLaunchKernelGGL(k_dispatch_colscan, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, bc, (int)nb, K,
+                     counts);
+  HMOE_TRY(launch_check("dispatch colscan"));
+  hipLaunchKernelGGL(k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
+  HMOE_TRY(launch_check("dispatch offsets"));
+  if (nb > 0) {
+    hipLaunchKernelGGL(k_dispatch_scatter, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
+                       offsets, perm, inv);
+    HMOE_TRY(launch_check("dispatch scatter"));
+  }
+  return HMOE_OK;
+}
+
+int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, int32_t w, hmoe_dtype_t dt,
+                   hipStream_t st) {
+  if (n == 0) return HMOE_OK;
+  const int vpr = (int)(w * dtype_size(dt) / 16);
+  const int64_t total = n * vpr;
+  int64_t grid = cdiv(total, 256);
+  if (grid > 8192) grid = 8192;
+  hipLaunchKernelGGL(k_permute_rows, dim3((unsigned)grid), dim3(256), 0, st, (const i32x4*)in, (i32x4*)out,
+                     index, n, vpr);
+  return launch_check("permute rows");
+}
+
+int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st) {
+  hipLaunchKernelGGL(k_seg_tiles, dim3(1), dim3(1024), 0, st, seg, G, tile, tile_start);
+  return launch_check("segment tiles");
+}
+
+template <typename T, typename O>
+int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* seg, int G, int w,
+                  int64_t n, O* out, int accumulate, Workspace& ws, hipStream_t st) {
+  const int64_t pieces = cdiv(n, kSegPiece) + G;
+  int32_t* ts = ws.take<int32_t>(G + 1);
+  double* part = ws.take<double>((size_t)pieces * w);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  HMOE_TRY(launch_seg_tiles(seg, G, kSegPiece, ts, st));
+  hipLaunchKernelGGL(k_segsum_partial<T>, dim3((unsigned)pieces), dim3(256), 0, st, X, ld, rowmap, seg, ts, G,
+                     w, part);
+  HMOE_TRY(launch_check("segsum partial"));
+  hipLaunchKernelGGL(k_segsum_final<O>, dim3((unsigned)cdiv((int64_t)G * w, 256)), dim3(256), 0, st, part,
+                     ts, G, w, out, accumulate);
+  return launch_check("segsum final");
+}
+
+size_t segsum_ws(int64_t n, int G, int w) {
+  Workspace ws(nullptr, 0);
+  ws.take<int32_t>(G + 1);
+  ws.take<double>((size_t)(cdiv(n, kSegPiece) + G) * w);
+  return ws.off;
+}
+
+template int launch_segsum<float, double>(const float*, int64_t, const int32_t*, const int32_t*, int, int,
+                                          int64_t, double*, int, Workspace&, hipStream_t);
+template int launch_segsum<bf16, double>(const bf16*, int64_t, const int32_t*, const int32_t*, int, int,
+                                         int64_t, double*, int, Workspace&, hipStream_t);
+template int launch_segsum<float, float>(const float*, int64_t, const int32_t*, const int32_t*, int, int,
+                                         int64_t, float*, int, Workspace&, hipStream_t);
+template int launch_segsum<bf16, float>(const bf16*, int64_t, const int32_t*, const int32_t*, int, int,
+                                        int64_t, float*, int, Workspace&, hipStream_t);
+
+int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, float* out_f32, Workspace& ws,
+                   hipStream_t st) {
+  double* part = ws.take<double>(kSumBlocks);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  hipLaunchKernelGGL(k_sum_partial<float>, dim3(kSumBlocks), dim3(256), 0, st, x, n, part);
+  HMOE_TRY(launch_check("sum partial"));
+  if (out_f64) hipLaunchKernelGGL(k_sum_final<double>, dim3(1), dim3(64), 0, st, part, scale, out_f64);
+  if (out_f32) hipLaunchKernelGGL(k_sum_final<float>, dim3(1), dim3(64), 0, st, part, scale, out_f32);
+  return launch_check("sum final");
+}
+
+}  // namespace hmoe

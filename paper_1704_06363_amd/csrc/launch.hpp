@@ -1,0 +1,48 @@
+// launch.hpp -- launchers implemented in the .hip translation units and called by api.cpp.
+// All of them only enqueue work on `st`; sizes have been validated by the caller.
+#pragma once
+#include "host.hpp"
+
+namespace hmoe {
+
+typedef __bf16 bf16;
+
+// dispatch.hip
+size_t dispatch_ws(int64_t n, int32_t K);
+int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int32_t* offsets,
+                    int32_t* perm, int32_t* inv, Workspace& ws, hipStream_t st);
+int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, int32_t w,
+                   hmoe_dtype_t dt, hipStream_t st);
+int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st);
+size_t segsum_ws(int64_t n, int G, int w);
+template <typename T, typename O>
+int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* seg, int G, int w,
+                  int64_t n, O* out, int accumulate, Workspace& ws, hipStream_t st);
+int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, float* out_f32,
+                   Workspace& ws, hipStream_t st);
+
+// kmeans.hip
+size_t assign_ws(int64_t n, int32_t K);
+size_t fit_ws_bytes(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt);
+size_t update_ws_bytes(int64_t n, int32_t d, int32_t K);
+int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K,
+                  int32_t* assign, float* min_dist, Workspace& ws, hipStream_t st);
+int launch_fit(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K, int32_t n_iter,
+               const double* u, int32_t reseed, float* C, int32_t* assign, float* min_dist,
+               int32_t* counts, double* objective, int32_t* init_idx, Workspace& ws, hipStream_t st);
+int launch_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t K, int32_t* assign,
+                  const float* min_dist, double* sums, int64_t* counts, float* C, int32_t mode,
+                  int32_t reseed, Workspace& ws, hipStream_t st);
+
+// moe.hip
+size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n);
+int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
+                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, float* lse,
+                       float* loss, float* loss_mean, Workspace& ws, hipStream_t st);
+int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
+                        const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y,
+                        const void* H1s, const void* H, const float* lse, float* dW1, float* db1,
+                        float* dW2, float* db2, float* dD, float* dbD, void* dX, Workspace& ws,
+                        hipStream_t st);
+
+}  // namespace hmoe

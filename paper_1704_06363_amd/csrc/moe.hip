@@ -1,0 +1,497 @@
+// moe.hip -- hard-routed expert evaluation with a shared decoder (Section 2, shared-decoder
+// figure) and the multilabel softmax loss (Section 4.1, Eq. 3), forward and backward.
+//
+// Rows arrive grouped by expert (X_sorted, offsets).  Every contraction runs on the MFMA tile
+// engine of gemm.hpp:
+//   experts, forward     row-grouped NT GEMMs (bias + ReLU epilogue; the second layer's
+//                        epilogue writes rows straight back to sample order = the combine)
+//   decoder, forward     NT GEMM H . D^T with a per-row (max, sum exp) epilogue; the V logits
+//                        are never stored; a merge pass forms lse and the loss
+//   decoder, backward    the logits are recomputed and turned into g = (p - y)/n (stored) with
+//                        per-tile column sums for dbD; then dH = g D (epilogue scatters rows to
+//                        expert order) and dD = g^T H
+//   experts, backward    reduction-grouped TN GEMMs for dW (empty experts give exact zeros),
+//                        row-grouped NN GEMMs for dH1 (ReLU mask epilogue) and dX (epilogue
+//                        scatters rows back to sample order); bias gradients are deterministic
+//                        segmented column sums.
+#include <float.h>
+
+#include "gemm.hpp"
+#include "launch.hpp"
+#include "primitives.hpp"
+
+namespace hmoe {
+
+// ------------------------------------------------------------------ expert forward
+
+// LAYER 1: H1s[m] = relu(Xs[m] W1_e^T + b1_e).   LAYER 2: H[perm[m]] = H1s[m] W2_e^T + b2_e.
+template <typename T, int LAYER>
+__global__ void __launch_bounds__(256, 2)
+    k_expert_fwd(const T* __restrict__ A, const T* __restrict__ W, const T* __restrict__ bias,
+                 const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
+                 const int32_t* __restrict__ perm, T* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_group_m(seg, tile_start, G, N, Kd);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, true, true>(A + tc.m0 * Kd, Kd, tc.m_rows, W + ((int64_t)tc.group * N + tc.n0) * Kd, Kd,
+                           tc.n_cols, Kd, smem, acc);
+  const Frag f;
+  const T* be = bias ? bias + (int64_t)tc.group * N : nullptr;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) continue;
+      const int64_t m = tc.m0 + row;
+      const int64_t orow = LAYER == 1 ? m : (int64_t)perm[m];
+      T* dst = out + orow * N + tc.n0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        if (col >= tc.n_cols) continue;
+        float v = acc[i][j][r] + (be ? to_f32(be[tc.n0 + col]) : 0.f);
+        if (LAYER == 1) v = fmaxf(v, 0.f);
+        dst[col] = from_f32<T>(v);
+      }
+    }
+}
+
+// ------------------------------------------------------------------ decoder forward
+
+// Per row and V-tile: m = max of the tile's logits, s = sum exp(logit - m).
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+    k_dec_fwd(const T* __restrict__ H, const T* __restrict__ D, const T* __restrict__ bD, int64_t n, int V, int o,
+              float* __restrict__ pm, float* __restrict__ ps) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_plain(n, V, o);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+  const Frag f;
+  float bias[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = f.col(j);
+    bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
+  }
+  float* rm = reinterpret_cast<float*>(smem);  // [2][128]
+  float* rs = rm + 256;                          // [2][128]
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v[4];
+      float mx = -FLT_MAX;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[j] = acc[i][j][r] + bias[j];
+        if (f.col(j) < tc.n_cols) mx = fmaxf(mx, v[j]);
+      }
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (f.col(j) < tc.n_cols) s += __expf(v[j] - mx);
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
+      if (f.lr == 0) {
+        rm[f.wn * 128 + f.row(i, r)] = mx;
+        rs[f.wn * 128 + f.row(i, r)] = s;
+      }
+    }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < tc.m_rows) {
+    float m0 = rm[t], s0 = rs[t];
+    const float m1 = rm[128 + t], s1 = rs[128 + t];
+    const float M = fmaxf(m0, m1);
+    const float S = s0 * __expf(m0 - M) + s1 * __expf(m1 - M);
+    const int64_t at = (int64_t)(tc.n0 / kBN) * n + tc.m0 + t;
+    pm[at] = M;
+    ps[at] = S;
+  }
+}
+
+// lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row.
+template <typename T>
+__global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, const float* __restrict__ ps,
+                                                  int nt, const T* __restrict__ H, const T* __restrict__ D,
+                                                  const T* __restrict__ bD, int64_t n, int o,
+                                                  const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag,
+                                                  float* __restrict__ lse, float* __restrict__ loss) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
+  if (row >= n) return;
+  float M = -FLT_MAX;
+  for (int t = l; t < nt; t += 64) M = fmaxf(M, pm[(int64_t)t * n + row]);
+  M = wave_max(M);
+  float S = 0.f;
+  for (int t = l; t < nt; t += 64) S += ps[(int64_t)t * n + row] * __expf(pm[(int64_t)t * n + row] - M);
+  S = wave_sum(S);
+  const float L = M + __logf(S);
+  const int32_t p0 = row_ptr[row], p1 = row_ptr[row + 1];
+  const T* h = H + row * o;
+  float pos = 0.f;
+  for (int32_t q = p0; q < p1; ++q) {
+    const int32_t tg = tag[q];
+    const T* dv = D + (int64_t)tg * o;
+    float s = 0.f;
+    for (int j = l; j < o; j += 64) s += to_f32(h[j]) * to_f32(dv[j]);
+    s = wave_sum(s);
+    pos += s + (bD ? to_f32(bD[tg]) : 0.f);
+  }
+  if (l == 0) {
+    lse[row] = L;
+    loss[row] = L - pos / (float)(p1 - p0);
+  }
+}
+
+// ------------------------------------------------------------------ decoder backward
+
+// g = (exp(logit - lse) - y) / n stored to G; per-tile column sums of g to part_db[mtile][V].
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+    k_dec_grad(const T* __restrict__ H, const T* __restrict__ D, const T* __restrict__ bD, int64_t n, int V, int o,
+               const float* __restrict__ lse, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag,
+               float inv_n, T* __restrict__ G, float* __restrict__ part_db) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_plain(n, V, o);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+  const Frag f;
+  float bias[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = f.col(j);
+    bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
+  }
+  const int wcol0 = tc.n0 + f.wn * 64;  // first column of this wave
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j][r] = 0.f;
+        continue;
+      }
+      const int64_t gr = tc.m0 + row;
+      const float L = lse[gr];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - L);
+      const int32_t p0 = row_ptr[gr], p1 = row_ptr[gr + 1];
+      const float y = 1.f / (float)(p1 - p0);
+      for (int32_t q = p0; q < p1; ++q) {
+        const int lc = tag[q] - wcol0;
+        if (lc >= 0 && lc < 64 && (lc & 15) == f.lr) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if ((lc >> 4) == j) acc[i][j][r] -= y;
+        }
+      }
+      T* dst = G + gr * V + tc.n0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        acc[i][j][r] *= inv_n;
+        if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
+      }
+    }
+  // column sums over this tile's rows: lanes of one column group, then the two row waves
+  float* cs = reinterpret_cast<float*>(smem);  // [2][128]
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s += acc[i][j][r];
+    s += shfl_xor(s, 16);
+    s += shfl_xor(s, 32);
+    if (f.lg == 0) cs[f.wm * 128 + f.col(j)] = s;
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < tc.n_cols) part_db[(tc.m0 / kBM) * (int64_t)V + tc.n0 + t] = cs[t] + cs[128 + t];
+}
+
+__global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int rows, int V,
+                                                      float* __restrict__ out) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= V) return;
+  float s = 0.f;
+  for (int q = 0; q < rows; ++q) s += part[(int64_t)q * V + c];
+  out[c] = s;
+}
+
+// dH = G D, written to expert order: dYs[inv[i]] = (G D)[i].
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+    k_dec_dH(const T* __restrict__ G, const T* __restrict__ D, int64_t n, int V, int o,
+             const int32_t* __restrict__ inv, T* __restrict__ dYs) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_plain(n, o, V);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
+  const Frag f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) continue;
+      T* dst = dYs + (int64_t)inv[tc.m0 + row] * o + tc.n0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
+      }
+    }
+}
+
+// dD = G^T H (fp32).
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+    k_dec_dD(const T* __restrict__ G, const T* __restrict__ H, int64_t n, int V, int o, float* __restrict__ dD) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_plain(V, o, (int)n);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
+  const Frag f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) continue;
+      float* dst = dD + (tc.m0 + row) * o + tc.n0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        if (col < tc.n_cols) dst[col] = acc[i][j][r];
+      }
+    }
+}
+
+// ------------------------------------------------------------------ expert backward
+
+// dW_e = A_e^T B_e over the rows of expert e (reduction-grouped; an empty expert writes zeros).
+//   A: [rows][M] (ld M), B: [rows][N] (ld N), out: [G][M][N] fp32.
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+    k_expert_wgrad(const T* __restrict__ A, const T* __restrict__ B, const int32_t* __restrict__ seg, int G, int M,
+                   int N, float* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_group_k(seg, G, M, N);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
+                             smem, acc);
+  const Frag f;
+  float* base = out + (int64_t)tc.group * M * N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) continue;
+      float* dst = base + (tc.m0 + row) * N + tc.n0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        if (col < tc.n_cols) dst[col] = acc[i][j][r];
+      }
+    }
+}
+
+// Row-grouped input gradients.  MASK: dZ[m] = (dYs[m] W2_e) * [H1s[m] > 0], stored in expert
+// order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order.
+//   A: [rows][Kd] (ld Kd), W: [G][Kd][N] (the layer's [out][in] weights seen as [K][N]).
+template <typename T, bool MASK>
+__global__ void __launch_bounds__(256, 2)
+    k_expert_dgrad(const T* __restrict__ A, const T* __restrict__ W, const int32_t* __restrict__ seg,
+                   const int32_t* __restrict__ tile_start, int G, int N, int Kd, const T* __restrict__ H1s,
+                   const int32_t* __restrict__ perm, T* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const TileCoord tc = tile_group_m(seg, tile_start, G, N, Kd);
+  if (!tc.valid) return;
+  floatx4 acc[4][4];
+  gemm_tile<T, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
+                            Kd, smem, acc);
+  const Frag f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = f.row(i, r);
+      if (row >= tc.m_rows) continue;
+      const int64_t m = tc.m0 + row;
+      const int64_t orow = MASK ? m : (int64_t)perm[m];
+      T* dst = out + orow * N + tc.n0;
+      const T* hm = MASK ? H1s + m * N + tc.n0 : nullptr;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = f.col(j);
+        if (col >= tc.n_cols) continue;
+        float v = acc[i][j][r];
+        if (MASK && !(to_f32(hm[col]) > 0.f)) v = 0.f;
+        dst[col] = from_f32<T>(v);
+      }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+
+struct MoeShape {
+  int64_t n;
+  int K, d, h, o, V;
+  size_t es;
+};
+
+static MoeShape shape_of(const hmoe_moe_params_t* p, int64_t n) {
+  return MoeShape{n, p->K, p->d_in, p->d_hid, p->d_out, p->vocab, dtype_size(p->dt)};
+}
+
+static size_t fwd_ws(const MoeShape& s) {
+  Workspace ws(nullptr, 0);
+  const int64_t ntv = cdiv(s.V, kBN);
+  ws.take<int32_t>(s.K + 1);
+  ws.take<float>((size_t)ntv * s.n);
+  ws.take<float>((size_t)ntv * s.n);
+  ws.take<double>(kSumBlocks);
+  return ws.off;
+}
+
+static size_t bwd_ws(const MoeShape& s) {
+  Workspace ws(nullptr, 0);
+  ws.take<int32_t>(s.K + 1);
+  ws.take<char>((size_t)s.n * s.V * s.es);
+  ws.take<char>((size_t)s.n * s.o * s.es);
+  ws.take<char>((size_t)s.n * s.h * s.es);
+  ws.take<float>((size_t)cdiv(s.n, kBM) * s.V);
+  const int w = s.h > s.o ? s.h : s.o;
+  return ws.off + segsum_ws(s.n, s.K, w) + 256;
+}
+
+size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n) {
+  const MoeShape s = shape_of(p, n);
+  const size_t a = fwd_ws(s), b = bwd_ws(s);
+  return a > b ? a : b;
+}
+
+template <typename T>
+static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
+                     const hmoe_labels_t* y, T* H1s, T* H, float* lse, float* loss, float* loss_mean, Workspace& ws,
+                     hipStream_t st) {
+  const MoeShape s = shape_of(p, n);
+  const int ntv = (int)cdiv(s.V, kBN);
+  int32_t* ts = ws.take<int32_t>(s.K + 1);
+  float* pm = ws.take<float>((size_t)ntv * n);
+  float* ps = ws.take<float>((size_t)ntv * n);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  const T* W1 = (const T*)p->W1;
+  const T* W2 = (const T*)p->W2;
+  const T* D = (const T*)p->D;
+  HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
+  const int64_t mt_bound = cdiv(n, kBM) + s.K;
+  hipLaunchKernelGGL((k_expert_fwd<T, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds, st,
+                     Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
+  HMOE_TRY(launch_check("expert layer 1"));
+  hipLaunchKernelGGL((k_expert_fwd<T, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
+                     (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
+  HMOE_TRY(launch_check("expert layer 2"));
+  hipLaunchKernelGGL(k_dec_fwd<T>, dim3((unsigned)(cdiv(n, kBM) * ntv)), dim3(kThreads), kGemmLds, st, (const T*)H, D,
+                     (const T*)p->bD, n, s.V, s.o, pm, ps);
+  HMOE_TRY(launch_check("decoder forward"));
+  hipLaunchKernelGGL(k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
+                     (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
+  HMOE_TRY(launch_check("decoder loss"));
+  return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
+}
+
+template <typename T>
+static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
+                      const int32_t* inv, const hmoe_labels_t* y, const T* H1s, const T* H, const float* lse,
+                      float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX, Workspace& ws,
+                      hipStream_t st) {
+  const MoeShape s = shape_of(p, n);
+  int32_t* ts = ws.take<int32_t>(s.K + 1);
+  T* G = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.V * sizeof(T)));
+  T* dYs = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.o * sizeof(T)));
+  T* dZ = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.h * sizeof(T)));
+  const int mt = (int)cdiv(n, kBM);
+  float* pdb = ws.take<float>((size_t)mt * s.V);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  const T* W1 = (const T*)p->W1;
+  const T* W2 = (const T*)p->W2;
+  const T* D = (const T*)p->D;
+  const int ntv = (int)cdiv(s.V, kBN);
+  // decoder
+  hipLaunchKernelGGL(k_dec_grad<T>, dim3((unsigned)(mt * ntv)), dim3(kThreads), kGemmLds, st, H, D, (const T*)p->bD, n,
+                     s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
+  HMOE_TRY(launch_check("decoder grad"));
+  if (dbD) {
+    hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V, dbD);
+    HMOE_TRY(launch_check("decoder bias grad"));
+  }
+  hipLaunchKernelGGL(k_dec_dH<T>, dim3((unsigned)(mt * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st, (const T*)G, D,
+                     n, s.V, s.o, inv, dYs);
+  HMOE_TRY(launch_check("decoder dH"));
+  hipLaunchKernelGGL(k_dec_dD<T>, dim3((unsigned)(cdiv(s.V, kBM) * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
+                     (const T*)G, H, n, s.V, s.o, dD);
+  HMOE_TRY(launch_check("decoder dD"));
+  // experts
+  HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
+  const size_t mark = ws.off;
+  if (db2) HMOE_TRY(launch_segsum<T, float>(dYs, s.o, nullptr, offsets, s.K, s.o, n, db2, 0, ws, st));
+  ws.off = mark;
+  hipLaunchKernelGGL(k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, kBM) * cdiv(s.h, kBN))),
+                     dim3(kThreads), kGemmLds, st, (const T*)dYs, H1s, offsets, s.K, s.o, s.h, dW2);
+  HMOE_TRY(launch_check("expert dW2"));
+  const int64_t mt_bound = cdiv(n, kBM) + s.K;
+  hipLaunchKernelGGL((k_expert_dgrad<T, true>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds,
+                     st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
+  HMOE_TRY(launch_check("expert dH1"));
+  if (db1) HMOE_TRY(launch_segsum<T, float>(dZ, s.h, nullptr, offsets, s.K, s.h, n, db1, 0, ws, st));
+  ws.off = mark;
+  hipLaunchKernelGGL(k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, kBM) * cdiv(s.d, kBN))),
+                     dim3(kThreads), kGemmLds, st, (const T*)dZ, Xs, offsets, s.K, s.h, s.d, dW1);
+  HMOE_TRY(launch_check("expert dW1"));
+  if (dX) {
+    hipLaunchKernelGGL((k_expert_dgrad<T, false>), dim3((unsigned)(mt_bound * cdiv(s.d, kBN))), dim3(kThreads),
+                       kGemmLds, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm, dX);
+    HMOE_TRY(launch_check("expert dX"));
+  }
+  return HMOE_OK;
+}
+
+int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
+                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, float* lse, float* loss,
+                       float* loss_mean, Workspace& ws, hipStream_t st) {
+  if (p->dt == HMOE_BF16)
+    return forward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, y, (bf16*)H1s, (bf16*)H, lse, loss, loss_mean, ws,
+                           st);
+  return forward_t<float>(p, n, (const float*)Xs, offsets, perm, y, (float*)H1s, (float*)H, lse, loss, loss_mean, ws,
+                          st);
+}
+
+int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
+                        const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1s,
+                        const void* H, const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD,
+                        float* dbD, void* dX, Workspace& ws, hipStream_t st) {
+  if (p->dt == HMOE_BF16)
+    return backward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, inv, y, (const bf16*)H1s, (const bf16*)H, lse, dW1,
+                            db1, dW2, db2, dD, dbD, (bf16*)dX, ws, st);
+  return backward_t<float>(p, n, (const float*)Xs, offsets, perm, inv, y, (const float*)H1s, (const float*)H, lse, dW1,
+                           db1, dW2, db2, dD, dbD, (float*)dX, ws, st);
+}
+
+}  // namespace hmoe

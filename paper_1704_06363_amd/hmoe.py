@@ -1,0 +1,303 @@
+"""Python binding of libhmoe.so (include/hmoe.h): argument marshalling only.
+
+Tensors are torch tensors on the GPU; every function hands their device pointers, the
+current HIP stream and a workspace to the C ABI and returns the output tensors.  No step of
+the hot path runs here: if the library is not built, or a call fails, an exception is
+raised -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhmoe.so")
+
+F32, BF16 = 0, 1
+UPDATE_FULL, UPDATE_ACCUMULATE, UPDATE_FINALIZE = 0, 1, 2
+_DT = {torch.float32: F32, torch.bfloat16: BF16}
+
+SYMBOLS = (
+    "hmoe_last_error", "hmoe_version",
+    "hmoe_kmeans_assign_workspace", "hmoe_kmeans_assign",
+    "hmoe_kmeans_fit_workspace", "hmoe_kmeans_fit",
+    "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
+    "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
+    "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
+)
+
+
+class HmoeError(RuntimeError):
+    pass
+
+
+class MoeParams(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("d_in", ctypes.c_int32), ("d_hid", ctypes.c_int32),
+                ("d_out", ctypes.c_int32), ("vocab", ctypes.c_int32), ("dt", ctypes.c_int),
+                ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("W2", ctypes.c_void_p),
+                ("b2", ctypes.c_void_p), ("D", ctypes.c_void_p), ("bD", ctypes.c_void_p)]
+
+
+class Labels(ctypes.Structure):
+    _fields_ = [("row_ptr", ctypes.c_void_p), ("tag", ctypes.c_void_p)]
+
+
+_lib = None
+
+_c = ctypes
+_I64, _I32, _SZ, _P, _D = _c.c_int64, _c.c_int32, _c.c_size_t, _c.c_void_p, _c.c_double
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise HmoeError("libhmoe.so is not built: run `python -m paper_1704_06363_amd.build` "
+                            "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        L.hmoe_last_error.restype = _c.c_char_p
+        L.hmoe_version.restype = _c.c_int
+        for name in ("hmoe_kmeans_assign_workspace", "hmoe_kmeans_fit_workspace",
+                     "hmoe_kmeans_update_workspace"):
+            getattr(L, name).restype = _SZ
+            getattr(L, name).argtypes = [_I64, _I32, _I32, _c.c_int]
+        L.hmoe_moe_dispatch_workspace.restype = _SZ
+        L.hmoe_moe_dispatch_workspace.argtypes = [_I64, _I32]
+        L.hmoe_moe_workspace.restype = _SZ
+        L.hmoe_moe_workspace.argtypes = [_c.POINTER(MoeParams), _I64]
+        L.hmoe_kmeans_assign.argtypes = [_P, _c.c_int, _I64, _I32, _P, _I32, _P, _P, _P, _SZ, _P]
+        L.hmoe_kmeans_fit.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _I32, _P, _I32, _P, _P, _P,
+                                      _P, _P, _P, _P, _SZ, _P]
+        L.hmoe_kmeans_update.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _P, _P, _P, _P, _P,
+                                         _I32, _I32, _P, _SZ, _P]
+        L.hmoe_moe_dispatch.argtypes = [_P, _I64, _I32, _P, _P, _P, _P, _P, _P, _c.c_int, _I32,
+                                        _P, _SZ, _P]
+        L.hmoe_permute_rows.argtypes = [_P, _P, _P, _I64, _I32, _c.c_int, _P]
+        L.hmoe_moe_forward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P,
+                                       _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _SZ, _P]
+        L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
+                                        _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                        _P, _P, _SZ, _P]
+        for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
+                     "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
+                     "hmoe_moe_backward"):
+            getattr(L, name).restype = _c.c_int
+        _lib = L
+    return _lib
+
+
+def version() -> int:
+    return lib().hmoe_version()
+
+
+def last_error() -> str:
+    return lib().hmoe_last_error().decode()
+
+
+def _chk(rc: int, what: str):
+    if rc != 0:
+        raise HmoeError(f"{what} failed ({rc}): {last_error()}")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise HmoeError("tensor is not on the GPU")
+    if not t.is_contiguous():
+        raise HmoeError("tensor is not contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dt(t):
+    try:
+        return _DT[t.dtype]
+    except KeyError:
+        raise HmoeError(f"unsupported dtype {t.dtype}") from None
+
+
+def _workspace(nbytes, ws, device):
+    if nbytes == 0:
+        return None, 0
+    if ws is not None:
+        if ws.numel() * ws.element_size() < nbytes:
+            raise HmoeError(f"workspace of {ws.numel() * ws.element_size()} bytes, {nbytes} needed")
+        return ws, ws.numel() * ws.element_size()
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+# ------------------------------------------------------------------ gater
+
+def kmeans_assign_workspace(n, d, K, dtype) -> int:
+    return lib().hmoe_kmeans_assign_workspace(n, d, K, _DT[dtype])
+
+
+def kmeans_assign(X, C, assign=None, min_dist=None, want_min_dist=True, ws=None):
+    """Eq. 2: nearest centroid per row (ties to the lowest index) and its squared distance."""
+    n, d = X.shape
+    K = C.shape[0]
+    dev = X.device
+    if assign is None:
+        assign = torch.empty(n, dtype=torch.int32, device=dev)
+    if min_dist is None and want_min_dist:
+        min_dist = torch.empty(n, dtype=torch.float32, device=dev)
+    w, wb = _workspace(kmeans_assign_workspace(n, d, K, X.dtype), ws, dev)
+    _chk(lib().hmoe_kmeans_assign(_ptr(X), _dt(X), n, d, _ptr(C), K, _ptr(assign), _ptr(min_dist),
+                                  _ptr(w), wb, _stream()), "kmeans_assign")
+    return assign, min_dist
+
+
+def kmeans_fit_workspace(n, d, K, dtype) -> int:
+    return lib().hmoe_kmeans_fit_workspace(n, d, K, _DT[dtype])
+
+
+def kmeans_fit(X, K, n_iter, init_uniforms=None, C=None, reseed=True, ws=None):
+    """Lloyd's K-means for n_iter iterations, k-means++ seeded from init_uniforms (K values in
+    [0,1)) or started from C.  Returns C (fp32), assign, min_dist, counts, objective,
+    init_idx."""
+    n, d = X.shape
+    dev = X.device
+    if (init_uniforms is None) == (C is None):
+        raise HmoeError("give exactly one of init_uniforms or C")
+    Cout = torch.empty(K, d, dtype=torch.float32, device=dev) if C is None else C.clone()
+    u = None
+    if init_uniforms is not None:
+        u = torch.as_tensor(init_uniforms, dtype=torch.float64).to(dev).contiguous()
+    out = {"C": Cout,
+           "assign": torch.empty(n, dtype=torch.int32, device=dev),
+           "min_dist": torch.empty(n, dtype=torch.float32, device=dev),
+           "counts": torch.empty(K, dtype=torch.int32, device=dev),
+           "objective": torch.empty(n_iter + 1, dtype=torch.float64, device=dev),
+           "init_idx": torch.empty(K, dtype=torch.int32, device=dev) if u is not None else None}
+    w, wb = _workspace(kmeans_fit_workspace(n, d, K, X.dtype), ws, dev)
+    _chk(lib().hmoe_kmeans_fit(_ptr(X), _dt(X), n, d, K, n_iter, _ptr(u), 1 if reseed else 0,
+                               _ptr(Cout), _ptr(out["assign"]), _ptr(out["min_dist"]),
+                               _ptr(out["counts"]), _ptr(out["objective"]), _ptr(out["init_idx"]),
+                               _ptr(w), wb, _stream()), "kmeans_fit")
+    return out
+
+
+def kmeans_update_workspace(n, d, K, dtype) -> int:
+    return lib().hmoe_kmeans_update_workspace(n, d, K, _DT[dtype])
+
+
+def kmeans_update(X, K, assign, min_dist, sums, counts, C, mode=UPDATE_FULL, reseed=True,
+                  ws=None):
+    """One Lloyd centre update (modes: full / accumulate a chunk / finalize).  sums (fp64
+    [K,d]), counts (int64 [K]), C (fp32 [K,d]) and assign are updated in place."""
+    n, d = (X.shape if X is not None else (0, C.shape[1]))
+    dev = C.device
+    dt = _dt(X) if X is not None else F32
+    w, wb = _workspace(lib().hmoe_kmeans_update_workspace(n, d, K, dt), ws, dev)
+    _chk(lib().hmoe_kmeans_update(_ptr(X), dt, n, d, K, _ptr(assign), _ptr(min_dist), _ptr(sums),
+                                  _ptr(counts), _ptr(C), mode, 1 if reseed else 0, _ptr(w), wb,
+                                  _stream()), "kmeans_update")
+
+
+# ------------------------------------------------------------------ routing
+
+def moe_dispatch_workspace(n, K) -> int:
+    return lib().hmoe_moe_dispatch_workspace(n, K)
+
+
+def moe_dispatch(expert, K, rows=None, out=None, ws=None):
+    """Stable bucketing of the batch by expert; optionally gathers rows into expert order."""
+    n = expert.shape[0]
+    dev = expert.device
+    o = out or {}
+    counts = o.get("counts", torch.empty(K, dtype=torch.int32, device=dev))
+    offsets = o.get("offsets", torch.empty(K + 1, dtype=torch.int32, device=dev))
+    perm = o.get("perm", torch.empty(n, dtype=torch.int32, device=dev))
+    inv = o.get("inv", torch.empty(n, dtype=torch.int32, device=dev))
+    rows_sorted = None
+    w = 0
+    dt = F32
+    if rows is not None:
+        rows_sorted = o.get("rows_sorted", torch.empty_like(rows))
+        w = rows.shape[1]
+        dt = _dt(rows)
+    wsb, wb = _workspace(moe_dispatch_workspace(n, K), ws, dev)
+    _chk(lib().hmoe_moe_dispatch(_ptr(expert), n, K, _ptr(counts), _ptr(offsets), _ptr(perm),
+                                 _ptr(inv), _ptr(rows), _ptr(rows_sorted), dt, w, _ptr(wsb), wb,
+                                 _stream()), "moe_dispatch")
+    return {"counts": counts, "offsets": offsets, "perm": perm, "inv": inv,
+            "rows_sorted": rows_sorted}
+
+
+def permute_rows(inp, index, out=None):
+    """out[r] = inp[index[r]]."""
+    n = index.shape[0]
+    if out is None:
+        out = torch.empty((n, inp.shape[1]), dtype=inp.dtype, device=inp.device)
+    _chk(lib().hmoe_permute_rows(_ptr(inp), _ptr(out), _ptr(index), n, inp.shape[1], _dt(inp),
+                                 _stream()), "permute_rows")
+    return out
+
+
+# ------------------------------------------------------------------ experts + decoder
+
+def make_params(p: dict) -> MoeParams:
+    """p: W1 [K,h,d], b1 [K,h] or None, W2 [K,o,h], b2 [K,o] or None, D [V,o], bD [V] or None."""
+    K, h, d = p["W1"].shape
+    o = p["W2"].shape[1]
+    V = p["D"].shape[0]
+    return MoeParams(K, d, h, o, V, _dt(p["W1"]), _ptr(p["W1"]), _ptr(p.get("b1")), _ptr(p["W2"]),
+                     _ptr(p.get("b2")), _ptr(p["D"]), _ptr(p.get("bD")))
+
+
+def moe_workspace(params: MoeParams, n) -> int:
+    return lib().hmoe_moe_workspace(ctypes.byref(params), n)
+
+
+def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None):
+    """Expert MLPs + shared decoder + multilabel softmax loss (Eq. 3)."""
+    prm = make_params(p)
+    n = X_sorted.shape[0]
+    dev = X_sorted.device
+    dt = X_sorted.dtype
+    o = out or {}
+    H1s = o.get("H1_sorted", torch.empty(n, prm.d_hid, dtype=dt, device=dev))
+    H = o.get("H", torch.empty(n, prm.d_out, dtype=dt, device=dev))
+    lse = o.get("lse", torch.empty(n, dtype=torch.float32, device=dev))
+    loss = o.get("loss", torch.empty(n, dtype=torch.float32, device=dev))
+    lm = o.get("loss_mean", torch.empty(1, dtype=torch.float32, device=dev))
+    lab = Labels(_ptr(row_ptr), _ptr(tag))
+    w, wb = _workspace(moe_workspace(prm, n), ws, dev)
+    _chk(lib().hmoe_moe_forward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
+                                ctypes.byref(lab), _ptr(H1s), _ptr(H), _ptr(lse), _ptr(loss),
+                                _ptr(lm), _ptr(w), wb, _stream()), "moe_forward")
+    return {"H1_sorted": H1s, "H": H, "lse": lse, "loss": loss, "loss_mean": lm}
+
+
+def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted, H, lse,
+                 want_dX=True, out=None, ws=None):
+    """Gradients of the mean loss for all expert and decoder parameters (fp32) and dX."""
+    prm = make_params(p)
+    n = X_sorted.shape[0]
+    dev = X_sorted.device
+    K, d, h, o_, V = prm.K, prm.d_in, prm.d_hid, prm.d_out, prm.vocab
+    f32 = torch.float32
+    o = out or {}
+    g = {"dW1": o.get("dW1", torch.empty(K, h, d, dtype=f32, device=dev)),
+         "db1": o.get("db1", torch.empty(K, h, dtype=f32, device=dev)),
+         "dW2": o.get("dW2", torch.empty(K, o_, h, dtype=f32, device=dev)),
+         "db2": o.get("db2", torch.empty(K, o_, dtype=f32, device=dev)),
+         "dD": o.get("dD", torch.empty(V, o_, dtype=f32, device=dev)),
+         "dbD": o.get("dbD", torch.empty(V, dtype=f32, device=dev)),
+         "dX": (o.get("dX", torch.empty(n, d, dtype=X_sorted.dtype, device=dev))
+                if want_dX else None)}
+    lab = Labels(_ptr(row_ptr), _ptr(tag))
+    w, wb = _workspace(moe_workspace(prm, n), ws, dev)
+    _chk(lib().hmoe_moe_backward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
+                                 _ptr(inv), ctypes.byref(lab), _ptr(H1_sorted), _ptr(H), _ptr(lse),
+                                 _ptr(g["dW1"]), _ptr(g["db1"]), _ptr(g["dW2"]), _ptr(g["db2"]),
+                                 _ptr(g["dD"]), _ptr(g["dbD"]), _ptr(g["dX"]), _ptr(w), wb,
+                                 _stream()), "moe_backward")
+    return g
