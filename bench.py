@@ -1,0 +1,382 @@
+"""Benchmark of the hard mixture-of-experts hot path on one MI355X.
+
+One step = one routed training step on the balanced workload: gater assignment of 65,536
+bf16 feature rows (d = 2048) to the nearest of K = 16 centres, counting-sort dispatch, the
+16 expert MLPs 2048 -> 4096 -> 1024 with the shared 1024 -> 50,000 decoder, multilabel
+softmax loss, and the full backward pass (all parameter gradients and dX).  Inputs are
+seeded synthetic tensors already resident in HBM.
+
+Printed: one JSON line with the step throughput (samples/s), the roofline of the dominant
+kernel (HIP events recorded around every launch in the timed region), the fp64 CPU oracle
+timed on a bounded sample of the same workload, and extra legs for the gater fit
+(2^20 fp32 rows, K = 64, 20 Lloyd iterations), the skewed routing step (K = 128, V = 100k)
+and the large streamed assignment (2^24 bf16 rows, K = 1024).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "k-means assign samples/s; routed MoE fwd+bwd samples/s and % MFMA/HBM peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ routed step
+
+def gemm_flops(s):
+    """Algorithmic FLOPs per launch of each labelled kernel of one routed step."""
+    n, d, h, o, V, K = s["n"], s["d"], s["h"], s["o"], s["V"], s["K"]
+    return {
+        "assign": 2.0 * n * K * d,
+        "expert layer 1": 2.0 * n * d * h,
+        "expert layer 2": 2.0 * n * h * o,
+        "decoder forward": 2.0 * n * V * o,
+        "decoder dH": 2.0 * n * V * o,
+        "decoder dD": 2.0 * n * V * o,
+        "expert dW2": 2.0 * n * o * h,
+        "expert dH1": 2.0 * n * o * h,
+        "expert dW1": 2.0 * n * h * d,
+        "expert dX": 2.0 * n * h * d,
+    }
+
+
+def step_flops(s, assign=True):
+    f = gemm_flops(s)
+    tot = sum(v for k, v in f.items() if k != "assign")
+    return tot + (f["assign"] if assign else 0.0)
+
+
+class RoutedStep:
+    """Preallocated buffers for one routed training step; run() enqueues it on the stream."""
+
+    def __init__(self, inp, routed_by_gater: bool):
+        import torch
+        from paper_1704_06363_amd import hmoe
+        self.h = hmoe
+        self.inp = inp
+        s = inp["shape"]
+        self.s = s
+        n, d, h, o, V, K = s["n"], s["d"], s["h"], s["o"], s["V"], s["K"]
+        dev = inp["X"].device
+        self.routed_by_gater = routed_by_gater
+        self.X = inp["X"]
+        self.C = inp.get("C")
+        self.ids = (torch.empty(n, dtype=torch.int32, device=dev) if routed_by_gater
+                    else torch.as_tensor(inp["ids"], dtype=torch.int32).to(dev))
+        self.md = torch.empty(n, dtype=torch.float32, device=dev)
+        self.row_ptr = torch.as_tensor(inp["row_ptr"]).to(dev)
+        self.tag = torch.as_tensor(inp["tag"]).to(dev)
+        bf = torch.bfloat16
+        self.disp = {"counts": torch.empty(K, dtype=torch.int32, device=dev),
+                     "offsets": torch.empty(K + 1, dtype=torch.int32, device=dev),
+                     "perm": torch.empty(n, dtype=torch.int32, device=dev),
+                     "inv": torch.empty(n, dtype=torch.int32, device=dev),
+                     "rows_sorted": torch.empty(n, d, dtype=bf, device=dev)}
+        self.fwd = {"H1_sorted": torch.empty(n, h, dtype=bf, device=dev),
+                    "H": torch.empty(n, o, dtype=bf, device=dev),
+                    "lse": torch.empty(n, dtype=torch.float32, device=dev),
+                    "loss": torch.empty(n, dtype=torch.float32, device=dev),
+                    "loss_mean": torch.empty(1, dtype=torch.float32, device=dev)}
+        f32 = torch.float32
+        self.grads = {"dW1": torch.empty(K, h, d, dtype=f32, device=dev),
+                      "db1": torch.empty(K, h, dtype=f32, device=dev),
+                      "dW2": torch.empty(K, o, h, dtype=f32, device=dev),
+                      "db2": torch.empty(K, o, dtype=f32, device=dev),
+                      "dD": torch.empty(V, o, dtype=f32, device=dev),
+                      "dbD": torch.empty(V, dtype=f32, device=dev),
+                      "dX": torch.empty(n, d, dtype=bf, device=dev)}
+        prm = hmoe.make_params(inp["params"])
+        need = max(hmoe.moe_workspace(prm, n), hmoe.moe_dispatch_workspace(n, K),
+                   hmoe.kmeans_assign_workspace(n, d, K, bf))
+        self.ws = torch.empty(need, dtype=torch.uint8, device=dev)
+
+    def run(self):
+        h, p = self.h, self.inp["params"]
+        if self.routed_by_gater:
+            h.kmeans_assign(self.X, self.C, assign=self.ids, min_dist=self.md, ws=self.ws)
+        h.moe_dispatch(self.ids, self.s["K"], rows=self.X, out=self.disp, ws=self.ws)
+        dd = self.disp
+        f = h.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], self.row_ptr, self.tag,
+                          out=self.fwd, ws=self.ws)
+        h.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], self.row_ptr,
+                       self.tag, f["H1_sorted"], f["H"], f["lse"], out=self.grads, ws=self.ws)
+
+
+def time_steps(fn, steps, warmup, timer=True):
+    import torch
+    from paper_1704_06363_amd import hmoe
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    if timer:
+        hmoe.timer_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    rep = {}
+    if timer:
+        rep = hmoe.timer_report()
+        hmoe.timer_enable(False)
+    return ms, rep
+
+
+def kernel_table(rep, flops, peak_tflops, steps):
+    out = {}
+    for label, (cnt, ms) in rep.items():
+        e = {"launches_per_step": cnt / steps, "avg_ms": ms / cnt}
+        if label in flops:
+            tf = flops[label] / (ms / cnt * 1e-3) / 1e12
+            e["tflops"] = round(tf, 2)
+            e["frac_peak"] = round(tf / peak_tflops, 4)
+        out[label] = e
+    return out
+
+
+def dominant(rep, flops):
+    best = None
+    for label, (cnt, ms) in rep.items():
+        if label in flops and (best is None or ms > rep[best][1]):
+            best = label
+    return best
+
+
+# ------------------------------------------------------------------ CPU oracle baseline
+
+def cpu_baseline(inp, sample: int, routed_by_gater: bool):
+    """The fp64 oracle on the first `sample` rows of the same workload: gater assignment
+    (if routed by the gater), dispatch, expert + decoder forward and full backward."""
+    from oracle import oracle as O
+    import torch
+
+    def h64(t):
+        return t.detach().to(torch.float64).cpu().numpy()
+
+    s = inp["shape"]
+    X = h64(inp["X"][:sample])
+    p = {k: (h64(v) if v is not None else None) for k, v in inp["params"].items()}
+    rp = inp["row_ptr"][:sample + 1].copy()
+    tg = inp["tag"][:rp[-1]].copy()
+    C = h64(inp["C"]) if routed_by_gater else None
+    ids = None if routed_by_gater else np.asarray(inp["ids"][:sample], np.int32)
+    O.build(force=False)
+    t0 = time.perf_counter()
+    if routed_by_gater:
+        ids, _, _ = O.assign(X, C)
+    O.dispatch(ids, s["K"])
+    f = O.moe_forward(X, ids, p["W1"], p["b1"], p["W2"], p["b2"], p["D"], p["bD"], rp, tg,
+                      store="bf16")
+    O.moe_backward(X, ids, p["W1"], p["W2"], p["D"], p["bD"], rp, tg, f["H1"], f["H"], f["lse"],
+                   store="bf16")
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    return {"value": round(sample / dt, 3), "unit": "samples/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"first {sample} of {s['n']} rows, full widths (d={s['d']}, h={s['h']}, "
+                      f"o={s['o']}, V={s['V']}, K={s['K']}): assign+dispatch+fwd+bwd in fp64, "
+                      f"{dt:.2f} s"}
+
+
+# ------------------------------------------------------------------ legs
+
+def leg_gater_fit(steps):
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    c = W.CONFIGS["gater_fit"]
+    X = W.gmm_features(c.n, c.d, c.extra["n_comp"], seed=0, dtype="f32", device="cuda",
+                       dirichlet_alpha=c.extra["alpha"])
+    u = torch.tensor(W.uniforms(c.K, 1), dtype=torch.float64, device="cuda")
+    ws = torch.empty(hmoe.kmeans_fit_workspace(c.n, c.d, c.K, torch.float32), dtype=torch.uint8,
+                     device="cuda")
+
+    def fn():
+        hmoe.kmeans_fit(X, c.K, c.n_iter, init_uniforms=u, ws=ws)
+
+    ms, rep = time_steps(fn, steps, 1)
+    a_cnt, a_ms = rep["assign"]
+    a_avg = a_ms / a_cnt
+    assign_tf = 2.0 * c.n * c.K * c.d / (a_avg * 1e-3) / 1e12
+    upd = sum(v[1] for k, v in rep.items() if k.startswith(("segsum", "dispatch", "reseed",
+                                                             "finalize", "permute")))
+    upd_iter_ms = upd / (steps * c.n_iter)
+    kpp = sum(v[1] for k, v in rep.items() if k.startswith("kmeans++")) / steps
+    out = {"workload": f"gater fit: n={c.n} fp32, d={c.d}, K={c.K}, k-means++ + {c.n_iter} "
+                       f"Lloyd iterations with reseeding",
+           "fit_ms": round(ms, 3),
+           "assign_samples_per_s": round(c.n / (a_avg * 1e-3), 1),
+           "assign_avg_ms": round(a_avg, 4),
+           "assign_tflops": round(assign_tf, 2),
+           "assign_frac_fp32_peak": round(assign_tf / PEAK_F32_TFLOPS, 4),
+           "update_ms_per_iter": round(upd_iter_ms, 4),
+           "update_frac_hbm_peak": round(c.n * c.d * 4 / (upd_iter_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "kmeanspp_ms": round(kpp, 3)}
+    del X
+    torch.cuda.empty_cache()
+    return out
+
+
+def leg_skewed(steps, warmup):
+    import torch
+    from paper_1704_06363_amd import workloads as W
+    inp = W.skewed_inputs(device="cuda", seed=0)
+    st = RoutedStep(inp, routed_by_gater=False)
+    ms, rep = time_steps(st.run, steps, warmup)
+    s = inp["shape"]
+    fl = gemm_flops(s)
+    tot = step_flops(s, assign=False)
+    out = {"workload": "skewed routed step: n=32768 bf16, d=2048, K=128 Zipf(1.3) buckets, "
+                       "MLP 2048-2048-1024, V=100000, fwd+bwd",
+           "samples_per_s": round(s["n"] / (ms * 1e-3), 1), "ms_per_step": round(ms, 3),
+           "tflops": round(tot / (ms * 1e-3) / 1e12, 1),
+           "frac_bf16_peak": round(tot / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "kernels": kernel_table(rep, fl, PEAK_BF16_TFLOPS, steps)}
+    del st, inp
+    torch.cuda.empty_cache()
+    return out
+
+
+def leg_large_assign(n_chunks):
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    c = W.CONFIGS["large_assign"]
+    chunk = c.extra["chunk"]
+    means = W.gmm_means(c.extra["n_comp"], c.d, seed=2, device="cuda")
+    chunks = [W.gmm_features(chunk, c.d, c.extra["n_comp"], seed=100 + i, dtype="bf16",
+                             device="cuda", means=means) for i in range(n_chunks)]
+    g = torch.Generator(device="cpu").manual_seed(3)
+    C = chunks[0][torch.randperm(chunk, generator=g)[:c.K].cuda()].contiguous()
+    a = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    md = torch.empty(chunk, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(hmoe.kmeans_assign_workspace(chunk, c.d, c.K, torch.bfloat16),
+                         hmoe.kmeans_update_workspace(chunk, c.d, c.K, torch.bfloat16)),
+                     dtype=torch.uint8, device="cuda")
+    sums = torch.zeros(c.K, c.d, dtype=torch.float64, device="cuda")
+    cnt = torch.zeros(c.K, dtype=torch.int64, device="cuda")
+    Cn = torch.empty(c.K, c.d, dtype=torch.float32, device="cuda")
+    hmoe.kmeans_assign(chunks[0], C, assign=a, min_dist=md, ws=ws)  # warm-up
+    torch.cuda.synchronize()
+    hmoe.timer_enable(True)
+    t0 = time.perf_counter()
+    for x in chunks:
+        hmoe.kmeans_assign(x, C, assign=a, min_dist=md, ws=ws)
+        hmoe.kmeans_update(x, c.K, a, md, sums, cnt, Cn, mode=hmoe.UPDATE_ACCUMULATE,
+                           reseed=False, ws=ws)
+    hmoe.kmeans_update(None, c.K, None, None, sums, cnt, Cn, mode=hmoe.UPDATE_FINALIZE, ws=ws)
+    torch.cuda.synchronize()
+    total_ms = (time.perf_counter() - t0) * 1e3
+    rep = hmoe.timer_report()
+    hmoe.timer_enable(False)
+    n = chunk * n_chunks
+    a_ms = rep["assign"][1] + rep.get("assign merge", (0, 0.0))[1] + rep["centre norms"][1]
+    gemm_ms = rep["assign"][1]
+    tf = 2.0 * n * c.K * c.d / (gemm_ms * 1e-3) / 1e12
+    upd_ms = total_ms - a_ms
+    out = {"workload": f"large assign: {n_chunks} chunks x {chunk} bf16 rows, d={c.d}, K={c.K}, "
+                       f"plus one streamed centre-update pass",
+           "assign_samples_per_s": round(n / (a_ms * 1e-3), 1),
+           "distance_gemm_tflops": round(tf, 1),
+           "distance_gemm_frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+           "assign_ms": round(a_ms, 3), "update_pass_ms": round(upd_ms, 3),
+           "update_frac_hbm_peak": round(n * c.d * 2 / (upd_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del chunks
+    torch.cuda.empty_cache()
+    return out
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-legs", action="store_true", help="skip the gater/skewed/large legs")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-sample", type=int, default=256)
+    ap.add_argument("--large-chunks", type=int, default=16)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is "
+              f"a design note, not a measured configuration.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    torch.cuda.set_device(0)
+    hmoe.lib()
+
+    log("balanced step: generating inputs")
+    inp = W.balanced_inputs(device="cuda", seed=0)
+    s = inp["shape"]
+    st = RoutedStep(inp, routed_by_gater=True)
+    log("balanced step: timing")
+    ms, rep = time_steps(st.run, args.steps, args.warmup)
+    fl = gemm_flops(s)
+    kern = kernel_table(rep, fl, PEAK_BF16_TFLOPS, args.steps)
+    dom = dominant(rep, fl)
+    cnt, tot_ms = rep[dom]
+    avg = tot_ms / cnt
+    achieved = fl[dom] / (avg * 1e-3) / 1e12
+    tot_flops = step_flops(s)
+    res = {
+        "metric": METRIC,
+        "value": round(s["n"] / (ms * 1e-3), 1),
+        "unit": "samples/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "balanced routed training step: gater assign (K=16 centres) + "
+                               "dispatch + 16 expert MLPs 2048-4096-1024 + shared decoder "
+                               "1024->50000 + multilabel softmax loss, forward and backward",
+                   "batch": s["n"], "d": s["d"], "experts": s["K"], "hidden": s["h"],
+                   "expert_out": s["o"], "vocab": s["V"], "max_tags": 8},
+        "step_tflops": round(tot_flops / (ms * 1e-3) / 1e12, 1),
+        "step_frac_bf16_peak": round(tot_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "avg_ms": round(avg, 4), "flop_per_launch": fl[dom]},
+        "kernels": kern,
+    }
+    loss = float(st.fwd["loss_mean"].item())
+    res["loss_mean"] = round(loss, 5)
+    del st
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        log("cpu oracle baseline")
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample, routed_by_gater=True)
+    del inp
+    torch.cuda.empty_cache()
+    if not args.no_legs:
+        legs = {}
+        log("leg: gater fit")
+        legs["gater_fit"] = leg_gater_fit(steps=2)
+        log("leg: skewed routing")
+        legs["skewed"] = leg_skewed(steps=max(2, args.steps // 2), warmup=1)
+        log("leg: large assign")
+        legs["large_assign"] = leg_large_assign(args.large_chunks)
+        res["legs"] = legs
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

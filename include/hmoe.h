@@ -167,6 +167,18 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                       float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* ------------------------------------------------------------------ diagnostics */
+
+/* Launch timing for benchmarks, not part of the hot path.  While enabled, every kernel the
+ * library launches is bracketed by a pair of HIP events on its stream (the pool of events
+ * grows as needed and is kept for the life of the process).  hmoe_timer_enable(1) starts a
+ * new recording, (0) stops it.  hmoe_timer_report() waits for the recorded events and writes
+ * one line per kernel label, "label<TAB>launches<TAB>total_ms", into buf (host memory,
+ * truncated to buf_bytes - 1 characters and NUL-terminated); it returns the full length of
+ * the report or a negative error code.  Not thread-safe. */
+int hmoe_timer_enable(int on);
+int64_t hmoe_timer_report(char* buf, size_t buf_bytes);
+
 #ifdef __cplusplus
 }
 #endif

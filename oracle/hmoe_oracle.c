@@ -12,7 +12,8 @@
  *     bf16 bytes widened to double by the caller).
  *   - Results are rounded to a storage precision only where the device library stores a
  *     tensor that a later step reads back: centroids (fp32), the expert hidden activations
- *     and outputs, and the input gradient (the data dtype).  `store` selects that rounding:
+ *     and outputs, the activation gradients (g, dh, dz) and the input gradient (the data
+ *     dtype: "bf16 in, fp32 accumulate, bf16 out" for every layer).  `store` selects that rounding:
  *     0 = keep fp64, 1 = fp32 (round to nearest even), 2 = bf16 (round to nearest even).
  *   - Matrices are row-major.  Expert weights follow the [out][in] convention.
  *   - OpenMP is used only across independent samples / output rows; every sum runs in a
@@ -384,7 +385,9 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
  *   g_i  = (p_i - y_i) * scale            (scale = 1/n for the batch mean)
  *   dbD  = sum_i g_i,  dD = sum_i g_i H[i]^T,  dh_i = D^T g_i
  *   db2_e = sum dh,  dW2_e = sum dh h1^T,  dh1 = W2_e^T dh,  dz = dh1 * [h1 > 0]
- *   db1_e = sum dz,  dW1_e = sum dz x^T,   dx = W1_e^T dz (rounded by `store`)
+ *   db1_e = sum dz,  dW1_e = sum dz x^T,   dx = W1_e^T dz
+ * The activation gradients g (as used by dD and dh), dh, dz and dx are the tensors a device
+ * stores and reads back; `store` rounds them (dbD sums the unrounded g).
  * Experts that receive no sample get zero gradients.  dX may be NULL. */
 int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
                           const double* X, const int32_t* a, const double* W1,
@@ -399,9 +402,10 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     if (row_ptr[i + 1] <= row_ptr[i]) return -4;
   }
   double* G = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * V);
+  double* GS = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * V);
   double* dH = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * o);
   double* dZ = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * h);
-  if (!G || !dH || !dZ) { free(G); free(dH); free(dZ); return -2; }
+  if (!G || !GS || !dH || !dZ) { free(G); free(GS); free(dH); free(dZ); return -2; }
 
   /* Per sample: g_i, dh_i, dz_i. */
 #pragma omp parallel for schedule(static)
@@ -418,20 +422,22 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     int32_t np = row_ptr[i + 1] - row_ptr[i];
     for (int32_t q = row_ptr[i]; q < row_ptr[i + 1]; ++q) g[tag[q]] -= 1.0 / (double)np;
     for (int32_t v = 0; v < V; ++v) g[v] *= scale;
+    double* gs = GS + i * (int64_t)V;
+    for (int32_t v = 0; v < V; ++v) gs[v] = store_round(g[v], store);
     double* dh = dH + i * (int64_t)o;
     for (int32_t j = 0; j < o; ++j) dh[j] = 0.0;
     for (int32_t v = 0; v < V; ++v) {
       const double* dv = D + (int64_t)v * o;
-      for (int32_t j = 0; j < o; ++j) dh[j] += g[v] * dv[j];
+      for (int32_t j = 0; j < o; ++j) dh[j] += gs[v] * dv[j];
     }
+    for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], store);
     const double* w2 = W2 + (int64_t)e * o * h;
     const double* h1 = H1 + i * (int64_t)h;
     double* dz = dZ + i * (int64_t)h;
     for (int32_t k = 0; k < h; ++k) dz[k] = 0.0;
     for (int32_t j = 0; j < o; ++j)
       for (int32_t k = 0; k < h; ++k) dz[k] += dh[j] * w2[(int64_t)j * h + k];
-    for (int32_t k = 0; k < h; ++k)
-      if (!(h1[k] > 0.0)) dz[k] = 0.0;
+    for (int32_t k = 0; k < h; ++k) dz[k] = (h1[k] > 0.0) ? store_round(dz[k], store) : 0.0;
     if (dX) {
       const double* w1 = W1 + (int64_t)e * h * d;
       double* dx = dX + i * (int64_t)d;
@@ -449,8 +455,8 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     double sb = 0.0;
     for (int32_t j = 0; j < o; ++j) dd[j] = 0.0;
     for (int64_t i = 0; i < n; ++i) {
-      double g = G[i * (int64_t)V + v];
-      sb += g;
+      sb += G[i * (int64_t)V + v];
+      const double g = GS[i * (int64_t)V + v];
       const double* y = H + i * (int64_t)o;
       for (int32_t j = 0; j < o; ++j) dd[j] += g * y[j];
     }
@@ -489,6 +495,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     if (db1) db1[(int64_t)e * h + k] = sb;
   }
   free(G);
+  free(GS);
   free(dH);
   free(dZ);
   return 0;

@@ -2,6 +2,9 @@
 // checks and dispatch to the launchers.  Host code only.
 #include <string.h>
 
+#include <string>
+#include <vector>
+
 #include "launch.hpp"
 
 namespace hmoe {
@@ -16,6 +19,45 @@ void set_error(const char* fmt, ...) {
 }
 
 void clear_error() { g_err[0] = 0; }
+
+// ------------------------------------------------------------------ launch timer
+// Process-wide diagnostics state: a pool of event pairs recorded around each launch while
+// enabled.  Not thread-safe; meant for a single benchmarking thread.
+namespace {
+struct LaunchTimer {
+  bool on = false;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<std::string> label;
+  size_t used = 0;
+  const char* pending = nullptr;
+};
+LaunchTimer g_timer;
+}  // namespace
+
+void timer_pre(const char* label, hipStream_t st) {
+  if (!g_timer.on) return;
+  if (g_timer.used == g_timer.start.size()) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return;
+    if (hipEventCreate(&b) != hipSuccess) {
+      hipEventDestroy(a);
+      return;
+    }
+    g_timer.start.push_back(a);
+    g_timer.stop.push_back(b);
+    g_timer.label.emplace_back();
+  }
+  g_timer.pending = label;
+  hipEventRecord(g_timer.start[g_timer.used], st);
+}
+
+void timer_post(hipStream_t st) {
+  if (!g_timer.on || !g_timer.pending) return;
+  hipEventRecord(g_timer.stop[g_timer.used], st);
+  g_timer.label[g_timer.used] = g_timer.pending;
+  g_timer.pending = nullptr;
+  ++g_timer.used;
+}
 
 static int fail(int code, const char* fmt, ...) {
   va_list ap;
@@ -66,6 +108,49 @@ extern "C" {
 const char* hmoe_last_error(void) { return g_err; }
 
 int hmoe_version(void) { return HMOE_VERSION; }
+
+int hmoe_timer_enable(int on) {
+  clear_error();
+  g_timer.on = on != 0;
+  g_timer.used = 0;
+  g_timer.pending = nullptr;
+  return HMOE_OK;
+}
+
+int64_t hmoe_timer_report(char* buf, size_t buf_bytes) {
+  clear_error();
+  // per label: launches and total milliseconds, in first-seen order
+  std::vector<std::string> names;
+  std::vector<double> ms;
+  std::vector<long long> cnt;
+  for (size_t i = 0; i < g_timer.used; ++i) {
+    if (hipEventSynchronize(g_timer.stop[i]) != hipSuccess) return fail(HMOE_EHIP, "timer: event sync failed");
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, g_timer.start[i], g_timer.stop[i]) != hipSuccess)
+      return fail(HMOE_EHIP, "timer: elapsed time failed");
+    size_t j = 0;
+    while (j < names.size() && names[j] != g_timer.label[i]) ++j;
+    if (j == names.size()) {
+      names.push_back(g_timer.label[i]);
+      ms.push_back(0.0);
+      cnt.push_back(0);
+    }
+    ms[j] += t;
+    cnt[j] += 1;
+  }
+  std::string out;
+  char line[256];
+  for (size_t j = 0; j < names.size(); ++j) {
+    snprintf(line, sizeof(line), "%s\t%lld\t%.6f\n", names[j].c_str(), cnt[j], ms[j]);
+    out += line;
+  }
+  if (buf && buf_bytes > 0) {
+    const size_t m = out.size() < buf_bytes - 1 ? out.size() : buf_bytes - 1;
+    memcpy(buf, out.data(), m);
+    buf[m] = 0;
+  }
+  return (int64_t)out.size();
+}
 
 size_t hmoe_kmeans_assign_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt) {
   (void)d;

@@ -155,19 +155,15 @@ int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int
   const int bits = id_bits(K);
   const size_t lds = 4 * (size_t)K * sizeof(int32_t);
   if (nb > 0) {
-    hipLaunchKernelGGL(k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
+    HMOE_LAUNCH("dispatch hist", k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        (int32_t*)nullptr);
-    HMOE_TRY(launch_check("dispatch hist"));
   }
-  hipLaunchKernelGGL(k_dispatch_colscan, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, bc, (int)nb, K,
+  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, bc, (int)nb, K,
                      counts);
-  HMOE_TRY(launch_check("dispatch colscan"));
-  hipLaunchKernelGGL(k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
-  HMOE_TRY(launch_check("dispatch offsets"));
+  HMOE_LAUNCH("dispatch offsets", k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
   if (nb > 0) {
-    hipLaunchKernelGGL(k_dispatch_scatter, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
+    HMOE_LAUNCH("dispatch scatter", k_dispatch_scatter, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        offsets, perm, inv);
-    HMOE_TRY(launch_check("dispatch scatter"));
   }
   return HMOE_OK;
 }
@@ -179,14 +175,14 @@ int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, i
   const int64_t total = n * vpr;
   int64_t grid = cdiv(total, 256);
   if (grid > 8192) grid = 8192;
-  hipLaunchKernelGGL(k_permute_rows, dim3((unsigned)grid), dim3(256), 0, st, (const i32x4*)in, (i32x4*)out,
+  HMOE_LAUNCH("permute rows", k_permute_rows, dim3((unsigned)grid), dim3(256), 0, st, (const i32x4*)in, (i32x4*)out,
                      index, n, vpr);
-  return launch_check("permute rows");
+  return HMOE_OK;
 }
 
 int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st) {
-  hipLaunchKernelGGL(k_seg_tiles, dim3(1), dim3(1024), 0, st, seg, G, tile, tile_start);
-  return launch_check("segment tiles");
+  HMOE_LAUNCH("segment tiles", k_seg_tiles, dim3(1), dim3(1024), 0, st, seg, G, tile, tile_start);
+  return HMOE_OK;
 }
 
 template <typename T, typename O>
@@ -197,12 +193,11 @@ int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* 
   double* part = ws.take<double>((size_t)pieces * w);
   if (!ws.fits()) return HMOE_EWORKSPACE;
   HMOE_TRY(launch_seg_tiles(seg, G, kSegPiece, ts, st));
-  hipLaunchKernelGGL(k_segsum_partial<T>, dim3((unsigned)pieces), dim3(256), 0, st, X, ld, rowmap, seg, ts, G,
+  HMOE_LAUNCH("segsum partial", k_segsum_partial<T>, dim3((unsigned)pieces), dim3(256), 0, st, X, ld, rowmap, seg, ts, G,
                      w, part);
-  HMOE_TRY(launch_check("segsum partial"));
-  hipLaunchKernelGGL(k_segsum_final<O>, dim3((unsigned)cdiv((int64_t)G * w, 256)), dim3(256), 0, st, part,
+  HMOE_LAUNCH("segsum final", k_segsum_final<O>, dim3((unsigned)cdiv((int64_t)G * w, 256)), dim3(256), 0, st, part,
                      ts, G, w, out, accumulate);
-  return launch_check("segsum final");
+  return HMOE_OK;
 }
 
 size_t segsum_ws(int64_t n, int G, int w) {
@@ -225,11 +220,10 @@ int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, flo
                    hipStream_t st) {
   double* part = ws.take<double>(kSumBlocks);
   if (!ws.fits()) return HMOE_EWORKSPACE;
-  hipLaunchKernelGGL(k_sum_partial<float>, dim3(kSumBlocks), dim3(256), 0, st, x, n, part);
-  HMOE_TRY(launch_check("sum partial"));
-  if (out_f64) hipLaunchKernelGGL(k_sum_final<double>, dim3(1), dim3(64), 0, st, part, scale, out_f64);
-  if (out_f32) hipLaunchKernelGGL(k_sum_final<float>, dim3(1), dim3(64), 0, st, part, scale, out_f32);
-  return launch_check("sum final");
+  HMOE_LAUNCH("sum partial", k_sum_partial<float>, dim3(kSumBlocks), dim3(256), 0, st, x, n, part);
+  if (out_f64) HMOE_LAUNCH("sum final", k_sum_final<double>, dim3(1), dim3(64), 0, st, part, scale, out_f64);
+  if (out_f32) HMOE_LAUNCH("sum final", k_sum_final<float>, dim3(1), dim3(64), 0, st, part, scale, out_f32);
+  return HMOE_OK;
 }
 
 }  // namespace hmoe

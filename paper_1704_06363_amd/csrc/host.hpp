@@ -47,6 +47,20 @@ inline size_t dtype_size(hmoe_dtype_t dt) { return dt == HMOE_BF16 ? 2 : 4; }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Optional per-launch HIP-event timing (off unless hmoe_timer_enable(1) was called).
+void timer_pre(const char* label, hipStream_t st);
+void timer_post(hipStream_t st);
+
+// Launch a kernel through the timer hooks and report launch failures as HMOE_EHIP.
+#define HMOE_LAUNCH(label, kernel, grid, block, lds, st, ...)          \
+  do {                                                                 \
+    ::hmoe::timer_pre(label, st);                                      \
+    hipLaunchKernelGGL(kernel, grid, block, lds, st, __VA_ARGS__);     \
+    ::hmoe::timer_post(st);                                            \
+    int _lrc = ::hmoe::launch_check(label);                            \
+    if (_lrc != HMOE_OK) return _lrc;                                  \
+  } while (0)
+
 #define HMOE_TRY(...)                 \
   do {                                \
     int _rc = (__VA_ARGS__);          \

@@ -136,17 +136,14 @@ static int assign_t(const T* X, int64_t n, int32_t d, const T* C, int32_t K, int
     xn = ws.take<float>(n);
   }
   if (!ws.fits()) return HMOE_EWORKSPACE;
-  hipLaunchKernelGGL(k_cnorm<T>, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, C, K, d, cn);
-  HMOE_TRY(launch_check("centre norms"));
+  HMOE_LAUNCH("centre norms", k_cnorm<T>, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, C, K, d, cn);
   if (n == 0) return HMOE_OK;
   const int64_t tiles = cdiv(n, kBM) * nt;
-  hipLaunchKernelGGL(k_assign<T>, dim3((unsigned)tiles), dim3(kThreads), kGemmLds, st, X, n, d, C, K, cn,
+  HMOE_LAUNCH("assign", k_assign<T>, dim3((unsigned)tiles), dim3(kThreads), kGemmLds, st, X, n, d, C, K, cn,
                      assign, min_dist, pv, pi, xn);
-  HMOE_TRY(launch_check("assign"));
   if (nt > 1) {
-    hipLaunchKernelGGL(k_assign_merge, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, pv, pi, xn, n, nt, assign,
+    HMOE_LAUNCH("assign merge", k_assign_merge, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, pv, pi, xn, n, nt, assign,
                        min_dist);
-    HMOE_TRY(launch_check("assign merge"));
   }
   return HMOE_OK;
 }
@@ -404,12 +401,12 @@ static int update_core(const T* X, int64_t n, int32_t d, int32_t K, int32_t* ass
   HMOE_TRY(launch_dispatch(assign, n, K, b.counts32, b.offsets, b.perm, b.inv, ws, st));
   HMOE_TRY(launch_segsum<T, double>(X, d, b.perm, b.offsets, K, d, n, sums, accumulate, ws, st));
   if (accumulate) {
-    hipLaunchKernelGGL(k_add_counts, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, b.counts32, K, counts64);
-    return launch_check("add counts");
+    HMOE_LAUNCH("add counts", k_add_counts, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, b.counts32, K, counts64);
+    return HMOE_OK;
   }
-  hipLaunchKernelGGL(k_reseed<T>, dim3(1), dim3(1024), 0, st, X, n, d, K, assign, d1, b.counts32, counts64, sums,
+  HMOE_LAUNCH("reseed", k_reseed<T>, dim3(1), dim3(1024), 0, st, X, n, d, K, assign, d1, b.counts32, counts64, sums,
                      reseed);
-  return launch_check("reseed");
+  return HMOE_OK;
 }
 
 static size_t update_scratch(int64_t n, int32_t d, int32_t K) {
@@ -436,9 +433,8 @@ static int update_t(const T* X, int64_t n, int32_t d, int32_t K, int32_t* assign
                             mode == HMOE_UPDATE_FULL ? reseed : 0, b, ws, st));
   }
   if (mode != HMOE_UPDATE_ACCUMULATE) {
-    hipLaunchKernelGGL((k_finalize<T, int64_t>), dim3((unsigned)cdiv((int64_t)K * d, 256)), dim3(256), 0, st, sums,
+    HMOE_LAUNCH("finalize centres", (k_finalize<T, int64_t>), dim3((unsigned)cdiv((int64_t)K * d, 256)), dim3(256), 0, st, sums,
                        counts64, K, d, C, (T*)nullptr);
-    HMOE_TRY(launch_check("finalize centres"));
   }
   return HMOE_OK;
 }
@@ -485,24 +481,19 @@ static int fit_t(const T* X, int64_t n, int32_t d, int32_t K, int32_t n_iter, co
   const bool same = sizeof(T) == sizeof(float);  // fp32 data assigns against C itself
   const T* Cuse = same ? reinterpret_cast<const T*>(C) : Cd;
   if (u) {
-    hipLaunchKernelGGL(k_kpp_first, dim3(1), dim3(64), 0, st, u, n, idx);
-    HMOE_TRY(launch_check("kmeans++ first"));
+    HMOE_LAUNCH("kmeans++ first", k_kpp_first, dim3(1), dim3(64), 0, st, u, n, idx);
     for (int t = 0; t < K; ++t) {
-      hipLaunchKernelGGL(k_kpp_update<T>, dim3((unsigned)nb), dim3(256), 0, st, X, n, d, idx, t, D2, bsum);
-      HMOE_TRY(launch_check("kmeans++ D2"));
+      HMOE_LAUNCH("kmeans++ D2", k_kpp_update<T>, dim3((unsigned)nb), dim3(256), 0, st, X, n, d, idx, t, D2, bsum);
       if (t + 1 < K) {
-        hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(1024), 0, st, D2, n, bsum, nb, u, t + 1, idx);
-        HMOE_TRY(launch_check("kmeans++ select"));
+        HMOE_LAUNCH("kmeans++ select", k_kpp_select, dim3(1), dim3(1024), 0, st, D2, n, bsum, nb, u, t + 1, idx);
       }
     }
-    hipLaunchKernelGGL(k_gather_centres<T>, dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, X, d, idx, K, C,
+    HMOE_LAUNCH("gather centres", k_gather_centres<T>, dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, X, d, idx, K, C,
                        same ? (T*)nullptr : Cd);
-    HMOE_TRY(launch_check("gather centres"));
   }
   if (!u && !same) {
     // data-precision copy of the given centres
-    hipLaunchKernelGGL((k_convert_centres<T>), dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, C, Kd, Cd);
-    HMOE_TRY(launch_check("convert centres"));
+    HMOE_LAUNCH("convert centres", (k_convert_centres<T>), dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, C, Kd, Cd);
   }
   UpdateBufs b;
   Workspace* wsp = &ws;
@@ -518,9 +509,8 @@ static int fit_t(const T* X, int64_t n, int32_t d, int32_t K, int32_t n_iter, co
     if (objective) HMOE_TRY(launch_sum_f32(d1, n, 1.0, objective + t, nullptr, ws, st));
     if (t == n_iter) break;
     HMOE_TRY(update_core<T>(X, n, d, K, assign, d1, sums, c64, 0, reseed, b, ws, st));
-    hipLaunchKernelGGL((k_finalize<T, int64_t>), dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, sums, c64, K, d,
+    HMOE_LAUNCH("finalize centres", (k_finalize<T, int64_t>), dim3((unsigned)cdiv(Kd, 256)), dim3(256), 0, st, sums, c64, K, d,
                        C, same ? (T*)nullptr : Cd);
-    HMOE_TRY(launch_check("finalize centres"));
   }
   if (counts) {
     ws.off = mark;

@@ -402,18 +402,14 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   const T* D = (const T*)p->D;
   HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
   const int64_t mt_bound = cdiv(n, kBM) + s.K;
-  hipLaunchKernelGGL((k_expert_fwd<T, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds, st,
+  HMOE_LAUNCH("expert layer 1", (k_expert_fwd<T, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds, st,
                      Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
-  HMOE_TRY(launch_check("expert layer 1"));
-  hipLaunchKernelGGL((k_expert_fwd<T, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
+  HMOE_LAUNCH("expert layer 2", (k_expert_fwd<T, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
                      (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
-  HMOE_TRY(launch_check("expert layer 2"));
-  hipLaunchKernelGGL(k_dec_fwd<T>, dim3((unsigned)(cdiv(n, kBM) * ntv)), dim3(kThreads), kGemmLds, st, (const T*)H, D,
+  HMOE_LAUNCH("decoder forward", k_dec_fwd<T>, dim3((unsigned)(cdiv(n, kBM) * ntv)), dim3(kThreads), kGemmLds, st, (const T*)H, D,
                      (const T*)p->bD, n, s.V, s.o, pm, ps);
-  HMOE_TRY(launch_check("decoder forward"));
-  hipLaunchKernelGGL(k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
+  HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
                      (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
-  HMOE_TRY(launch_check("decoder loss"));
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
 }
 
@@ -435,40 +431,32 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   const T* D = (const T*)p->D;
   const int ntv = (int)cdiv(s.V, kBN);
   // decoder
-  hipLaunchKernelGGL(k_dec_grad<T>, dim3((unsigned)(mt * ntv)), dim3(kThreads), kGemmLds, st, H, D, (const T*)p->bD, n,
+  HMOE_LAUNCH("decoder grad", k_dec_grad<T>, dim3((unsigned)(mt * ntv)), dim3(kThreads), kGemmLds, st, H, D, (const T*)p->bD, n,
                      s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
-  HMOE_TRY(launch_check("decoder grad"));
   if (dbD) {
-    hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V, dbD);
-    HMOE_TRY(launch_check("decoder bias grad"));
+    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V, dbD);
   }
-  hipLaunchKernelGGL(k_dec_dH<T>, dim3((unsigned)(mt * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st, (const T*)G, D,
+  HMOE_LAUNCH("decoder dH", k_dec_dH<T>, dim3((unsigned)(mt * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st, (const T*)G, D,
                      n, s.V, s.o, inv, dYs);
-  HMOE_TRY(launch_check("decoder dH"));
-  hipLaunchKernelGGL(k_dec_dD<T>, dim3((unsigned)(cdiv(s.V, kBM) * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
+  HMOE_LAUNCH("decoder dD", k_dec_dD<T>, dim3((unsigned)(cdiv(s.V, kBM) * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
                      (const T*)G, H, n, s.V, s.o, dD);
-  HMOE_TRY(launch_check("decoder dD"));
   // experts
   HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
   const size_t mark = ws.off;
   if (db2) HMOE_TRY(launch_segsum<T, float>(dYs, s.o, nullptr, offsets, s.K, s.o, n, db2, 0, ws, st));
   ws.off = mark;
-  hipLaunchKernelGGL(k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, kBM) * cdiv(s.h, kBN))),
+  HMOE_LAUNCH("expert dW2", k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, kBM) * cdiv(s.h, kBN))),
                      dim3(kThreads), kGemmLds, st, (const T*)dYs, H1s, offsets, s.K, s.o, s.h, dW2);
-  HMOE_TRY(launch_check("expert dW2"));
   const int64_t mt_bound = cdiv(n, kBM) + s.K;
-  hipLaunchKernelGGL((k_expert_dgrad<T, true>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds,
+  HMOE_LAUNCH("expert dH1", (k_expert_dgrad<T, true>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds,
                      st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
-  HMOE_TRY(launch_check("expert dH1"));
   if (db1) HMOE_TRY(launch_segsum<T, float>(dZ, s.h, nullptr, offsets, s.K, s.h, n, db1, 0, ws, st));
   ws.off = mark;
-  hipLaunchKernelGGL(k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, kBM) * cdiv(s.d, kBN))),
+  HMOE_LAUNCH("expert dW1", k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, kBM) * cdiv(s.d, kBN))),
                      dim3(kThreads), kGemmLds, st, (const T*)dZ, Xs, offsets, s.K, s.h, s.d, dW1);
-  HMOE_TRY(launch_check("expert dW1"));
   if (dX) {
-    hipLaunchKernelGGL((k_expert_dgrad<T, false>), dim3((unsigned)(mt_bound * cdiv(s.d, kBN))), dim3(kThreads),
+    HMOE_LAUNCH("expert dX", (k_expert_dgrad<T, false>), dim3((unsigned)(mt_bound * cdiv(s.d, kBN))), dim3(kThreads),
                        kGemmLds, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm, dX);
-    HMOE_TRY(launch_check("expert dX"));
   }
   return HMOE_OK;
 }

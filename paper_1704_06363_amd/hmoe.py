@@ -26,6 +26,7 @@ SYMBOLS = (
     "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
     "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
     "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
+    "hmoe_timer_enable", "hmoe_timer_report",
 )
 
 
@@ -81,6 +82,10 @@ def lib():
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                         _P, _P, _SZ, _P]
+        L.hmoe_timer_enable.argtypes = [_c.c_int]
+        L.hmoe_timer_enable.restype = _c.c_int
+        L.hmoe_timer_report.argtypes = [_c.c_char_p, _SZ]
+        L.hmoe_timer_report.restype = _I64
         for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
                      "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
                      "hmoe_moe_backward"):
@@ -95,6 +100,25 @@ def version() -> int:
 
 def last_error() -> str:
     return lib().hmoe_last_error().decode()
+
+
+def timer_enable(on: bool = True):
+    """Start (or stop) recording HIP events around every kernel the library launches."""
+    _chk(lib().hmoe_timer_enable(1 if on else 0), "timer_enable")
+
+
+def timer_report() -> dict:
+    """{kernel label: (launches, total_ms)} for the launches recorded since timer_enable."""
+    n = lib().hmoe_timer_report(None, 0)
+    if n < 0:
+        raise HmoeError(f"timer_report failed ({n}): {last_error()}")
+    buf = ctypes.create_string_buffer(int(n) + 1)
+    lib().hmoe_timer_report(buf, int(n) + 1)
+    out = {}
+    for line in buf.value.decode().splitlines():
+        label, cnt, ms = line.split("\t")
+        out[label] = (int(cnt), float(ms))
+    return out
 
 
 def _chk(rc: int, what: str):

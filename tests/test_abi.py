@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 14
+    assert len(names) == 16
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(hmoe.SYMBOLS)

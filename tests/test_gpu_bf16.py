@@ -1,0 +1,152 @@
+"""bf16 parity of the routed step and the gater against the fp64 oracle at sizes the oracle
+finishes in seconds, spanning several 128-wide tiles with ragged tails, plus the degenerate
+cases (empty experts, K = 1, n = 0)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_1704_06363_amd import hmoe
+from paper_1704_06363_amd import workloads as W
+from tests.parity import RTOL, assert_assign, assert_close, assert_scalar_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+RT = RTOL["bf16"]
+
+
+def _step(X, ids, K, p, rp, tg, want_dX=True):
+    a = torch.as_tensor(ids, dtype=torch.int32).cuda()
+    d = hmoe.moe_dispatch(a, K, rows=X)
+    row_ptr = torch.tensor(rp, device="cuda")
+    tag = torch.tensor(tg, device="cuda")
+    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag)
+    return d, f, row_ptr, tag
+
+
+def _check_step(X, ids, K, p, rp, tg, rt=RT):
+    """Forward on the HIP path vs the oracle; backward from the oracle's saved activations."""
+    d, f, row_ptr, tag = _step(X, ids, K, p, rp, tg)
+    Xh = np64(X)
+    ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
+    ref = O.moe_forward(Xh, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
+                        store="bf16")
+    perm = npi(d["perm"])
+    counts, offsets, perm_ref, inv_ref = O.dispatch(ids, K)
+    assert np.array_equal(perm, perm_ref)
+    assert_close(f["H1_sorted"], ref["H1"][perm], rt, "H1_sorted")
+    assert_close(f["H"], ref["H"], rt, "H")
+    assert_close(f["lse"], ref["lse"], rt, "lse")
+    assert_close(f["loss"], ref["loss"], rt, "loss")
+    assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
+    H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(torch.bfloat16).cuda()
+    H = torch.tensor(ref["H"], dtype=torch.float32).to(torch.bfloat16).cuda()
+    lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
+    g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag,
+                          H1s, H, lse)
+    gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
+                        ref["lse"], store="bf16")
+    for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
+        assert_close(g[k], gr[k], rt, k)
+    return g, counts
+
+
+def test_routed_step_ragged_tiles():
+    # n, h, o, V all leave ragged tails in the 128-wide tiles; biases exercised
+    inp = W.balanced_inputs(device="cuda", seed=3, n=600, d=256, h=384, o=136, V=1000, K=5,
+                            bias=True)
+    C = inp["C"]
+    a, _ = hmoe.kmeans_assign(inp["X"], C)
+    a_ref, d1, d2 = O.assign(np64(inp["X"]), np64(C))
+    assert_assign(a, a_ref, d1, d2)
+    _check_step(inp["X"], a_ref, 5, inp["params"], inp["row_ptr"], inp["tag"])
+
+
+def test_skewed_routing_with_empty_experts():
+    n, K = 900, 24
+    inp = W.skewed_inputs(device="cuda", seed=5, n=n, d=128, h=256, o=64, V=520, K=K)
+    ids = inp["ids"]
+    g, counts = _check_step(inp["X"], ids, K, inp["params"], inp["row_ptr"], inp["tag"])
+    empty = np.flatnonzero(counts == 0)
+    assert len(empty) >= 2
+    for k in ("dW1", "db1", "dW2", "db2"):
+        assert torch.count_nonzero(g[k][torch.as_tensor(empty).cuda()]) == 0, k
+
+
+def test_single_expert():
+    inp = W.skewed_inputs(device="cuda", seed=6, n=300, d=64, h=128, o=64, V=256, K=1)
+    ids = np.zeros(300, np.int32)
+    _check_step(inp["X"], ids, 1, inp["params"], inp["row_ptr"], inp["tag"])
+
+
+@pytest.mark.parametrize("n,d,K", [(3000, 2048, 300), (1000, 512, 64), (777, 64, 129)])
+def test_assign_bf16_multi_tile(n, d, K):
+    X = W.gmm_features(n, d, 40, seed=n, dtype="bf16", device="cuda")
+    C = X[torch.randperm(n, generator=torch.Generator().manual_seed(1))[:K].cuda()].contiguous()
+    a, md = hmoe.kmeans_assign(X, C)
+    a_ref, d1, d2 = O.assign(np64(X), np64(C))
+    assert_assign(a, a_ref, d1, d2)
+    assert_close(md, d1, 1e-4, "min_dist")  # fp32 accumulation of exact bf16 products
+
+
+def test_kmeans_fit_bf16():
+    n, d, K = 5000, 256, 20
+    X = W.gmm_features(n, d, 32, seed=11, dtype="bf16", device="cuda", dirichlet_alpha=0.5)
+    u = W.uniforms(K, 12)
+    out = hmoe.kmeans_fit(X, K, 6, init_uniforms=u)
+    ref = O.fit(np64(X), K, 6, u=u, data_store="bf16")
+    assert npi(out["init_idx"]).tolist() == ref["init_idx"].tolist()
+    _, d1, d2 = O.assign(np64(X), O.round_store(ref["C"], "bf16"))
+    assert_assign(out["assign"], ref["a"], d1, d2)
+    assert_close(out["C"], ref["C"], 1e-4, "centres")
+    J = npi(out["objective"])
+    for t in range(7):
+        assert_scalar_close(J[t], ref["J"][t], 1e-4, f"J[{t}]")
+
+
+def test_update_chunks_and_reseed():
+    n, d, K = 4000, 64, 12
+    X = W.gmm_features(n, d, 6, seed=21, dtype="f32", device="cuda")
+    Xh = np64(X)
+    C0 = Xh[:K].copy()
+    C0[K - 3:] = 1e3  # three far-away centres: their clusters start empty
+    a_ref, d1, _ = O.assign(Xh, C0)
+    # full update with reseeding, from the oracle's assignment
+    a = torch.tensor(a_ref, dtype=torch.int32, device="cuda")
+    md = torch.tensor(d1, dtype=torch.float32, device="cuda")
+    C = torch.tensor(C0, dtype=torch.float32, device="cuda")
+    sums = torch.zeros(K, d, dtype=torch.float64, device="cuda")
+    cnt = torch.zeros(K, dtype=torch.int64, device="cuda")
+    hmoe.kmeans_update(X, K, a, md, sums, cnt, C, mode=hmoe.UPDATE_FULL, reseed=True)
+    C_ref, counts_ref, a2_ref = O.update(Xh, a_ref, np64(md), C0, reseed=True)
+    assert npi(cnt).tolist() == counts_ref.tolist()
+    assert np.array_equal(npi(a), a2_ref)
+    assert_close(C, O.round_store(C_ref, "f32"), 1e-6, "centres")
+    # the same update streamed in three chunks (no reseeding)
+    C2 = torch.tensor(C0, dtype=torch.float32, device="cuda")
+    sums.zero_()
+    cnt.zero_()
+    a = torch.tensor(a_ref, dtype=torch.int32, device="cuda")
+    for lo, hi in ((0, 1500), (1500, 1501), (1501, n)):
+        hmoe.kmeans_update(X[lo:hi].contiguous(), K, a[lo:hi].contiguous(), None, sums, cnt, C2,
+                           mode=hmoe.UPDATE_ACCUMULATE, reseed=False)
+    hmoe.kmeans_update(None, K, None, None, sums, cnt, C2, mode=hmoe.UPDATE_FINALIZE)
+    C_ref2, counts2, _ = O.update(Xh, a_ref, None, C0, reseed=False)
+    assert npi(cnt).tolist() == counts2.tolist()
+    assert_close(C2, O.round_store(C_ref2, "f32"), 1e-6, "chunked centres")
+
+
+def test_empty_batch():
+    X = torch.empty(0, 64, dtype=torch.bfloat16, device="cuda")
+    C = torch.randn(4, 64, device="cuda").to(torch.bfloat16)
+    a, md = hmoe.kmeans_assign(X, C)
+    assert a.numel() == 0
+    d = hmoe.moe_dispatch(torch.empty(0, dtype=torch.int32, device="cuda"), 3)
+    assert npi(d["counts"]).tolist() == [0, 0, 0] and npi(d["offsets"]).tolist() == [0, 0, 0, 0]
+    p = W.moe_params(3, 64, 128, 64, 80, seed=0, dtype="bf16", device="cuda")
+    z = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = hmoe.moe_backward(p, X, d["offsets"], d["perm"], d["inv"], z, z,
+                          torch.empty(0, 128, dtype=torch.bfloat16, device="cuda"),
+                          torch.empty(0, 64, dtype=torch.bfloat16, device="cuda"),
+                          torch.empty(0, device="cuda"), want_dX=False)
+    for k in ("dW1", "dW2", "dD", "dbD"):
+        assert torch.count_nonzero(g[k]) == 0
