@@ -156,7 +156,7 @@ size_t hmoe_kmeans_assign_workspace(int64_t n, int32_t d, int32_t K, hmoe_dtype_
   (void)d;
   (void)dt;
   if (n < 0 || K < 1) return 0;
-  return assign_ws(n, K);
+  return assign_ws(n, K, dt);
 }
 
 int hmoe_kmeans_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K,
@@ -171,7 +171,7 @@ int hmoe_kmeans_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, con
     HMOE_TRY(check_ptr("X", X));
     HMOE_TRY(check_ptr("assign", assign, false));
   }
-  HMOE_TRY(check_ws(assign_ws(n, K), ws_bytes, ws));
+  HMOE_TRY(check_ws(assign_ws(n, K, dt), ws_bytes, ws));
   Workspace w(ws, ws_bytes);
   return launch_assign(X, dt, n, d, C, K, assign, min_dist, w, (hipStream_t)stream);
 }

@@ -1,77 +1,115 @@
 // gemm.hpp -- MFMA tile engine shared by every dense contraction of the hot path.
 //
-// C[m, n] = sum_k A(m, k) * B(n, k) over one 128 x 128 output tile per workgroup (256 threads,
-// four 64-wide waves in a 2 x 2 grid, each wave 64 x 64).  Operands are staged through LDS
-// in a "row-major, K-contiguous" layout whatever their layout in HBM:
-//   K-contiguous operand  (stored [rows][K]): 16-byte vector loads go straight to LDS;
-//   K-strided operand     (stored [K][rows]): each thread loads 4 K-rows of one 16-byte
-//                         column chunk and transposes them in registers before the LDS store.
+// C[m, n] = sum_k A(m, k) * B(n, k) over one BM x BN output tile per workgroup, split into
+// (BM/WM) x (BN/WN) wavefronts of WM x WN.  Operands are staged through LDS in a row-major,
+// K-contiguous layout whatever their layout in HBM:
+//   K-contiguous operand (stored [rows][K]): 16-byte vector loads go straight to LDS;
+//   K-strided operand    (stored [K][rows]): each thread loads a block of K-rows x 4 rows --
+//                        8 x 4 for bf16, 4 x 4 for fp32 -- and transposes it in registers, so
+//                        the LDS store is again one 16-byte vector (one chunk) per row.
+// One stage covers 128 bytes of K per row (64 bf16 or 32 fp32), i.e. 8 chunks of 16 bytes.
+// LDS rows are not padded; chunk c of row r lives at chunk c ^ ((r ^ (r >> 3)) & 7), which
+// keeps every group of 8 lanes on distinct banks for the MFMA reads (8 consecutive rows, one
+// chunk), the transposed stores (8 rows four apart) and the direct stores (one row, 8 chunks).
 // bf16 uses v_mfma_f32_16x16x32_bf16 (8 consecutive k per lane); fp32 uses
-// v_mfma_f32_16x16x4_f32, fed from the same 16-byte LDS reads (4 consecutive k per lane,
+// v_mfma_f32_16x16x4_f32 fed from the same 16-byte LDS reads (4 consecutive k per lane,
 // consumed by 4 MFMAs).  Accumulation is fp32.  The K loop is double-buffered: the next
 // stage's global loads are in flight while the current stage feeds the MFMAs.
 //
 // Accumulator ownership (verified layout of the 16x16 MFMA outputs): lane l of wave w holds,
 // for sub-tile (i, j) and r = 0..3,
-//   row = (w / 2) * 64 + 16 i + 4 (l / 16) + r,     col = (w % 2) * 64 + 16 j + (l % 16).
+//   row = wm * WM + 16 i + 4 (l / 16) + r,     col = wn * WN + 16 j + (l % 16),
+// with wm = w / (BN / WN), wn = w % (BN / WN).
 #pragma once
 #include "common.hpp"
 
 namespace hmoe {
 
-constexpr int kBM = 128;
-constexpr int kBN = 128;
-constexpr int kThreads = 256;
-constexpr int kStageRowBytes = 128;  // K extent of one stage, in bytes (64 bf16 or 32 fp32)
-constexpr int kLdsStride = 144;      // padded LDS row stride (bytes): conflict-free b128 reads
-constexpr int kOperandBytes = kBM * kLdsStride;
-constexpr int kGemmLds = 4 * kOperandBytes;  // A and B, two stages each
+constexpr int kStageRowBytes = 128;  // K extent of one stage, in bytes
 
-template <typename T>
-struct Elt {
-  static constexpr int per_vec = 16 / sizeof(T);             // elements per 16-byte vector
-  static constexpr int bk = kStageRowBytes / sizeof(T);      // K per stage
+template <typename T, int BM_, int BN_, int WM_, int WN_>
+struct Cfg {
+  using type = T;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int WAVES_N = BN / WN, WAVES_M = BM / WM;
+  static constexpr int WAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int MI = WM / 16, NJ = WN / 16;
+  static constexpr int EPV = 16 / sizeof(T);             // elements per 16-byte vector
+  static constexpr int BK = kStageRowBytes / sizeof(T);  // K per stage
+  static constexpr int A_BYTES = BM * kStageRowBytes, B_BYTES = BN * kStageRowBytes;
+  static constexpr int LDS = 2 * (A_BYTES + B_BYTES);
 };
+
+// bf16 GEMMs: 256 x 256 tiles, eight waves of 128 x 64 (one workgroup, two waves per SIMD).
+typedef Cfg<bf16, 256, 256, 128, 64> CfgBig;
+// fp32 GEMMs and narrow problems: 128 x 128 tiles, four waves of 64 x 64.
+template <typename T>
+using CfgSmall = Cfg<T, 128, 128, 64, 64>;
+
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * kStageRowBytes + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 4);
+}
 
 // ------------------------------------------------------------------ operand staging
 
-// Loads one 128-row x (one stage of K) operand tile into registers.  `rows_valid` rows
-// exist (others read as zero); K positions >= k_valid read as zero.
-template <typename T, bool KCONTIG>
+// One ROWS-row operand tile of one K stage, held in registers between the global loads and
+// the LDS store.  Rows >= rows_valid and K positions >= k_valid read as zero.
+template <typename T, int ROWS, int THREADS, bool KCONTIG>
 struct Stager {
-  i32x4 v[4];
+  static constexpr int EPV = 16 / sizeof(T);
+  static constexpr bool BF = sizeof(T) == 2;
+  // K-contiguous: ROWS * 8 vectors of 16 bytes.
+  // K-strided bf16: ROWS / 4 * 8 pieces of 8 K-rows x 4 rows, loaded as 8-byte rows.
+  // K-strided fp32: ROWS / 4 * 8 blocks of 4 K-rows x 4 rows, loaded as 16-byte rows.
+  static constexpr int NPIECE = KCONTIG ? 0 : (ROWS / 4) * 8 / THREADS;
+  static constexpr int NV = KCONTIG ? ROWS * 8 / THREADS : (BF ? NPIECE * 4 : NPIECE * 4);
+  static_assert(KCONTIG ? (ROWS * 8) % THREADS == 0 : ((ROWS / 4) * 8) % THREADS == 0, "tile/threads");
+  i32x4 v[NV];
 
-  // K-contiguous: element (r, k) at base + r * ld + k.  k_valid must be a multiple of the
-  // vector width (checked by the host).
-  // K-strided:    element (r, k) at base + k * ld + r.  rows_valid must be a multiple of the
-  // vector width.
-  __device__ __forceinline__ void load(const T* __restrict__ base, int64_t ld, int rows_valid,
-                                       int k0, int k_valid) {
+  // K-contiguous: element (r, k) at base + r * ld + k (k_valid a multiple of EPV).
+  // K-strided:    element (r, k) at base + k * ld + r (rows_valid a multiple of 4).
+  __device__ __forceinline__ void load(const T* __restrict__ base, int64_t ld, int rows_valid, int k0,
+                                       int k_valid) {
     const int t = threadIdx.x;
-    constexpr int EPV = Elt<T>::per_vec;
     if constexpr (KCONTIG) {
-      const int vc = t & 7;
-      const int k = k0 + vc * EPV;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = (t >> 3) + 32 * q;
+      for (int q = 0; q < NV; ++q) {
+        const int vi = t + THREADS * q;
+        const int r = vi >> 3;
+        const int k = k0 + (vi & 7) * EPV;
         if (r < rows_valid && k < k_valid)
           v[q] = *reinterpret_cast<const i32x4*>(base + (int64_t)r * ld + k);
         else
           v[q] = i32x4{0, 0, 0, 0};
       }
     } else {
-      constexpr int CHUNKS = kBM / EPV;  // 16 (bf16) or 32 (fp32) column chunks
-      const int rc = t % CHUNKS;
-      const int kq = t / CHUNKS;         // 0..15 (bf16) or 0..7 (fp32): 4 K-rows each
-      const int r = rc * EPV;
+      constexpr int RQ = ROWS / 4;  // groups of 4 rows
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int k = k0 + 4 * kq + q;
-        if (r < rows_valid && k < k_valid)
-          v[q] = *reinterpret_cast<const i32x4*>(base + (int64_t)k * ld + r);
-        else
-          v[q] = i32x4{0, 0, 0, 0};
+      for (int q = 0; q < NPIECE; ++q) {
+        const int pc = t + THREADS * q;
+        const int r = (pc % RQ) * 4;
+        const int kb = pc / RQ;  // which 16-byte chunk of the stage
+        if constexpr (BF) {
+          // 8 K-rows x 4 bf16: two K-rows per i32x4 (low pair from even, high pair from odd)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int k = k0 + kb * 8 + 2 * i;
+            uint2 e = make_uint2(0u, 0u), o = make_uint2(0u, 0u);
+            if (r < rows_valid && k < k_valid) e = *reinterpret_cast<const uint2*>(base + (int64_t)k * ld + r);
+            if (r < rows_valid && k + 1 < k_valid) o = *reinterpret_cast<const uint2*>(base + (int64_t)(k + 1) * ld + r);
+            v[q * 4 + i] = i32x4{(int)e.x, (int)e.y, (int)o.x, (int)o.y};
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int k = k0 + kb * 4 + i;
+            if (r < rows_valid && k < k_valid)
+              v[q * 4 + i] = *reinterpret_cast<const i32x4*>(base + (int64_t)k * ld + r);
+            else
+              v[q * 4 + i] = i32x4{0, 0, 0, 0};
+          }
+        }
       }
     }
   }
@@ -79,76 +117,93 @@ struct Stager {
   __device__ __forceinline__ void store(char* lds) const {
     const int t = threadIdx.x;
     if constexpr (KCONTIG) {
-      const int vc = t & 7;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = (t >> 3) + 32 * q;
-        *reinterpret_cast<i32x4*>(lds + r * kLdsStride + vc * 16) = v[q];
-      }
-    } else if constexpr (sizeof(T) == 2) {
-      // v[q] holds 8 bf16 of K-row q; row r' of the tile gets (v[0][r'], .., v[3][r']).
-      const int rc = t % 16, kq = t / 16;
-      const uint16_t* s0 = reinterpret_cast<const uint16_t*>(&v[0]);
-      const uint16_t* s1 = reinterpret_cast<const uint16_t*>(&v[1]);
-      const uint16_t* s2 = reinterpret_cast<const uint16_t*>(&v[2]);
-      const uint16_t* s3 = reinterpret_cast<const uint16_t*>(&v[3]);
-#pragma unroll
-      for (int rr = 0; rr < 8; ++rr) {
-        uint32_t lo = (uint32_t)s0[rr] | ((uint32_t)s1[rr] << 16);
-        uint32_t hi = (uint32_t)s2[rr] | ((uint32_t)s3[rr] << 16);
-        uint2 w = make_uint2(lo, hi);
-        *reinterpret_cast<uint2*>(lds + (rc * 8 + rr) * kLdsStride + kq * 8) = w;
+      for (int q = 0; q < NV; ++q) {
+        const int vi = t + THREADS * q;
+        *reinterpret_cast<i32x4*>(lds + swz(vi >> 3, vi & 7)) = v[q];
       }
     } else {
-      const int rc = t % 32, kq = t / 32;
-      const floatx4 s0 = __builtin_bit_cast(floatx4, v[0]);
-      const floatx4 s1 = __builtin_bit_cast(floatx4, v[1]);
-      const floatx4 s2 = __builtin_bit_cast(floatx4, v[2]);
-      const floatx4 s3 = __builtin_bit_cast(floatx4, v[3]);
-      const floatx4 w0 = {s0[0], s1[0], s2[0], s3[0]};
-      const floatx4 w1 = {s0[1], s1[1], s2[1], s3[1]};
-      const floatx4 w2 = {s0[2], s1[2], s2[2], s3[2]};
-      const floatx4 w3 = {s0[3], s1[3], s2[3], s3[3]};
-      char* dst = lds + (rc * 4) * kLdsStride + kq * 16;
-      *reinterpret_cast<floatx4*>(dst) = w0;
-      *reinterpret_cast<floatx4*>(dst + kLdsStride) = w1;
-      *reinterpret_cast<floatx4*>(dst + 2 * kLdsStride) = w2;
-      *reinterpret_cast<floatx4*>(dst + 3 * kLdsStride) = w3;
+      constexpr int RQ = ROWS / 4;
+#pragma unroll
+      for (int q = 0; q < NPIECE; ++q) {
+        const int pc = t + THREADS * q;
+        const int r0 = (pc % RQ) * 4;
+        const int kb = pc / RQ;
+        if constexpr (BF) {
+          // v[q*4+i] = (K-row 2i: rows r0..r0+3 as 2 words, K-row 2i+1: 2 words).
+          // Output row j = 8 consecutive K values: word p = (K-row 2p, K-row 2p+1) of row j.
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int word = j >> 1;
+            const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+            uint32_t o[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+              const uint32_t a = (uint32_t)v[q * 4 + p][word];      // K-row 2p
+              const uint32_t c = (uint32_t)v[q * 4 + p][2 + word];  // K-row 2p+1
+              o[p] = __builtin_amdgcn_perm(c, a, sel);
+            }
+            *reinterpret_cast<i32x4*>(lds + swz(r0 + j, kb)) = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+          }
+        } else {
+          const i32x4 s0 = v[q * 4 + 0], s1 = v[q * 4 + 1], s2 = v[q * 4 + 2], s3 = v[q * 4 + 3];
+          *reinterpret_cast<i32x4*>(lds + swz(r0 + 0, kb)) = i32x4{s0[0], s1[0], s2[0], s3[0]};
+          *reinterpret_cast<i32x4*>(lds + swz(r0 + 1, kb)) = i32x4{s0[1], s1[1], s2[1], s3[1]};
+          *reinterpret_cast<i32x4*>(lds + swz(r0 + 2, kb)) = i32x4{s0[2], s1[2], s2[2], s3[2]};
+          *reinterpret_cast<i32x4*>(lds + swz(r0 + 3, kb)) = i32x4{s0[3], s1[3], s2[3], s3[3]};
+        }
+      }
+    }
+  }
+
+  // Squared norms of the K-contiguous rows this thread staged: xs[q] gets row
+  // (threadIdx.x + THREADS * q) >> 3; the 8 lanes sharing a row together hold its full norm.
+  __device__ __forceinline__ void add_sq(float* xs) const {
+    static_assert(KCONTIG, "row norms need a K-contiguous operand");
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const T* e = reinterpret_cast<const T*>(&v[q]);
+#pragma unroll
+      for (int z = 0; z < EPV; ++z) {
+        const float f = to_f32(e[z]);
+        xs[q] += f * f;
+      }
     }
   }
 };
 
-// ------------------------------------------------------------------ MFMA step
+// ------------------------------------------------------------------ MFMA stage
 
-template <typename T>
+template <class C>
 __device__ __forceinline__ void mfma_stage(const char* ldsA, const char* ldsB,
-                                           floatx4 (&acc)[4][4]) {
+                                           floatx4 (&acc)[C::MI][C::NJ]) {
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / C::WAVES_N, wn = w % C::WAVES_N;
   const int lr = l & 15, lg = l >> 4;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    i32x4 a[4], b[4];
+  for (int s = 0; s < 2; ++s) {
+    const int chunk = 4 * s + lg;
+    i32x4 a[C::MI], b[C::NJ];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = *reinterpret_cast<const i32x4*>(ldsA + (wm * 64 + 16 * i + lr) * kLdsStride + c * 64 + lg * 16);
+    for (int i = 0; i < C::MI; ++i)
+      a[i] = *reinterpret_cast<const i32x4*>(ldsA + swz(wm * C::WM + 16 * i + lr, chunk));
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      b[j] = *reinterpret_cast<const i32x4*>(ldsB + (wn * 64 + 16 * j + lr) * kLdsStride + c * 64 + lg * 16);
+    for (int j = 0; j < C::NJ; ++j)
+      b[j] = *reinterpret_cast<const i32x4*>(ldsB + swz(wn * C::WN + 16 * j + lr, chunk));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < C::MI; ++i) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if constexpr (sizeof(T) == 2) {
+      for (int j = 0; j < C::NJ; ++j) {
+        if constexpr (sizeof(typename C::type) == 2) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
               __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
         } else {
           const floatx4 af = __builtin_bit_cast(floatx4, a[i]);
           const floatx4 bf = __builtin_bit_cast(floatx4, b[j]);
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[s], bf[s], acc[i][j], 0, 0, 0);
+          for (int e = 0; e < 4; ++e)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[e], bf[e], acc[i][j], 0, 0, 0);
         }
       }
     }
@@ -156,47 +211,32 @@ __device__ __forceinline__ void mfma_stage(const char* ldsA, const char* ldsB,
 }
 
 // Full K loop for one tile.  A rows [0, a_rows), B rows [0, b_rows), K positions [0, k_len).
-// With ROWNORM (K-contiguous A only) xs[q] accumulates the squared norm of the part of A
-// row (threadIdx.x >> 3) + 32 q that this thread staged; the 8 lanes sharing a row together
-// hold the full norm.
-template <typename T>
-__device__ __forceinline__ void add_sq(const i32x4 (&v)[4], float* xs) {
-  constexpr int EPV = Elt<T>::per_vec;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const T* e = reinterpret_cast<const T*>(&v[q]);
-#pragma unroll
-    for (int z = 0; z < EPV; ++z) {
-      const float f = to_f32(e[z]);
-      xs[q] += f * f;
-    }
-  }
-}
-
-template <typename T, bool A_KC, bool B_KC, bool ROWNORM = false>
-__device__ __forceinline__ void gemm_tile(const T* __restrict__ A, int64_t lda, int a_rows,
-                                          const T* __restrict__ B, int64_t ldb, int b_rows,
-                                          int k_len, char* smem, floatx4 (&acc)[4][4],
+// With ROWNORM (K-contiguous A only) xs[] collects squared row norms of A (see add_sq).
+template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
+__device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
+                                          const typename C::type* __restrict__ B, int64_t ldb, int b_rows,
+                                          int k_len, char* smem, floatx4 (&acc)[C::MI][C::NJ],
                                           float* xs = nullptr) {
-  static_assert(!ROWNORM || A_KC, "row norms need a K-contiguous A");
+  using T = typename C::type;
+  using SA = Stager<T, C::BM, C::THREADS, A_KC>;
+  using SB = Stager<T, C::BN, C::THREADS, B_KC>;
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
   if constexpr (ROWNORM) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) xs[q] = 0.f;
+    for (int q = 0; q < SA::NV; ++q) xs[q] = 0.f;
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  constexpr int BK = Elt<T>::bk;
-  const int nk = (int)cdiv(k_len, BK);
+  const int nk = (int)cdiv(k_len, C::BK);
   if (nk == 0) return;
-  Stager<T, A_KC> sa;
-  Stager<T, B_KC> sb;
-  char* bufA[2] = {smem, smem + kOperandBytes};
-  char* bufB[2] = {smem + 2 * kOperandBytes, smem + 3 * kOperandBytes};
+  SA sa;
+  SB sb;
+  char* bufA[2] = {smem, smem + C::A_BYTES};
+  char* bufB[2] = {smem + 2 * C::A_BYTES, smem + 2 * C::A_BYTES + C::B_BYTES};
   sa.load(A, lda, a_rows, 0, k_len);
   sb.load(B, ldb, b_rows, 0, k_len);
-  if constexpr (ROWNORM) add_sq<T>(sa.v, xs);
+  if constexpr (ROWNORM) sa.add_sq(xs);
   sa.store(bufA[0]);
   sb.store(bufB[0]);
   __syncthreads();
@@ -204,12 +244,12 @@ __device__ __forceinline__ void gemm_tile(const T* __restrict__ A, int64_t lda, 
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {
-      sa.load(A, lda, a_rows, (kt + 1) * BK, k_len);
-      sb.load(B, ldb, b_rows, (kt + 1) * BK, k_len);
+      sa.load(A, lda, a_rows, (kt + 1) * C::BK, k_len);
+      sb.load(B, ldb, b_rows, (kt + 1) * C::BK, k_len);
     }
-    mfma_stage<T>(bufA[cur], bufB[cur], acc);
+    mfma_stage<C>(bufA[cur], bufB[cur], acc);
     if (more) {
-      if constexpr (ROWNORM) add_sq<T>(sa.v, xs);
+      if constexpr (ROWNORM) sa.add_sq(xs);
       sa.store(bufA[cur ^ 1]);
       sb.store(bufB[cur ^ 1]);
     }
@@ -223,9 +263,9 @@ __device__ __forceinline__ void gemm_tile(const T* __restrict__ A, int64_t lda, 
 struct TileCoord {
   int group;      // expert id (0 for ungrouped problems)
   int64_t m0;     // first output row (global, in the row space of A / C)
-  int m_rows;     // valid rows in this tile (<= 128)
+  int m_rows;     // valid rows in this tile
   int n0;         // first output column
-  int n_cols;     // valid columns (<= 128)
+  int n_cols;     // valid columns
   int64_t k0;     // first reduction index (grouped-K problems)
   int k_len;      // reduction length
   bool valid;
@@ -233,10 +273,11 @@ struct TileCoord {
 
 // Plain problem: M x N tiles, bands of `band` m-tiles walked m-fastest so that concurrently
 // running workgroups share both operand tiles in the caches.
+template <class C>
 __device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
   TileCoord tc;
-  const int64_t mt = cdiv(M, kBM);
-  const int nt = (int)cdiv(N, kBN);
+  const int64_t mt = cdiv(M, C::BM);
+  const int nt = (int)cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
   constexpr int band = 16;
   const int64_t band_tiles = (int64_t)band * nt;
@@ -247,25 +288,26 @@ __device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
   const int64_t mi = m_first + in % bm;
   const int ni = (int)(in / bm);
   tc.group = 0;
-  tc.m0 = mi * kBM;
-  tc.n0 = ni * kBN;
+  tc.m0 = mi * C::BM;
+  tc.n0 = ni * C::BN;
   tc.valid = (mi < mt) && (ni < nt);
-  tc.m_rows = (int)((M - tc.m0) < kBM ? (M - tc.m0) : kBM);
-  tc.n_cols = (N - tc.n0) < kBN ? (N - tc.n0) : kBN;
+  tc.m_rows = (int)((M - tc.m0) < C::BM ? (M - tc.m0) : C::BM);
+  tc.n_cols = (N - tc.n0) < C::BN ? (N - tc.n0) : C::BN;
   tc.k0 = 0;
   tc.k_len = K;
   return tc;
 }
 
 // Row-grouped problem (experts' forward / input-gradient GEMMs): group e owns rows
-// [seg[e], seg[e+1]) of A and C.  tile_start[e] = number of m-tiles of groups < e (prefix,
-// tile_start[G] = total).  Launched over an upper bound of m-tiles x n-tiles; the excess
-// workgroups find no tile and exit.
+// [seg[e], seg[e+1]) of A and C.  tile_start[e] = number of BM-row tiles of groups < e
+// (prefix, tile_start[G] = total).  Launched over an upper bound of m-tiles x n-tiles; the
+// excess workgroups find no tile and exit.
+template <class C>
 __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ seg,
-                                                  const int32_t* __restrict__ tile_start, int G,
-                                                  int N, int K) {
+                                                  const int32_t* __restrict__ tile_start, int G, int N,
+                                                  int K) {
   TileCoord tc;
-  const int nt = (int)cdiv(N, kBN);
+  const int nt = (int)cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
   const int64_t mtile = b / nt;
   const int ni = (int)(b - mtile * nt);
@@ -281,10 +323,10 @@ __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ se
   const int64_t local = mtile - tile_start[e];
   const int64_t rows = seg[e + 1] - seg[e];
   tc.group = e;
-  tc.m0 = seg[e] + local * kBM;
-  tc.m_rows = (int)((rows - local * kBM) < kBM ? (rows - local * kBM) : kBM);
-  tc.n0 = ni * kBN;
-  tc.n_cols = (N - tc.n0) < kBN ? (N - tc.n0) : kBN;
+  tc.m0 = seg[e] + local * C::BM;
+  tc.m_rows = (int)((rows - local * C::BM) < C::BM ? (rows - local * C::BM) : C::BM);
+  tc.n0 = ni * C::BN;
+  tc.n_cols = (N - tc.n0) < C::BN ? (N - tc.n0) : C::BN;
   tc.k0 = 0;
   tc.k_len = K;
   tc.valid = tc.m_rows > 0;
@@ -293,10 +335,10 @@ __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ se
 
 // Reduction-grouped problem (experts' weight gradients): group e reduces over the rows
 // [seg[e], seg[e+1]) of both operands; output tile (m, n) of group e.
-__device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ seg, int G, int M,
-                                                  int N) {
+template <class C>
+__device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ seg, int G, int M, int N) {
   TileCoord tc;
-  const int mt = (int)cdiv(M, kBM), nt = (int)cdiv(N, kBN);
+  const int mt = (int)cdiv(M, C::BM), nt = (int)cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
   const int per = mt * nt;
   const int e = (int)(b / per);
@@ -304,10 +346,10 @@ __device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ se
   const int mi = in / nt, ni = in % nt;
   tc.group = e;
   tc.valid = e < G;
-  tc.m0 = (int64_t)mi * kBM;
-  tc.m_rows = (M - mi * kBM) < kBM ? (M - mi * kBM) : kBM;
-  tc.n0 = ni * kBN;
-  tc.n_cols = (N - tc.n0) < kBN ? (N - tc.n0) : kBN;
+  tc.m0 = (int64_t)mi * C::BM;
+  tc.m_rows = (M - mi * C::BM) < C::BM ? (M - mi * C::BM) : C::BM;
+  tc.n0 = ni * C::BN;
+  tc.n_cols = (N - tc.n0) < C::BN ? (N - tc.n0) : C::BN;
   if (tc.valid) {
     tc.k0 = seg[e];
     tc.k_len = seg[e + 1] - seg[e];
@@ -320,17 +362,18 @@ __device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ se
 
 // ------------------------------------------------------------------ epilogue helpers
 
+template <class C>
 struct Frag {
   int wm, wn, lr, lg;
   __device__ __forceinline__ Frag() {
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-    wm = w >> 1;
-    wn = w & 1;
+    wm = w / C::WAVES_N;
+    wn = w % C::WAVES_N;
     lr = l & 15;
     lg = l >> 4;
   }
-  __device__ __forceinline__ int row(int i, int r) const { return wm * 64 + 16 * i + 4 * lg + r; }
-  __device__ __forceinline__ int col(int j) const { return wn * 64 + 16 * j + lr; }
+  __device__ __forceinline__ int row(int i, int r) const { return wm * C::WM + 16 * i + 4 * lg + r; }
+  __device__ __forceinline__ int col(int j) const { return wn * C::WN + 16 * j + lr; }
 };
 
 }  // namespace hmoe

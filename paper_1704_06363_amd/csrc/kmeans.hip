@@ -28,42 +28,43 @@ __global__ void __launch_bounds__(256) k_cnorm(const T* __restrict__ C, int K, i
 
 // ------------------------------------------------------------------ distance GEMM + argmin
 
-// One 128-row x 128-centre tile: dist'(i, k) = |c_k|^2 - 2 x_i . c_k (the |x_i|^2 term is
+// One BM-row x BN-centre tile: dist'(i, k) = |c_k|^2 - 2 x_i . c_k (the |x_i|^2 term is
 // common to the row); the tile's minimum per row (lowest k on ties) goes either straight to
 // assign / min_dist (all centres in one tile) or to per-tile partials merged afterwards.
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_assign(const T* __restrict__ X, int64_t n, int d, const T* __restrict__ C, int K,
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_assign(const typename C::type* __restrict__ X, int64_t n, int d, const typename C::type* __restrict__ Cn, int K,
              const float* __restrict__ cn, int32_t* __restrict__ assign, float* __restrict__ min_dist,
              float* __restrict__ part_v, int32_t* __restrict__ part_i, float* __restrict__ xnorm) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_plain(n, K, d);
+  constexpr int NV = C::BM * 8 / C::THREADS;  // staged A vectors per thread
+  const TileCoord tc = tile_plain<C>(n, K, d);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  float xs[4];
-  gemm_tile<T, true, true, true>(X + tc.m0 * d, d, tc.m_rows, C + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem,
-                                 acc, xs);
-  float* xn = reinterpret_cast<float*>(smem);  // [128]
-  float* rv = xn + 128;                         // [2][128]
-  int32_t* ri = reinterpret_cast<int32_t*>(rv + 256);
+  floatx4 acc[C::MI][C::NJ];
+  float xs[NV];
+  gemm_tile<C, true, true, true>(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem, acc,
+                                 xs);
+  float* xn = reinterpret_cast<float*>(smem);  // [BM]
+  float* rv = xn + C::BM;                       // [WAVES_N][BM]
+  int32_t* ri = reinterpret_cast<int32_t*>(rv + C::WAVES_N * C::BM);
   const int t = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < NV; ++q) {
     float s = xs[q];
     s += shfl_xor(s, 1);
     s += shfl_xor(s, 2);
     s += shfl_xor(s, 4);
-    if ((t & 7) == 0) xn[(t >> 3) + 32 * q] = s;
+    if ((t & 7) == 0) xn[(t + C::THREADS * q) >> 3] = s;
   }
-  const Frag f;
+  const Frag<C> f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < C::MI; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float best = FLT_MAX;
       int bi = INT_MAX;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col < tc.n_cols) argmin_merge(best, bi, cn[tc.n0 + col] - 2.f * acc[i][j][r], tc.n0 + col);
       }
@@ -74,26 +75,27 @@ __global__ void __launch_bounds__(256, 2)
         argmin_merge(best, bi, v2, i2);
       }
       if (f.lr == 0) {
-        rv[f.wn * 128 + f.row(i, r)] = best;
-        ri[f.wn * 128 + f.row(i, r)] = bi;
+        rv[f.wn * C::BM + f.row(i, r)] = best;
+        ri[f.wn * C::BM + f.row(i, r)] = bi;
       }
     }
   }
   __syncthreads();
-  if (t < tc.m_rows) {
-    float v = rv[t];
-    int bi = ri[t];
-    argmin_merge(v, bi, rv[128 + t], ri[128 + t]);
-    const int64_t row = tc.m0 + t;
-    const int nt = (int)cdiv(K, kBN);
+  const int nt = (int)cdiv(K, C::BN);
+  for (int q = t; q < tc.m_rows; q += C::THREADS) {
+    float v = rv[q];
+    int bi = ri[q];
+#pragma unroll
+    for (int w = 1; w < C::WAVES_N; ++w) argmin_merge(v, bi, rv[w * C::BM + q], ri[w * C::BM + q]);
+    const int64_t row = tc.m0 + q;
     if (nt == 1) {
       assign[row] = bi;
-      if (min_dist) min_dist[row] = fmaxf(v + xn[t], 0.f);
+      if (min_dist) min_dist[row] = fmaxf(v + xn[q], 0.f);
     } else {
-      const int ti = tc.n0 / kBN;
+      const int ti = tc.n0 / C::BN;
       part_v[(int64_t)ti * n + row] = v;
       part_i[(int64_t)ti * n + row] = bi;
-      if (ti == 0) xnorm[row] = xn[t];
+      if (ti == 0) xnorm[row] = xn[q];
     }
   }
 }
@@ -111,9 +113,12 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
   if (min_dist) min_dist[row] = fmaxf(v + xnorm[row], 0.f);
 }
 
-static size_t assign_ws_bytes(int64_t n, int32_t K) {
+// Centre-tile width of the assignment: bf16 with many centres runs the 256 x 256 engine.
+static int assign_bn(hmoe_dtype_t dt, int32_t K) { return (dt == HMOE_BF16 && K > 128) ? CfgBig::BN : 128; }
+
+static size_t assign_ws_bytes(int64_t n, int32_t K, hmoe_dtype_t dt) {
   Workspace ws(nullptr, 0);
-  const int nt = (int)cdiv(K, kBN);
+  const int nt = (int)cdiv(K, assign_bn(dt, K));
   ws.take<float>(K);
   if (nt > 1) {
     ws.take<float>((size_t)nt * n);
@@ -123,10 +128,11 @@ static size_t assign_ws_bytes(int64_t n, int32_t K) {
   return ws.off;
 }
 
-template <typename T>
-static int assign_t(const T* X, int64_t n, int32_t d, const T* C, int32_t K, int32_t* assign, float* min_dist,
-                    Workspace& ws, hipStream_t st) {
-  const int nt = (int)cdiv(K, kBN);
+template <class C>
+static int assign_t(const typename C::type* X, int64_t n, int32_t d, const typename C::type* Cn, int32_t K,
+                    int32_t* assign, float* min_dist, Workspace& ws, hipStream_t st) {
+  using T = typename C::type;
+  const int nt = (int)cdiv(K, C::BN);
   float* cn = ws.take<float>(K);
   float *pv = nullptr, *xn = nullptr;
   int32_t* pi = nullptr;
@@ -136,23 +142,25 @@ static int assign_t(const T* X, int64_t n, int32_t d, const T* C, int32_t K, int
     xn = ws.take<float>(n);
   }
   if (!ws.fits()) return HMOE_EWORKSPACE;
-  HMOE_LAUNCH("centre norms", k_cnorm<T>, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, C, K, d, cn);
+  HMOE_LAUNCH("centre norms", k_cnorm<T>, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, Cn, K, d, cn);
   if (n == 0) return HMOE_OK;
-  const int64_t tiles = cdiv(n, kBM) * nt;
-  HMOE_LAUNCH("assign", k_assign<T>, dim3((unsigned)tiles), dim3(kThreads), kGemmLds, st, X, n, d, C, K, cn,
-                     assign, min_dist, pv, pi, xn);
-  if (nt > 1) {
-    HMOE_LAUNCH("assign merge", k_assign_merge, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, pv, pi, xn, n, nt, assign,
-                       min_dist);
-  }
+  const int64_t tiles = cdiv(n, C::BM) * nt;
+  HMOE_LAUNCH("assign", k_assign<C>, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, st, X, n, d, Cn, K, cn, assign,
+              min_dist, pv, pi, xn);
+  if (nt > 1)
+    HMOE_LAUNCH("assign merge", k_assign_merge, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, pv, pi, xn, n, nt,
+                assign, min_dist);
   return HMOE_OK;
 }
 
 int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K, int32_t* assign,
                   float* min_dist, Workspace& ws, hipStream_t st) {
-  if (dt == HMOE_BF16)
-    return assign_t<bf16>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
-  return assign_t<float>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
+  if (dt == HMOE_BF16) {
+    if (assign_bn(dt, K) == CfgBig::BN)
+      return assign_t<CfgBig>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+    return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+  }
+  return assign_t<CfgSmall<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
 }
 
 // ------------------------------------------------------------------ k-means++ seeding
@@ -458,11 +466,11 @@ size_t fit_ws_bytes(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt) {
   ws.take<double>(n);                       // D^2 for k-means++
   ws.take<double>(cdiv(n, kKppRows));       // block sums
   ws.take<int32_t>(K);                      // picks when the caller passes none
-  size_t s = ws.off + update_scratch(n, d, K) + assign_ws_bytes(n, K) + 4096;
+  size_t s = ws.off + update_scratch(n, d, K) + assign_ws_bytes(n, K, dt) + 4096;
   return s;
 }
 
-size_t assign_ws(int64_t n, int32_t K) { return assign_ws_bytes(n, K) + 256; }
+size_t assign_ws(int64_t n, int32_t K, hmoe_dtype_t dt) { return assign_ws_bytes(n, K, dt) + 256; }
 
 template <typename T>
 static int fit_t(const T* X, int64_t n, int32_t d, int32_t K, int32_t n_iter, const double* u, int32_t reseed,

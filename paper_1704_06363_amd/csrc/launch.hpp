@@ -22,7 +22,7 @@ int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, flo
                    Workspace& ws, hipStream_t st);
 
 // kmeans.hip
-size_t assign_ws(int64_t n, int32_t K);
+size_t assign_ws(int64_t n, int32_t K, hmoe_dtype_t dt);
 size_t fit_ws_bytes(int64_t n, int32_t d, int32_t K, hmoe_dtype_t dt);
 size_t update_ws_bytes(int64_t n, int32_t d, int32_t K);
 int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K,

@@ -22,24 +22,42 @@
 
 namespace hmoe {
 
+// Tile configuration per data type: bf16 runs the 256 x 256 engine, fp32 the 128 x 128 one.
+template <typename T>
+struct Pick {
+  using C = CfgSmall<float>;
+};
+template <>
+struct Pick<bf16> {
+  using C = CfgBig;
+};
+
 // ------------------------------------------------------------------ expert forward
 
 // LAYER 1: H1s[m] = relu(Xs[m] W1_e^T + b1_e).   LAYER 2: H[perm[m]] = H1s[m] W2_e^T + b2_e.
-template <typename T, int LAYER>
-__global__ void __launch_bounds__(256, 2)
-    k_expert_fwd(const T* __restrict__ A, const T* __restrict__ W, const T* __restrict__ bias,
-                 const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
-                 const int32_t* __restrict__ perm, T* __restrict__ out) {
+template <class C, int LAYER>
+__global__ void __launch_bounds__(C::THREADS)
+    k_expert_fwd(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
+                 const typename C::type* __restrict__ bias, const int32_t* __restrict__ seg,
+                 const int32_t* __restrict__ tile_start, int G, int N, int Kd, const int32_t* __restrict__ perm,
+                 typename C::type* __restrict__ out) {
+  using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_group_m(seg, tile_start, G, N, Kd);
+  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, true, true>(A + tc.m0 * Kd, Kd, tc.m_rows, W + ((int64_t)tc.group * N + tc.n0) * Kd, Kd,
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, true>(A + tc.m0 * Kd, Kd, tc.m_rows, W + ((int64_t)tc.group * N + tc.n0) * Kd, Kd,
                            tc.n_cols, Kd, smem, acc);
-  const Frag f;
+  const Frag<C> f;
   const T* be = bias ? bias + (int64_t)tc.group * N : nullptr;
+  float bv[C::NJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int j = 0; j < C::NJ; ++j) {
+    const int col = f.col(j);
+    bv[j] = (be && col < tc.n_cols) ? to_f32(be[tc.n0 + col]) : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
@@ -48,10 +66,10 @@ __global__ void __launch_bounds__(256, 2)
       const int64_t orow = LAYER == 1 ? m : (int64_t)perm[m];
       T* dst = out + orow * N + tc.n0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col >= tc.n_cols) continue;
-        float v = acc[i][j][r] + (be ? to_f32(be[tc.n0 + col]) : 0.f);
+        float v = acc[i][j][r] + bv[j];
         if (LAYER == 1) v = fmaxf(v, 0.f);
         dst[col] = from_f32<T>(v);
       }
@@ -61,56 +79,55 @@ __global__ void __launch_bounds__(256, 2)
 // ------------------------------------------------------------------ decoder forward
 
 // Per row and V-tile: m = max of the tile's logits, s = sum exp(logit - m).
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_dec_fwd(const T* __restrict__ H, const T* __restrict__ D, const T* __restrict__ bD, int64_t n, int V, int o,
-              float* __restrict__ pm, float* __restrict__ ps) {
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
+              const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
+              float* __restrict__ ps) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_plain(n, V, o);
+  const TileCoord tc = tile_plain<C>(n, V, o);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
-  const Frag f;
-  float bias[4];
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+  const Frag<C> f;
+  float bias[C::NJ];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < C::NJ; ++j) {
     const int col = f.col(j);
     bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
   }
-  float* rm = reinterpret_cast<float*>(smem);  // [2][128]
-  float* rs = rm + 256;                          // [2][128]
+  float* rm = reinterpret_cast<float*>(smem);  // [WAVES_N][BM]
+  float* rs = rm + C::WAVES_N * C::BM;         // [WAVES_N][BM]
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float v[4];
       float mx = -FLT_MAX;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v[j] = acc[i][j][r] + bias[j];
-        if (f.col(j) < tc.n_cols) mx = fmaxf(mx, v[j]);
-      }
+      for (int j = 0; j < C::NJ; ++j)
+        if (f.col(j) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[j]);
 #pragma unroll
       for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
       float s = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (f.col(j) < tc.n_cols) s += __expf(v[j] - mx);
+      for (int j = 0; j < C::NJ; ++j)
+        if (f.col(j) < tc.n_cols) s += __expf(acc[i][j][r] + bias[j] - mx);
 #pragma unroll
       for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
       if (f.lr == 0) {
-        rm[f.wn * 128 + f.row(i, r)] = mx;
-        rs[f.wn * 128 + f.row(i, r)] = s;
+        rm[f.wn * C::BM + f.row(i, r)] = mx;
+        rs[f.wn * C::BM + f.row(i, r)] = s;
       }
     }
   __syncthreads();
-  const int t = threadIdx.x;
-  if (t < tc.m_rows) {
-    float m0 = rm[t], s0 = rs[t];
-    const float m1 = rm[128 + t], s1 = rs[128 + t];
-    const float M = fmaxf(m0, m1);
-    const float S = s0 * __expf(m0 - M) + s1 * __expf(m1 - M);
-    const int64_t at = (int64_t)(tc.n0 / kBN) * n + tc.m0 + t;
+  for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
+    float M = rm[t];
+#pragma unroll
+    for (int w = 1; w < C::WAVES_N; ++w) M = fmaxf(M, rm[w * C::BM + t]);
+    float S = 0.f;
+#pragma unroll
+    for (int w = 0; w < C::WAVES_N; ++w) S += rs[w * C::BM + t] * __expf(rm[w * C::BM + t] - M);
+    const int64_t at = (int64_t)(tc.n0 / C::BN) * n + tc.m0 + t;
     pm[at] = M;
     ps[at] = S;
   }
@@ -153,72 +170,93 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
 // ------------------------------------------------------------------ decoder backward
 
 // g = (exp(logit - lse) - y) / n stored to G; per-tile column sums of g to part_db[mtile][V].
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_dec_grad(const T* __restrict__ H, const T* __restrict__ D, const T* __restrict__ bD, int64_t n, int V, int o,
-               const float* __restrict__ lse, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag,
-               float inv_n, T* __restrict__ G, float* __restrict__ part_db) {
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_grad(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
+               const typename C::type* __restrict__ bD, int64_t n, int V, int o, const float* __restrict__ lse,
+               const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag, float inv_n,
+               typename C::type* __restrict__ G, float* __restrict__ part_db) {
+  using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_plain(n, V, o);
+  const TileCoord tc = tile_plain<C>(n, V, o);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
-  const Frag f;
-  float bias[4];
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+  const Frag<C> f;
+  float bias[C::NJ];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < C::NJ; ++j) {
     const int col = f.col(j);
     bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
   }
-  const int wcol0 = tc.n0 + f.wn * 64;  // first column of this wave
+  // Per-row data of the tile, staged once in LDS (the operand buffers are free now).
+  constexpr int MAXT = 16;
+  float* s_lse = reinterpret_cast<float*>(smem);                // [BM]
+  int32_t* s_p0 = reinterpret_cast<int32_t*>(s_lse + C::BM);    // [BM]
+  int32_t* s_cnt = s_p0 + C::BM;                                // [BM]
+  int32_t* s_tag = s_cnt + C::BM;                               // [BM][MAXT]
+  float* cs = reinterpret_cast<float*>(s_tag + C::BM * MAXT);   // [WAVES_M][BN]
+  for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
+    const int64_t gr = tc.m0 + t;
+    const int32_t p0 = row_ptr[gr], cnt = row_ptr[gr + 1] - p0;
+    s_lse[t] = lse[gr];
+    s_p0[t] = p0;
+    s_cnt[t] = cnt;
+    for (int q = 0; q < cnt && q < MAXT; ++q) s_tag[t * MAXT + q] = tag[p0 + q];
+  }
+  __syncthreads();
+  const int wcol0 = tc.n0 + f.wn * C::WN;  // first column of this wave
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
       if (row >= tc.m_rows) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j][r] = 0.f;
+        for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = 0.f;
         continue;
       }
       const int64_t gr = tc.m0 + row;
-      const float L = lse[gr];
+      const float L = s_lse[row];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - L);
-      const int32_t p0 = row_ptr[gr], p1 = row_ptr[gr + 1];
-      const float y = 1.f / (float)(p1 - p0);
-      for (int32_t q = p0; q < p1; ++q) {
-        const int lc = tag[q] - wcol0;
-        if (lc >= 0 && lc < 64 && (lc & 15) == f.lr) {
+      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - L);
+      const int32_t cnt = s_cnt[row];
+      const float y = 1.f / (float)cnt;
+      for (int32_t q = 0; q < cnt; ++q) {
+        const int lc = (q < MAXT ? s_tag[row * MAXT + q] : tag[s_p0[row] + q]) - wcol0;
+        if (lc >= 0 && lc < C::WN && (lc & 15) == f.lr) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < C::NJ; ++j)
             if ((lc >> 4) == j) acc[i][j][r] -= y;
         }
       }
       T* dst = G + gr * V + tc.n0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         acc[i][j][r] *= inv_n;
         if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
       }
     }
-  // column sums over this tile's rows: lanes of one column group, then the two row waves
-  float* cs = reinterpret_cast<float*>(smem);  // [2][128]
+  // column sums over this tile's rows: lanes of one column group, then the row waves
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < C::NJ; ++j) {
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < C::MI; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) s += acc[i][j][r];
     s += shfl_xor(s, 16);
     s += shfl_xor(s, 32);
-    if (f.lg == 0) cs[f.wm * 128 + f.col(j)] = s;
+    if (f.lg == 0) cs[f.wm * C::BN + f.col(j)] = s;
   }
   __syncthreads();
-  const int t = threadIdx.x;
-  if (t < tc.n_cols) part_db[(tc.m0 / kBM) * (int64_t)V + tc.n0 + t] = cs[t] + cs[128 + t];
+  for (int t = threadIdx.x; t < tc.n_cols; t += C::THREADS) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < C::WAVES_M; ++w) s += cs[w * C::BN + t];
+    part_db[(tc.m0 / C::BM) * (int64_t)V + tc.n0 + t] = s;
+  }
 }
 
 __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int rows, int V,
@@ -231,25 +269,26 @@ __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ 
 }
 
 // dH = G D, written to expert order: dYs[inv[i]] = (G D)[i].
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_dec_dH(const T* __restrict__ G, const T* __restrict__ D, int64_t n, int V, int o,
-             const int32_t* __restrict__ inv, T* __restrict__ dYs) {
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_dH(const typename C::type* __restrict__ G, const typename C::type* __restrict__ D, int64_t n, int V, int o,
+             const int32_t* __restrict__ inv, typename C::type* __restrict__ dYs) {
+  using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_plain(n, o, V);
+  const TileCoord tc = tile_plain<C>(n, o, V);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
-  const Frag f;
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
+  const Frag<C> f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
       if (row >= tc.m_rows) continue;
       T* dst = dYs + (int64_t)inv[tc.m0 + row] * o + tc.n0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
       }
@@ -257,24 +296,25 @@ __global__ void __launch_bounds__(256, 2)
 }
 
 // dD = G^T H (fp32).
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_dec_dD(const T* __restrict__ G, const T* __restrict__ H, int64_t n, int V, int o, float* __restrict__ dD) {
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_dD(const typename C::type* __restrict__ G, const typename C::type* __restrict__ H, int64_t n, int V, int o,
+             float* __restrict__ dD) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_plain(V, o, (int)n);
+  const TileCoord tc = tile_plain<C>(V, o, (int)n);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
-  const Frag f;
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
+  const Frag<C> f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
       if (row >= tc.m_rows) continue;
       float* dst = dD + (tc.m0 + row) * o + tc.n0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col < tc.n_cols) dst[col] = acc[i][j][r];
       }
@@ -285,27 +325,27 @@ __global__ void __launch_bounds__(256, 2)
 
 // dW_e = A_e^T B_e over the rows of expert e (reduction-grouped; an empty expert writes zeros).
 //   A: [rows][M] (ld M), B: [rows][N] (ld N), out: [G][M][N] fp32.
-template <typename T>
-__global__ void __launch_bounds__(256, 2)
-    k_expert_wgrad(const T* __restrict__ A, const T* __restrict__ B, const int32_t* __restrict__ seg, int G, int M,
-                   int N, float* __restrict__ out) {
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_expert_wgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ B,
+                   const int32_t* __restrict__ seg, int G, int M, int N, float* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_group_k(seg, G, M, N);
+  const TileCoord tc = tile_group_k<C>(seg, G, M, N);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
                              smem, acc);
-  const Frag f;
+  const Frag<C> f;
   float* base = out + (int64_t)tc.group * M * N;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
       if (row >= tc.m_rows) continue;
       float* dst = base + (tc.m0 + row) * N + tc.n0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col < tc.n_cols) dst[col] = acc[i][j][r];
       }
@@ -315,20 +355,22 @@ __global__ void __launch_bounds__(256, 2)
 // Row-grouped input gradients.  MASK: dZ[m] = (dYs[m] W2_e) * [H1s[m] > 0], stored in expert
 // order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order.
 //   A: [rows][Kd] (ld Kd), W: [G][Kd][N] (the layer's [out][in] weights seen as [K][N]).
-template <typename T, bool MASK>
-__global__ void __launch_bounds__(256, 2)
-    k_expert_dgrad(const T* __restrict__ A, const T* __restrict__ W, const int32_t* __restrict__ seg,
-                   const int32_t* __restrict__ tile_start, int G, int N, int Kd, const T* __restrict__ H1s,
-                   const int32_t* __restrict__ perm, T* __restrict__ out) {
+template <class C, bool MASK>
+__global__ void __launch_bounds__(C::THREADS)
+    k_expert_dgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
+                   const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
+                   const typename C::type* __restrict__ H1s, const int32_t* __restrict__ perm,
+                   typename C::type* __restrict__ out) {
+  using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const TileCoord tc = tile_group_m(seg, tile_start, G, N, Kd);
+  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
   if (!tc.valid) return;
-  floatx4 acc[4][4];
-  gemm_tile<T, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
                             Kd, smem, acc);
-  const Frag f;
+  const Frag<C> f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = f.row(i, r);
@@ -338,7 +380,7 @@ __global__ void __launch_bounds__(256, 2)
       T* dst = out + orow * N + tc.n0;
       const T* hm = MASK ? H1s + m * N + tc.n0 : nullptr;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < C::NJ; ++j) {
         const int col = f.col(j);
         if (col >= tc.n_cols) continue;
         float v = acc[i][j][r];
@@ -353,16 +395,17 @@ __global__ void __launch_bounds__(256, 2)
 struct MoeShape {
   int64_t n;
   int K, d, h, o, V;
-  size_t es;
 };
 
 static MoeShape shape_of(const hmoe_moe_params_t* p, int64_t n) {
-  return MoeShape{n, p->K, p->d_in, p->d_hid, p->d_out, p->vocab, dtype_size(p->dt)};
+  return MoeShape{n, p->K, p->d_in, p->d_hid, p->d_out, p->vocab};
 }
 
+template <typename T>
 static size_t fwd_ws(const MoeShape& s) {
+  using C = typename Pick<T>::C;
   Workspace ws(nullptr, 0);
-  const int64_t ntv = cdiv(s.V, kBN);
+  const int64_t ntv = cdiv(s.V, C::BN);
   ws.take<int32_t>(s.K + 1);
   ws.take<float>((size_t)ntv * s.n);
   ws.take<float>((size_t)ntv * s.n);
@@ -370,20 +413,23 @@ static size_t fwd_ws(const MoeShape& s) {
   return ws.off;
 }
 
+template <typename T>
 static size_t bwd_ws(const MoeShape& s) {
+  using C = typename Pick<T>::C;
   Workspace ws(nullptr, 0);
   ws.take<int32_t>(s.K + 1);
-  ws.take<char>((size_t)s.n * s.V * s.es);
-  ws.take<char>((size_t)s.n * s.o * s.es);
-  ws.take<char>((size_t)s.n * s.h * s.es);
-  ws.take<float>((size_t)cdiv(s.n, kBM) * s.V);
+  ws.take<T>((size_t)s.n * s.V);
+  ws.take<T>((size_t)s.n * s.o);
+  ws.take<T>((size_t)s.n * s.h);
+  ws.take<float>((size_t)cdiv(s.n, C::BM) * s.V);
   const int w = s.h > s.o ? s.h : s.o;
   return ws.off + segsum_ws(s.n, s.K, w) + 256;
 }
 
 size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n) {
   const MoeShape s = shape_of(p, n);
-  const size_t a = fwd_ws(s), b = bwd_ws(s);
+  const size_t a = p->dt == HMOE_BF16 ? fwd_ws<bf16>(s) : fwd_ws<float>(s);
+  const size_t b = p->dt == HMOE_BF16 ? bwd_ws<bf16>(s) : bwd_ws<float>(s);
   return a > b ? a : b;
 }
 
@@ -391,8 +437,9 @@ template <typename T>
 static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
                      const hmoe_labels_t* y, T* H1s, T* H, float* lse, float* loss, float* loss_mean, Workspace& ws,
                      hipStream_t st) {
+  using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
-  const int ntv = (int)cdiv(s.V, kBN);
+  const int ntv = (int)cdiv(s.V, C::BN);
   int32_t* ts = ws.take<int32_t>(s.K + 1);
   float* pm = ws.take<float>((size_t)ntv * n);
   float* ps = ws.take<float>((size_t)ntv * n);
@@ -400,16 +447,16 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
   const T* D = (const T*)p->D;
-  HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
-  const int64_t mt_bound = cdiv(n, kBM) + s.K;
-  HMOE_LAUNCH("expert layer 1", (k_expert_fwd<T, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds, st,
-                     Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
-  HMOE_LAUNCH("expert layer 2", (k_expert_fwd<T, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
-                     (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
-  HMOE_LAUNCH("decoder forward", k_dec_fwd<T>, dim3((unsigned)(cdiv(n, kBM) * ntv)), dim3(kThreads), kGemmLds, st, (const T*)H, D,
-                     (const T*)p->bD, n, s.V, s.o, pm, ps);
+  HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
+  const int64_t mt_bound = cdiv(n, C::BM) + s.K;
+  HMOE_LAUNCH("expert layer 1", (k_expert_fwd<C, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
+              dim3(C::THREADS), C::LDS, st, Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
+  HMOE_LAUNCH("expert layer 2", (k_expert_fwd<C, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
+              dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
+  HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS, st,
+              (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps);
   HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
-                     (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
+              (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
 }
 
@@ -418,46 +465,47 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
                       const int32_t* inv, const hmoe_labels_t* y, const T* H1s, const T* H, const float* lse,
                       float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX, Workspace& ws,
                       hipStream_t st) {
+  using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
   int32_t* ts = ws.take<int32_t>(s.K + 1);
-  T* G = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.V * sizeof(T)));
-  T* dYs = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.o * sizeof(T)));
-  T* dZ = reinterpret_cast<T*>(ws.take<char>((size_t)n * s.h * sizeof(T)));
-  const int mt = (int)cdiv(n, kBM);
+  T* G = ws.take<T>((size_t)n * s.V);
+  T* dYs = ws.take<T>((size_t)n * s.o);
+  T* dZ = ws.take<T>((size_t)n * s.h);
+  const int mt = (int)cdiv(n, C::BM);
   float* pdb = ws.take<float>((size_t)mt * s.V);
   if (!ws.fits()) return HMOE_EWORKSPACE;
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
   const T* D = (const T*)p->D;
-  const int ntv = (int)cdiv(s.V, kBN);
+  const int ntv = (int)cdiv(s.V, C::BN);
   // decoder
-  HMOE_LAUNCH("decoder grad", k_dec_grad<T>, dim3((unsigned)(mt * ntv)), dim3(kThreads), kGemmLds, st, H, D, (const T*)p->bD, n,
-                     s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
-  if (dbD) {
-    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V, dbD);
-  }
-  HMOE_LAUNCH("decoder dH", k_dec_dH<T>, dim3((unsigned)(mt * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st, (const T*)G, D,
-                     n, s.V, s.o, inv, dYs);
-  HMOE_LAUNCH("decoder dD", k_dec_dD<T>, dim3((unsigned)(cdiv(s.V, kBM) * cdiv(s.o, kBN))), dim3(kThreads), kGemmLds, st,
-                     (const T*)G, H, n, s.V, s.o, dD);
+  HMOE_LAUNCH("decoder grad", k_dec_grad<C>, dim3((unsigned)(mt * ntv)), dim3(C::THREADS), C::LDS, st, H, D,
+              (const T*)p->bD, n, s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
+  if (dbD)
+    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V,
+                dbD);
+  HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
+              (const T*)G, D, n, s.V, s.o, inv, dYs);
+  HMOE_LAUNCH("decoder dD", k_dec_dD<C>, dim3((unsigned)(cdiv(s.V, C::BM) * cdiv(s.o, C::BN))), dim3(C::THREADS),
+              C::LDS, st, (const T*)G, H, n, s.V, s.o, dD);
   // experts
-  HMOE_TRY(launch_seg_tiles(offsets, s.K, kBM, ts, st));
+  HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
   const size_t mark = ws.off;
   if (db2) HMOE_TRY(launch_segsum<T, float>(dYs, s.o, nullptr, offsets, s.K, s.o, n, db2, 0, ws, st));
   ws.off = mark;
-  HMOE_LAUNCH("expert dW2", k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, kBM) * cdiv(s.h, kBN))),
-                     dim3(kThreads), kGemmLds, st, (const T*)dYs, H1s, offsets, s.K, s.o, s.h, dW2);
-  const int64_t mt_bound = cdiv(n, kBM) + s.K;
-  HMOE_LAUNCH("expert dH1", (k_expert_dgrad<T, true>), dim3((unsigned)(mt_bound * cdiv(s.h, kBN))), dim3(kThreads), kGemmLds,
-                     st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
+  HMOE_LAUNCH("expert dW2", k_expert_wgrad<C>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, C::BM) * cdiv(s.h, C::BN))),
+              dim3(C::THREADS), C::LDS, st, (const T*)dYs, H1s, offsets, s.K, s.o, s.h, dW2);
+  const int64_t mt_bound = cdiv(n, C::BM) + s.K;
+  HMOE_LAUNCH("expert dH1", (k_expert_dgrad<C, true>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
+              dim3(C::THREADS), C::LDS, st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
   if (db1) HMOE_TRY(launch_segsum<T, float>(dZ, s.h, nullptr, offsets, s.K, s.h, n, db1, 0, ws, st));
   ws.off = mark;
-  HMOE_LAUNCH("expert dW1", k_expert_wgrad<T>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, kBM) * cdiv(s.d, kBN))),
-                     dim3(kThreads), kGemmLds, st, (const T*)dZ, Xs, offsets, s.K, s.h, s.d, dW1);
-  if (dX) {
-    HMOE_LAUNCH("expert dX", (k_expert_dgrad<T, false>), dim3((unsigned)(mt_bound * cdiv(s.d, kBN))), dim3(kThreads),
-                       kGemmLds, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm, dX);
-  }
+  HMOE_LAUNCH("expert dW1", k_expert_wgrad<C>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, C::BM) * cdiv(s.d, C::BN))),
+              dim3(C::THREADS), C::LDS, st, (const T*)dZ, Xs, offsets, s.K, s.h, s.d, dW1);
+  if (dX)
+    HMOE_LAUNCH("expert dX", (k_expert_dgrad<C, false>), dim3((unsigned)(mt_bound * cdiv(s.d, C::BN))),
+                dim3(C::THREADS), C::LDS, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm,
+                dX);
   return HMOE_OK;
 }
 
