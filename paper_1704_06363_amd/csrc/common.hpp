@@ -15,6 +15,12 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
+// Types in LDS (address space 3).  Pointers into shared memory are kept in this address
+// space explicitly so that every access compiles to ds_read / ds_write (generic pointers
+// would become flat instructions that also wait on outstanding global loads).
+template <typename T>
+using lds = __attribute__((address_space(3))) T;
+
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
 

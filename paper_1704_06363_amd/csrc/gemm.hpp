@@ -114,13 +114,13 @@ struct Stager {
     }
   }
 
-  __device__ __forceinline__ void store(char* lds) const {
+  __device__ __forceinline__ void store(lds<char>* dst) const {
     const int t = threadIdx.x;
     if constexpr (KCONTIG) {
 #pragma unroll
       for (int q = 0; q < NV; ++q) {
         const int vi = t + THREADS * q;
-        *reinterpret_cast<i32x4*>(lds + swz(vi >> 3, vi & 7)) = v[q];
+        *reinterpret_cast<lds<i32x4>*>(dst + swz(vi >> 3, vi & 7)) = v[q];
       }
     } else {
       constexpr int RQ = ROWS / 4;
@@ -143,14 +143,14 @@ struct Stager {
               const uint32_t c = (uint32_t)v[q * 4 + p][2 + word];  // K-row 2p+1
               o[p] = __builtin_amdgcn_perm(c, a, sel);
             }
-            *reinterpret_cast<i32x4*>(lds + swz(r0 + j, kb)) = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+            *reinterpret_cast<lds<i32x4>*>(dst + swz(r0 + j, kb)) = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
           }
         } else {
           const i32x4 s0 = v[q * 4 + 0], s1 = v[q * 4 + 1], s2 = v[q * 4 + 2], s3 = v[q * 4 + 3];
-          *reinterpret_cast<i32x4*>(lds + swz(r0 + 0, kb)) = i32x4{s0[0], s1[0], s2[0], s3[0]};
-          *reinterpret_cast<i32x4*>(lds + swz(r0 + 1, kb)) = i32x4{s0[1], s1[1], s2[1], s3[1]};
-          *reinterpret_cast<i32x4*>(lds + swz(r0 + 2, kb)) = i32x4{s0[2], s1[2], s2[2], s3[2]};
-          *reinterpret_cast<i32x4*>(lds + swz(r0 + 3, kb)) = i32x4{s0[3], s1[3], s2[3], s3[3]};
+          *reinterpret_cast<lds<i32x4>*>(dst + swz(r0 + 0, kb)) = i32x4{s0[0], s1[0], s2[0], s3[0]};
+          *reinterpret_cast<lds<i32x4>*>(dst + swz(r0 + 1, kb)) = i32x4{s0[1], s1[1], s2[1], s3[1]};
+          *reinterpret_cast<lds<i32x4>*>(dst + swz(r0 + 2, kb)) = i32x4{s0[2], s1[2], s2[2], s3[2]};
+          *reinterpret_cast<lds<i32x4>*>(dst + swz(r0 + 3, kb)) = i32x4{s0[3], s1[3], s2[3], s3[3]};
         }
       }
     }
@@ -175,7 +175,7 @@ struct Stager {
 // ------------------------------------------------------------------ MFMA stage
 
 template <class C>
-__device__ __forceinline__ void mfma_stage(const char* ldsA, const char* ldsB,
+__device__ __forceinline__ void mfma_stage(const lds<char>* ldsA, const lds<char>* ldsB,
                                            floatx4 (&acc)[C::MI][C::NJ]) {
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -187,10 +187,10 @@ __device__ __forceinline__ void mfma_stage(const char* ldsA, const char* ldsB,
     i32x4 a[C::MI], b[C::NJ];
 #pragma unroll
     for (int i = 0; i < C::MI; ++i)
-      a[i] = *reinterpret_cast<const i32x4*>(ldsA + swz(wm * C::WM + 16 * i + lr, chunk));
+      a[i] = *reinterpret_cast<const lds<i32x4>*>(ldsA + swz(wm * C::WM + 16 * i + lr, chunk));
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j)
-      b[j] = *reinterpret_cast<const i32x4*>(ldsB + swz(wn * C::WN + 16 * j + lr, chunk));
+      b[j] = *reinterpret_cast<const lds<i32x4>*>(ldsB + swz(wn * C::WN + 16 * j + lr, chunk));
 #pragma unroll
     for (int i = 0; i < C::MI; ++i) {
 #pragma unroll
@@ -215,7 +215,7 @@ __device__ __forceinline__ void mfma_stage(const char* ldsA, const char* ldsB,
 template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
 __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
                                           const typename C::type* __restrict__ B, int64_t ldb, int b_rows,
-                                          int k_len, char* smem, floatx4 (&acc)[C::MI][C::NJ],
+                                          int k_len, lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
                                           float* xs = nullptr) {
   using T = typename C::type;
   using SA = Stager<T, C::BM, C::THREADS, A_KC>;
@@ -232,13 +232,13 @@ __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A
   if (nk == 0) return;
   SA sa;
   SB sb;
-  char* bufA[2] = {smem, smem + C::A_BYTES};
-  char* bufB[2] = {smem + 2 * C::A_BYTES, smem + 2 * C::A_BYTES + C::B_BYTES};
+  lds<char>* const bufA0 = smem;
+  lds<char>* const bufB0 = smem + 2 * C::A_BYTES;
   sa.load(A, lda, a_rows, 0, k_len);
   sb.load(B, ldb, b_rows, 0, k_len);
   if constexpr (ROWNORM) sa.add_sq(xs);
-  sa.store(bufA[0]);
-  sb.store(bufB[0]);
+  sa.store(bufA0);
+  sb.store(bufB0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
@@ -247,11 +247,11 @@ __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A
       sa.load(A, lda, a_rows, (kt + 1) * C::BK, k_len);
       sb.load(B, ldb, b_rows, (kt + 1) * C::BK, k_len);
     }
-    mfma_stage<C>(bufA[cur], bufB[cur], acc);
+    mfma_stage<C>(bufA0 + cur * C::A_BYTES, bufB0 + cur * C::B_BYTES, acc);
     if (more) {
       if constexpr (ROWNORM) sa.add_sq(xs);
-      sa.store(bufA[cur ^ 1]);
-      sb.store(bufB[cur ^ 1]);
+      sa.store(bufA0 + (cur ^ 1) * C::A_BYTES);
+      sb.store(bufB0 + (cur ^ 1) * C::B_BYTES);
     }
     __syncthreads();
   }

@@ -36,7 +36,8 @@ __global__ void __launch_bounds__(C::THREADS)
     k_assign(const typename C::type* __restrict__ X, int64_t n, int d, const typename C::type* __restrict__ Cn, int K,
              const float* __restrict__ cn, int32_t* __restrict__ assign, float* __restrict__ min_dist,
              float* __restrict__ part_v, int32_t* __restrict__ part_i, float* __restrict__ xnorm) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   constexpr int NV = C::BM * 8 / C::THREADS;  // staged A vectors per thread
   const TileCoord tc = tile_plain<C>(n, K, d);
   if (!tc.valid) return;
@@ -44,9 +45,9 @@ __global__ void __launch_bounds__(C::THREADS)
   float xs[NV];
   gemm_tile<C, true, true, true>(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem, acc,
                                  xs);
-  float* xn = reinterpret_cast<float*>(smem);  // [BM]
-  float* rv = xn + C::BM;                       // [WAVES_N][BM]
-  int32_t* ri = reinterpret_cast<int32_t*>(rv + C::WAVES_N * C::BM);
+  lds<float>* xn = reinterpret_cast<lds<float>*>(smem);  // [BM]
+  lds<float>* rv = xn + C::BM;                       // [WAVES_N][BM]
+  lds<int32_t>* ri = reinterpret_cast<lds<int32_t>*>(rv + C::WAVES_N * C::BM);
   const int t = threadIdx.x;
 #pragma unroll
   for (int q = 0; q < NV; ++q) {

@@ -42,7 +42,8 @@ __global__ void __launch_bounds__(C::THREADS)
                  const int32_t* __restrict__ tile_start, int G, int N, int Kd, const int32_t* __restrict__ perm,
                  typename C::type* __restrict__ out) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -84,7 +85,8 @@ __global__ void __launch_bounds__(C::THREADS)
     k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
               const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
               float* __restrict__ ps) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_plain<C>(n, V, o);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -96,8 +98,8 @@ __global__ void __launch_bounds__(C::THREADS)
     const int col = f.col(j);
     bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
   }
-  float* rm = reinterpret_cast<float*>(smem);  // [WAVES_N][BM]
-  float* rs = rm + C::WAVES_N * C::BM;         // [WAVES_N][BM]
+  lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // [WAVES_N][BM]
+  lds<float>* rs = rm + C::WAVES_N * C::BM;         // [WAVES_N][BM]
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
 #pragma unroll
@@ -177,7 +179,8 @@ __global__ void __launch_bounds__(C::THREADS)
                const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag, float inv_n,
                typename C::type* __restrict__ G, float* __restrict__ part_db) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_plain<C>(n, V, o);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -191,11 +194,11 @@ __global__ void __launch_bounds__(C::THREADS)
   }
   // Per-row data of the tile, staged once in LDS (the operand buffers are free now).
   constexpr int MAXT = 16;
-  float* s_lse = reinterpret_cast<float*>(smem);                // [BM]
-  int32_t* s_p0 = reinterpret_cast<int32_t*>(s_lse + C::BM);    // [BM]
-  int32_t* s_cnt = s_p0 + C::BM;                                // [BM]
-  int32_t* s_tag = s_cnt + C::BM;                               // [BM][MAXT]
-  float* cs = reinterpret_cast<float*>(s_tag + C::BM * MAXT);   // [WAVES_M][BN]
+  lds<float>* s_lse = reinterpret_cast<lds<float>*>(smem);                // [BM]
+  lds<int32_t>* s_p0 = reinterpret_cast<lds<int32_t>*>(s_lse + C::BM);    // [BM]
+  lds<int32_t>* s_cnt = s_p0 + C::BM;                                // [BM]
+  lds<int32_t>* s_tag = s_cnt + C::BM;                               // [BM][MAXT]
+  lds<float>* cs = reinterpret_cast<lds<float>*>(s_tag + C::BM * MAXT);   // [WAVES_M][BN]
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     const int64_t gr = tc.m0 + t;
     const int32_t p0 = row_ptr[gr], cnt = row_ptr[gr + 1] - p0;
@@ -274,7 +277,8 @@ __global__ void __launch_bounds__(C::THREADS)
     k_dec_dH(const typename C::type* __restrict__ G, const typename C::type* __restrict__ D, int64_t n, int V, int o,
              const int32_t* __restrict__ inv, typename C::type* __restrict__ dYs) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_plain<C>(n, o, V);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -300,7 +304,8 @@ template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_dD(const typename C::type* __restrict__ G, const typename C::type* __restrict__ H, int64_t n, int V, int o,
              float* __restrict__ dD) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_plain<C>(V, o, (int)n);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -329,7 +334,8 @@ template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_expert_wgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ B,
                    const int32_t* __restrict__ seg, int G, int M, int N, float* __restrict__ out) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_group_k<C>(seg, G, M, N);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
@@ -362,7 +368,8 @@ __global__ void __launch_bounds__(C::THREADS)
                    const typename C::type* __restrict__ H1s, const int32_t* __restrict__ perm,
                    typename C::type* __restrict__ out) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
