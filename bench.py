@@ -3,8 +3,9 @@
 One step = one routed training step on the balanced workload: gater assignment of 65,536
 bf16 feature rows (d = 2048) to the nearest of K = 16 centres, counting-sort dispatch, the
 16 expert MLPs 2048 -> 4096 -> 1024 with the shared 1024 -> 50,000 decoder, multilabel
-softmax loss, and the full backward pass (all parameter gradients and dX).  Inputs are
-seeded synthetic tensors already resident in HBM.
+softmax loss, and the full backward pass (all parameter gradients and dX; the forward saves
+the bf16 logits so the backward does not recompute them).  Inputs are seeded synthetic
+tensors already resident in HBM.
 
 Printed: one JSON line with the step throughput (samples/s), the roofline of the dominant
 kernel (HIP events recorded around every launch in the timed region), the fp64 CPU oracle
@@ -90,7 +91,8 @@ class RoutedStep:
                     "H": torch.empty(n, o, dtype=bf, device=dev),
                     "lse": torch.empty(n, dtype=torch.float32, device=dev),
                     "loss": torch.empty(n, dtype=torch.float32, device=dev),
-                    "loss_mean": torch.empty(1, dtype=torch.float32, device=dev)}
+                    "loss_mean": torch.empty(1, dtype=torch.float32, device=dev),
+                    "logits": torch.empty(n, V, dtype=bf, device=dev)}
         f32 = torch.float32
         self.grads = {"dW1": torch.empty(K, h, d, dtype=f32, device=dev),
                       "db1": torch.empty(K, h, dtype=f32, device=dev),
@@ -113,7 +115,8 @@ class RoutedStep:
         f = h.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], self.row_ptr, self.tag,
                           out=self.fwd, ws=self.ws)
         h.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], self.row_ptr,
-                       self.tag, f["H1_sorted"], f["H"], f["lse"], out=self.grads, ws=self.ws)
+                       self.tag, f["H1_sorted"], f["H"], f["lse"], out=self.grads, ws=self.ws,
+                       logits=f["logits"])
 
 
 def time_steps(fn, steps, warmup, timer=True):

@@ -143,28 +143,31 @@ typedef struct {
  *   perm int32[n] (slot -> sample).
  *   H1_sorted [n x d_hid] out: relu(W1_e x + b1_e) in expert order (saved for backward).
  *   H [n x d_out] out: expert outputs W2_e h1 + b2_e in SAMPLE order (the combine).
- *   lse float[n] out: log-sum-exp of the V logits D H_i + bD.
+ *   logits [n x vocab] out or NULL: D H_i + bD in dtype dt, saved so that the backward does
+ *     not recompute them (n * vocab * 2 bytes in bf16; pass NULL to save the memory).
+ *   lse float[n] out: log-sum-exp of the V logits (from the fp32 logits).
  *   loss float[n] out: lse_i - mean of the logits of the positive tags.
  *   loss_mean float[1] out: mean over the batch. */
 size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n);
 int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
                      const int32_t* offsets, const int32_t* perm, const hmoe_labels_t* y,
-                     void* H1_sorted, void* H, float* lse, float* loss, float* loss_mean,
-                     void* ws, size_t ws_bytes, void* stream);
+                     void* H1_sorted, void* H, void* logits, float* lse, float* loss,
+                     float* loss_mean, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward pass: gradients of loss_mean (the 1/n is included) with respect to every expert
  * and decoder parameter, and optionally the input features.  The gater is fixed (Section
  * 2.2), so nothing flows to the centres.  With p = softmax(D H_i + bD), y_i the target:
  *   g = (p - y)/n; dbD = sum g; dD = g^T H; dH = g D; per expert e: db2 = sum dH,
  *   dW2 = dH^T H1, dZ = (dH W2) * [H1 > 0]; db1 = sum dZ; dW1 = dZ^T X; dX = dZ W1.
- *   Inputs are the forward's saved tensors (H1_sorted, H, lse) and inv int32[n].
+ *   Inputs are the forward's saved tensors (H1_sorted, H, lse, and logits if it saved them:
+ *   then p is formed from the stored logits; NULL recomputes them from H) and inv int32[n].
  *   dW1, db1, dW2, db2, dD, dbD: float out (overwritten; experts without samples get 0);
  *   db1, db2, dbD may be NULL.  dX [n x d_in] in dtype dt, SAMPLE order, or NULL. */
 int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
                       const int32_t* offsets, const int32_t* perm, const int32_t* inv,
                       const hmoe_labels_t* y, const void* H1_sorted, const void* H,
-                      const float* lse, float* dW1, float* db1, float* dW2, float* db2,
-                      float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
+                      const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
+                      float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
 /* ------------------------------------------------------------------ diagnostics */

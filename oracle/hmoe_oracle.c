@@ -308,13 +308,14 @@ int hmoe_orc_dispatch(int64_t n, int32_t K, const int32_t* e, int32_t* counts,
  *   lse = log sum_j exp(l_j);  loss_i = lse - (1/|P_i|) sum_{j in P_i} l_j
  * The target mass is spread uniformly over the positive tags P_i (tags listed in
  * tag[row_ptr[i] .. row_ptr[i+1]), distinct); the batch loss is the mean over samples.
- * b1, b2, bD may be NULL (no bias).  probs (n x V) is optional. */
+ * b1, b2, bD may be NULL (no bias).  probs (n x V) is optional; logits (n x V), optional, receives
+ * the logits rounded by `store` (the tensor a device saves for the backward). */
 int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
                          const double* X, const int32_t* a, const double* W1, const double* b1,
                          const double* W2, const double* b2, const double* D,
                          const double* bD, const int32_t* row_ptr, const int32_t* tag,
                          int store, double* H1, double* H, double* lse, double* loss,
-                         double* loss_mean, double* probs) {
+                         double* loss_mean, double* probs, double* logits) {
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
   for (int64_t i = 0; i < n; ++i) {
     if (a[i] < 0 || a[i] >= K) return -3;
@@ -365,6 +366,8 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
       loss[i] = L - pos / (double)np;
       if (probs)
         for (int32_t v = 0; v < V; ++v) probs[i * (int64_t)V + v] = exp(lg[v] - L);
+      if (logits)
+        for (int32_t v = 0; v < V; ++v) logits[i * (int64_t)V + v] = store_round(lg[v], store);
     }
     free(lg);
   }
@@ -387,15 +390,16 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
  *   db2_e = sum dh,  dW2_e = sum dh h1^T,  dh1 = W2_e^T dh,  dz = dh1 * [h1 > 0]
  *   db1_e = sum dz,  dW1_e = sum dz x^T,   dx = W1_e^T dz
  * The activation gradients g (as used by dD and dh), dh, dz and dx are the tensors a device
- * stores and reads back; `store` rounds them (dbD sums the unrounded g).
+ * stores and reads back; `store` rounds them (dbD sums the unrounded g).  With logit_round the
+ * recomputed logits are rounded by `store` first, as when a device saved them in the forward.
  * Experts that receive no sample get zero gradients.  dX may be NULL. */
 int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
                           const double* X, const int32_t* a, const double* W1,
                           const double* W2, const double* D, const double* bD,
                           const int32_t* row_ptr, const int32_t* tag, const double* H1,
                           const double* H, const double* lse, double scale, int store,
-                          double* dW1, double* db1, double* dW2, double* db2, double* dD,
-                          double* dbD, double* dX) {
+                          int logit_round, double* dW1, double* db1, double* dW2, double* db2,
+                          double* dD, double* dbD, double* dX) {
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
   for (int64_t i = 0; i < n; ++i) {
     if (a[i] < 0 || a[i] >= K) return -3;
@@ -417,6 +421,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
       double s = bD ? bD[v] : 0.0;
       const double* dv = D + (int64_t)v * o;
       for (int32_t j = 0; j < o; ++j) s += dv[j] * y[j];
+      if (logit_round) s = store_round(s, store);
       g[v] = exp(s - lse[i]);
     }
     int32_t np = row_ptr[i + 1] - row_ptr[i];

@@ -165,7 +165,7 @@ def dispatch(e, K: int):
 
 
 def moe_forward(X, a, W1, b1, W2, b2, D, bD, row_ptr, tag, store: str = "f64",
-                want_probs: bool = False):
+                want_probs: bool = False, want_logits: bool = False):
     """Shared-decoder hard MoE forward with the multilabel softmax loss (Section 2, shared
     decoder; Section 4.1, Eq. 3).  Per-sample outputs in sample order."""
     X = _f64(X)
@@ -181,22 +181,26 @@ def moe_forward(X, a, W1, b1, W2, b2, D, bD, row_ptr, tag, store: str = "f64",
     H1 = np.empty((n, h)); H = np.empty((n, o)); lse = np.empty(n); loss = np.empty(n)
     lm = np.zeros(1)
     probs = np.empty((n, V)) if want_probs else None
+    logits = np.empty((n, V)) if want_logits else None
     rc = _load().hmoe_orc_moe_forward(
         ctypes.c_int64(n), ctypes.c_int32(d), ctypes.c_int32(h), ctypes.c_int32(o),
         ctypes.c_int32(V), ctypes.c_int32(K), _p(X), _p(a), _p(W1), _p(b1), _p(W2), _p(b2),
         _p(D), _p(bD), _p(row_ptr), _p(tag), ctypes.c_int(_STORE[store]), _p(H1), _p(H),
-        _p(lse), _p(loss), _p(lm), _p(probs))
+        _p(lse), _p(loss), _p(lm), _p(probs), _p(logits))
     _check(rc, "moe_forward")
     out = {"H1": H1, "H": H, "lse": lse, "loss": loss, "loss_mean": float(lm[0])}
     if want_probs:
         out["probs"] = probs
+    if want_logits:
+        out["logits"] = logits
     return out
 
 
 def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
-                 store: str = "f64", want_dX: bool = True):
+                 store: str = "f64", want_dX: bool = True, logit_round: bool = False):
     """Gradients of the mean loss w.r.t. every expert and decoder parameter (and X) given the
-    saved activations (Section 2; Section 4.1, Eq. 3; the gater gets none, Section 2.2)."""
+    saved activations (Section 2; Section 4.1, Eq. 3; the gater gets none, Section 2.2).
+    logit_round: the logits are taken as stored in `store` precision (saved-logits path)."""
     X = _f64(X)
     n, d = X.shape
     K, h, _ = W1.shape
@@ -215,7 +219,7 @@ def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
         ctypes.c_int64(n), ctypes.c_int32(d), ctypes.c_int32(h), ctypes.c_int32(o),
         ctypes.c_int32(V), ctypes.c_int32(K), _p(X), _p(a), _p(W1), _p(W2), _p(D), _p(bD),
         _p(row_ptr), _p(tag), _p(H1), _p(H), _p(lse), ctypes.c_double(scale),
-        ctypes.c_int(_STORE[store]), _p(dW1), _p(db1), _p(dW2), _p(db2), _p(dD), _p(dbD),
-        _p(dX))
+        ctypes.c_int(_STORE[store]), ctypes.c_int(1 if logit_round else 0), _p(dW1), _p(db1),
+        _p(dW2), _p(db2), _p(dD), _p(dbD), _p(dX))
     _check(rc, "moe_backward")
     return {"dW1": dW1, "db1": db1, "dW2": dW2, "db2": db2, "dD": dD, "dbD": dbD, "dX": dX}

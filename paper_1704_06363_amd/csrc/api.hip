@@ -297,8 +297,8 @@ size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n) {
 }
 
 int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
-                     const int32_t* perm, const hmoe_labels_t* y, void* H1_sorted, void* H, float* lse, float* loss,
-                     float* loss_mean, void* ws, size_t ws_bytes, void* stream) {
+                     const int32_t* perm, const hmoe_labels_t* y, void* H1_sorted, void* H, void* logits, float* lse,
+                     float* loss, float* loss_mean, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   HMOE_TRY(check_params(p));
   HMOE_TRY(check_n(n));
@@ -311,19 +311,20 @@ int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted
   HMOE_TRY(check_ptr("labels.tag", y->tag, false));
   HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
   HMOE_TRY(check_ptr("H", H));
+  if (logits) HMOE_TRY(check_ptr("logits", logits));
   HMOE_TRY(check_ptr("lse", lse, false));
   HMOE_TRY(check_ptr("loss", loss, false));
   HMOE_TRY(check_ptr("loss_mean", loss_mean, false));
   HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
   Workspace w(ws, ws_bytes);
-  return launch_moe_forward(p, n, X_sorted, offsets, perm, y, H1_sorted, H, lse, loss, loss_mean, w,
+  return launch_moe_forward(p, n, X_sorted, offsets, perm, y, H1_sorted, H, logits, lse, loss, loss_mean, w,
                             (hipStream_t)stream);
 }
 
 int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
                       const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1_sorted,
-                      const void* H, const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD,
-                      float* dbD, void* dX, void* ws, size_t ws_bytes, void* stream) {
+                      const void* H, const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
+                      float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   HMOE_TRY(check_params(p));
   HMOE_TRY(check_n(n));
@@ -352,11 +353,12 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
   HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
   HMOE_TRY(check_ptr("H", H));
   HMOE_TRY(check_ptr("lse", lse, false));
+  if (logits) HMOE_TRY(check_ptr("logits", logits));
   if (dX) HMOE_TRY(check_ptr("dX", dX));
   HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
   Workspace w(ws, ws_bytes);
-  return launch_moe_backward(p, n, X_sorted, offsets, perm, inv, y, H1_sorted, H, lse, dW1, db1, dW2, db2, dD, dbD,
-                             dX, w, (hipStream_t)stream);
+  return launch_moe_backward(p, n, X_sorted, offsets, perm, inv, y, H1_sorted, H, logits, lse, dW1, db1, dW2, db2,
+                             dD, dbD, dX, w, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -376,4 +376,54 @@ struct Frag {
   __device__ __forceinline__ int col(int j) const { return wn * C::WN + 16 * j + lr; }
 };
 
+// Epilogue store through LDS: the tile is written to LDS row-major (padded rows, conflict-free
+// for the accumulator layout) in bands of rows, then copied out so that every lane stores whole
+// 16-byte row segments.  Must be entered by the whole workgroup after the main loop.
+//   elem(i, j, r, v)            value to store for accumulator element (i, j, r) holding v
+//   rowmap(local_row)           destination row index (local_row < m_rows)
+//   vec(dst_row, local_row, col, raw)  last transform of a 16-byte vector (e.g. a mask)
+// n_cols must be a multiple of 16 / sizeof(O).
+struct NoVec {
+  __device__ __forceinline__ i32x4 operator()(int64_t, int, int, i32x4 v) const { return v; }
+};
+
+template <class C, typename O, class Elem, class RowMap, class Vec>
+__device__ __forceinline__ void store_tile(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                           lds<char>* smem, O* __restrict__ out, int64_t ldo, Elem elem,
+                                           RowMap rowmap, Vec vec) {
+  constexpr int ROWB = C::BN * (int)sizeof(O) + 16;
+  constexpr int FIT = C::LDS / ROWB;
+  constexpr int BAND = FIT >= 256 ? 256 : (FIT >= 128 ? 128 : (FIT >= 64 ? 64 : 32));
+  constexpr int VPR = C::BN * (int)sizeof(O) / 16;
+  constexpr int EPV = 16 / (int)sizeof(O);
+  const Frag<C> f;
+#pragma unroll
+  for (int b = 0; b < (C::BM + BAND - 1) / BAND; ++b) {
+    if (b * BAND >= tc.m_rows) break;
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = f.row(i, r) - b * BAND;
+        if (row < 0 || row >= BAND) continue;
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j)
+          *reinterpret_cast<lds<O>*>(smem + row * ROWB + f.col(j) * (int)sizeof(O)) =
+              from_f32<O>(elem(i, j, r, acc[i][j][r]));
+      }
+    __syncthreads();
+    for (int q = threadIdx.x; q < BAND * VPR; q += C::THREADS) {
+      const int lrow = q / VPR, v = q - lrow * VPR;
+      const int row = b * BAND + lrow, col = v * EPV;
+      if (row < tc.m_rows && col < tc.n_cols) {
+        const int64_t dr = rowmap(row);
+        i32x4 raw = *reinterpret_cast<const lds<i32x4>*>(smem + lrow * ROWB + v * 16);
+        raw = vec(dr, row, col, raw);
+        *reinterpret_cast<i32x4*>(out + dr * ldo + tc.n0 + col) = raw;
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace hmoe

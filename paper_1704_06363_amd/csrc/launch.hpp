@@ -37,12 +37,12 @@ int launch_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t 
 // moe.hip
 size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n);
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
-                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, float* lse,
-                       float* loss, float* loss_mean, Workspace& ws, hipStream_t st);
+                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits,
+                       float* lse, float* loss, float* loss_mean, Workspace& ws, hipStream_t st);
 int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                         const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y,
-                        const void* H1s, const void* H, const float* lse, float* dW1, float* db1,
-                        float* dW2, float* db2, float* dD, float* dbD, void* dX, Workspace& ws,
+                        const void* H1s, const void* H, const void* logits, const float* lse, float* dW1,
+                        float* db1, float* dW2, float* db2, float* dD, float* dbD, void* dX, Workspace& ws,
                         hipStream_t st);
 
 }  // namespace hmoe

@@ -34,6 +34,19 @@ struct Pick<bf16> {
 
 // ------------------------------------------------------------------ expert forward
 
+struct RowId {
+  int64_t m0;
+  __device__ __forceinline__ int64_t operator()(int r) const { return m0 + r; }
+};
+struct RowVia {  // destination row = map[m0 + r]
+  const int32_t* __restrict__ map;
+  int64_t m0;
+  __device__ __forceinline__ int64_t operator()(int r) const { return map[m0 + r]; }
+};
+struct Ident {
+  __device__ __forceinline__ float operator()(int, int, int, float v) const { return v; }
+};
+
 // LAYER 1: H1s[m] = relu(Xs[m] W1_e^T + b1_e).   LAYER 2: H[perm[m]] = H1s[m] W2_e^T + b2_e.
 template <class C, int LAYER>
 __global__ void __launch_bounds__(C::THREADS)
@@ -57,34 +70,26 @@ __global__ void __launch_bounds__(C::THREADS)
     const int col = f.col(j);
     bv[j] = (be && col < tc.n_cols) ? to_f32(be[tc.n0 + col]) : 0.f;
   }
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
-      if (row >= tc.m_rows) continue;
-      const int64_t m = tc.m0 + row;
-      const int64_t orow = LAYER == 1 ? m : (int64_t)perm[m];
-      T* dst = out + orow * N + tc.n0;
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        if (col >= tc.n_cols) continue;
-        float v = acc[i][j][r] + bv[j];
-        if (LAYER == 1) v = fmaxf(v, 0.f);
-        dst[col] = from_f32<T>(v);
-      }
-    }
+  auto elem = [&](int, int j, int, float v) {
+    v += bv[j];
+    return LAYER == 1 ? fmaxf(v, 0.f) : v;
+  };
+  if (LAYER == 1)
+    store_tile<C, T>(tc, acc, smem, out, N, elem, RowId{tc.m0}, NoVec{});
+  else
+    store_tile<C, T>(tc, acc, smem, out, N, elem, RowVia{perm, tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ decoder forward
 
-// Per row and V-tile: m = max of the tile's logits, s = sum exp(logit - m).
+// Per row and V-tile: m = max of the tile's logits, s = sum exp(logit - m); the logits
+// themselves are stored to L when L is given (saved for the backward).
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
               const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
-              float* __restrict__ ps) {
+              float* __restrict__ ps, typename C::type* __restrict__ L) {
+  using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
   const TileCoord tc = tile_plain<C>(n, V, o);
@@ -133,6 +138,11 @@ __global__ void __launch_bounds__(C::THREADS)
     pm[at] = M;
     ps[at] = S;
   }
+  if (L) {
+    __syncthreads();
+    store_tile<C, T>(tc, acc, smem, L, V, [&](int, int j, int, float v) { return v + bias[j]; }, RowId{tc.m0},
+                     NoVec{});
+  }
 }
 
 // lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row.
@@ -151,7 +161,7 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
   float S = 0.f;
   for (int t = l; t < nt; t += 64) S += ps[(int64_t)t * n + row] * __expf(pm[(int64_t)t * n + row] - M);
   S = wave_sum(S);
-  const float L = M + __logf(S);
+  const float Lv = M + __logf(S);
   const int32_t p0 = row_ptr[row], p1 = row_ptr[row + 1];
   const T* h = H + row * o;
   float pos = 0.f;
@@ -164,14 +174,15 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
     pos += s + (bD ? to_f32(bD[tg]) : 0.f);
   }
   if (l == 0) {
-    lse[row] = L;
-    loss[row] = L - pos / (float)(p1 - p0);
+    lse[row] = Lv;
+    loss[row] = Lv - pos / (float)(p1 - p0);
   }
 }
 
 // ------------------------------------------------------------------ decoder backward
 
-// g = (exp(logit - lse) - y) / n stored to G; per-tile column sums of g to part_db[mtile][V].
+// Recompute path: g = (exp(logit - lse) - y) / n with the logits recomputed by the GEMM;
+// g stored to G, per-tile column sums of g to part_db[mtile][V].
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_grad(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
@@ -196,8 +207,8 @@ __global__ void __launch_bounds__(C::THREADS)
   constexpr int MAXT = 16;
   lds<float>* s_lse = reinterpret_cast<lds<float>*>(smem);                // [BM]
   lds<int32_t>* s_p0 = reinterpret_cast<lds<int32_t>*>(s_lse + C::BM);    // [BM]
-  lds<int32_t>* s_cnt = s_p0 + C::BM;                                // [BM]
-  lds<int32_t>* s_tag = s_cnt + C::BM;                               // [BM][MAXT]
+  lds<int32_t>* s_cnt = s_p0 + C::BM;                                     // [BM]
+  lds<int32_t>* s_tag = s_cnt + C::BM;                                    // [BM][MAXT]
   lds<float>* cs = reinterpret_cast<lds<float>*>(s_tag + C::BM * MAXT);   // [WAVES_M][BN]
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     const int64_t gr = tc.m0 + t;
@@ -219,10 +230,9 @@ __global__ void __launch_bounds__(C::THREADS)
         for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = 0.f;
         continue;
       }
-      const int64_t gr = tc.m0 + row;
-      const float L = s_lse[row];
+      const float Lr = s_lse[row];
 #pragma unroll
-      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - L);
+      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - Lr);
       const int32_t cnt = s_cnt[row];
       const float y = 1.f / (float)cnt;
       for (int32_t q = 0; q < cnt; ++q) {
@@ -233,13 +243,8 @@ __global__ void __launch_bounds__(C::THREADS)
             if ((lc >> 4) == j) acc[i][j][r] -= y;
         }
       }
-      T* dst = G + gr * V + tc.n0;
 #pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        acc[i][j][r] *= inv_n;
-        if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
-      }
+      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = (f.col(j) < tc.n_cols) ? acc[i][j][r] * inv_n : 0.f;
     }
   // column sums over this tile's rows: lanes of one column group, then the row waves
 #pragma unroll
@@ -260,6 +265,67 @@ __global__ void __launch_bounds__(C::THREADS)
     for (int w = 0; w < C::WAVES_M; ++w) s += cs[w * C::BN + t];
     part_db[(tc.m0 / C::BM) * (int64_t)V + tc.n0 + t] = s;
   }
+  __syncthreads();
+  store_tile<C, T>(tc, acc, smem, G, V, Ident{}, RowId{tc.m0}, NoVec{});
+}
+
+// Saved-logits path: g = (exp(L - lse) - y) / n elementwise over [n x V]; each thread owns one
+// 16-byte column vector over kGradRows rows and writes its column sums to part_db[rowblock][V].
+constexpr int kGradRows = 256;
+
+template <typename T>
+__global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, const float* __restrict__ lse,
+                                                       const int32_t* __restrict__ row_ptr,
+                                                       const int32_t* __restrict__ tag, int64_t n, int V,
+                                                       float inv_n, T* __restrict__ G, float* __restrict__ part_db) {
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int MAXT = 16;
+  __shared__ float s_lse[kGradRows];
+  __shared__ int32_t s_p0[kGradRows], s_cnt[kGradRows], s_tag[kGradRows * MAXT];
+  const int64_t r0 = (int64_t)blockIdx.x * kGradRows;
+  const int rows = (int)((n - r0) < kGradRows ? (n - r0) : kGradRows);
+  for (int t = threadIdx.x; t < rows; t += 256) {
+    const int32_t p0 = row_ptr[r0 + t], cnt = row_ptr[r0 + t + 1] - p0;
+    s_lse[t] = lse[r0 + t];
+    s_p0[t] = p0;
+    s_cnt[t] = cnt;
+    for (int q = 0; q < cnt && q < MAXT; ++q) s_tag[t * MAXT + q] = tag[p0 + q];
+  }
+  __syncthreads();
+  const int c0 = (blockIdx.y * 256 + threadIdx.x) * EPV;
+  if (c0 >= V) return;
+  float cs[EPV];
+#pragma unroll
+  for (int e = 0; e < EPV; ++e) cs[e] = 0.f;
+  for (int t = 0; t < rows; ++t) {
+    const int64_t off = (r0 + t) * V + c0;
+    const i32x4 raw = *reinterpret_cast<const i32x4*>(L + off);
+    const T* lv = reinterpret_cast<const T*>(&raw);
+    const float Lr = s_lse[t];
+    float g[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) g[e] = __expf(to_f32(lv[e]) - Lr);
+    const int32_t cnt = s_cnt[t];
+    const float y = 1.f / (float)cnt;
+    for (int32_t q = 0; q < cnt; ++q) {
+      const int d = (q < MAXT ? s_tag[t * MAXT + q] : tag[s_p0[t] + q]) - c0;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e)
+        if (d == e) g[e] -= y;
+    }
+    i32x4 outv;
+    T* ov = reinterpret_cast<T*>(&outv);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) {
+      g[e] *= inv_n;
+      cs[e] += g[e];
+      ov[e] = from_f32<T>(g[e]);
+    }
+    *reinterpret_cast<i32x4*>(G + off) = outv;
+  }
+  float* dst = part_db + (int64_t)blockIdx.x * V + c0;
+#pragma unroll
+  for (int e = 0; e < EPV; ++e) dst[e] = cs[e];
 }
 
 __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int rows, int V,
@@ -283,20 +349,7 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
-  const Frag<C> f;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
-      if (row >= tc.m_rows) continue;
-      T* dst = dYs + (int64_t)inv[tc.m0 + row] * o + tc.n0;
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        if (col < tc.n_cols) dst[col] = from_f32<T>(acc[i][j][r]);
-      }
-    }
+  store_tile<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
 }
 
 // dD = G^T H (fp32).
@@ -310,20 +363,7 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
-  const Frag<C> f;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
-      if (row >= tc.m_rows) continue;
-      float* dst = dD + (tc.m0 + row) * o + tc.n0;
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        if (col < tc.n_cols) dst[col] = acc[i][j][r];
-      }
-    }
+  store_tile<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ expert backward
@@ -341,22 +381,26 @@ __global__ void __launch_bounds__(C::THREADS)
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
                              smem, acc);
-  const Frag<C> f;
-  float* base = out + (int64_t)tc.group * M * N;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
-      if (row >= tc.m_rows) continue;
-      float* dst = base + (tc.m0 + row) * N + tc.n0;
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        if (col < tc.n_cols) dst[col] = acc[i][j][r];
-      }
-    }
+  store_tile<C, float>(tc, acc, smem, out + (int64_t)tc.group * M * N, N, Ident{}, RowId{tc.m0}, NoVec{});
 }
+
+// Zeroes the bf16 / fp32 lanes of a 16-byte vector where the saved activation is not positive.
+template <typename T>
+struct ReluMask {
+  const T* __restrict__ H1s;
+  int64_t m0;
+  int N, n0;
+  __device__ __forceinline__ i32x4 operator()(int64_t, int row, int col, i32x4 v) const {
+    constexpr int EPV = 16 / sizeof(T);
+    const i32x4 h = *reinterpret_cast<const i32x4*>(H1s + (m0 + row) * N + n0 + col);
+    const T* hv = reinterpret_cast<const T*>(&h);
+    T* vv = reinterpret_cast<T*>(&v);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e)
+      if (!(to_f32(hv[e]) > 0.f)) vv[e] = from_f32<T>(0.f);
+    return v;
+  }
+};
 
 // Row-grouped input gradients.  MASK: dZ[m] = (dYs[m] W2_e) * [H1s[m] > 0], stored in expert
 // order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order.
@@ -375,26 +419,10 @@ __global__ void __launch_bounds__(C::THREADS)
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
                             Kd, smem, acc);
-  const Frag<C> f;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
-      if (row >= tc.m_rows) continue;
-      const int64_t m = tc.m0 + row;
-      const int64_t orow = MASK ? m : (int64_t)perm[m];
-      T* dst = out + orow * N + tc.n0;
-      const T* hm = MASK ? H1s + m * N + tc.n0 : nullptr;
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
-        if (col >= tc.n_cols) continue;
-        float v = acc[i][j][r];
-        if (MASK && !(to_f32(hm[col]) > 0.f)) v = 0.f;
-        dst[col] = from_f32<T>(v);
-      }
-    }
+  if (MASK)
+    store_tile<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, ReluMask<T>{H1s, tc.m0, N, tc.n0});
+  else
+    store_tile<C, T>(tc, acc, smem, out, N, Ident{}, RowVia{perm, tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ launchers
@@ -428,7 +456,8 @@ static size_t bwd_ws(const MoeShape& s) {
   ws.take<T>((size_t)s.n * s.V);
   ws.take<T>((size_t)s.n * s.o);
   ws.take<T>((size_t)s.n * s.h);
-  ws.take<float>((size_t)cdiv(s.n, C::BM) * s.V);
+  const int64_t prow = cdiv(s.n, C::BM) > cdiv(s.n, kGradRows) ? cdiv(s.n, C::BM) : cdiv(s.n, kGradRows);
+  ws.take<float>((size_t)prow * s.V);
   const int w = s.h > s.o ? s.h : s.o;
   return ws.off + segsum_ws(s.n, s.K, w) + 256;
 }
@@ -442,8 +471,8 @@ size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n) {
 
 template <typename T>
 static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
-                     const hmoe_labels_t* y, T* H1s, T* H, float* lse, float* loss, float* loss_mean, Workspace& ws,
-                     hipStream_t st) {
+                     const hmoe_labels_t* y, T* H1s, T* H, T* Lg, float* lse, float* loss, float* loss_mean,
+                     Workspace& ws, hipStream_t st) {
   using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
   const int ntv = (int)cdiv(s.V, C::BN);
@@ -461,7 +490,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   HMOE_LAUNCH("expert layer 2", (k_expert_fwd<C, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
   HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS, st,
-              (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps);
+              (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
   HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
               (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
@@ -469,9 +498,9 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
 
 template <typename T>
 static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
-                      const int32_t* inv, const hmoe_labels_t* y, const T* H1s, const T* H, const float* lse,
-                      float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX, Workspace& ws,
-                      hipStream_t st) {
+                      const int32_t* inv, const hmoe_labels_t* y, const T* H1s, const T* H, const T* Lg,
+                      const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX,
+                      Workspace& ws, hipStream_t st) {
   using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
   int32_t* ts = ws.take<int32_t>(s.K + 1);
@@ -479,18 +508,28 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   T* dYs = ws.take<T>((size_t)n * s.o);
   T* dZ = ws.take<T>((size_t)n * s.h);
   const int mt = (int)cdiv(n, C::BM);
-  float* pdb = ws.take<float>((size_t)mt * s.V);
+  const int gr = (int)cdiv(n, kGradRows);
+  float* pdb = ws.take<float>((size_t)(mt > gr ? mt : gr) * s.V);
   if (!ws.fits()) return HMOE_EWORKSPACE;
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
   const T* D = (const T*)p->D;
   const int ntv = (int)cdiv(s.V, C::BN);
   // decoder
-  HMOE_LAUNCH("decoder grad", k_dec_grad<C>, dim3((unsigned)(mt * ntv)), dim3(C::THREADS), C::LDS, st, H, D,
-              (const T*)p->bD, n, s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
+  int prow;
+  if (Lg) {
+    constexpr int EPV = 16 / sizeof(T);
+    HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)gr, (unsigned)cdiv(s.V, 256 * EPV)), dim3(256),
+                0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), G, pdb);
+    prow = gr;
+  } else {
+    HMOE_LAUNCH("decoder grad", k_dec_grad<C>, dim3((unsigned)(mt * ntv)), dim3(C::THREADS), C::LDS, st, H, D,
+                (const T*)p->bD, n, s.V, s.o, lse, y->row_ptr, y->tag, (float)(1.0 / (double)n), G, pdb);
+    prow = mt;
+  }
   if (dbD)
-    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, mt, s.V,
-                dbD);
+    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, prow,
+                s.V, dbD);
   HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
               (const T*)G, D, n, s.V, s.o, inv, dYs);
   HMOE_LAUNCH("decoder dD", k_dec_dD<C>, dim3((unsigned)(cdiv(s.V, C::BM) * cdiv(s.o, C::BN))), dim3(C::THREADS),
@@ -517,24 +556,24 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
 }
 
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
-                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, float* lse, float* loss,
-                       float* loss_mean, Workspace& ws, hipStream_t st) {
+                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits, float* lse,
+                       float* loss, float* loss_mean, Workspace& ws, hipStream_t st) {
   if (p->dt == HMOE_BF16)
-    return forward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, y, (bf16*)H1s, (bf16*)H, lse, loss, loss_mean, ws,
-                           st);
-  return forward_t<float>(p, n, (const float*)Xs, offsets, perm, y, (float*)H1s, (float*)H, lse, loss, loss_mean, ws,
-                          st);
+    return forward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, y, (bf16*)H1s, (bf16*)H, (bf16*)logits, lse, loss,
+                           loss_mean, ws, st);
+  return forward_t<float>(p, n, (const float*)Xs, offsets, perm, y, (float*)H1s, (float*)H, (float*)logits, lse, loss,
+                          loss_mean, ws, st);
 }
 
 int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                         const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1s,
-                        const void* H, const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD,
-                        float* dbD, void* dX, Workspace& ws, hipStream_t st) {
+                        const void* H, const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
+                        float* db2, float* dD, float* dbD, void* dX, Workspace& ws, hipStream_t st) {
   if (p->dt == HMOE_BF16)
-    return backward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, inv, y, (const bf16*)H1s, (const bf16*)H, lse, dW1,
-                            db1, dW2, db2, dD, dbD, (bf16*)dX, ws, st);
-  return backward_t<float>(p, n, (const float*)Xs, offsets, perm, inv, y, (const float*)H1s, (const float*)H, lse, dW1,
-                           db1, dW2, db2, dD, dbD, (float*)dX, ws, st);
+    return backward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, inv, y, (const bf16*)H1s, (const bf16*)H,
+                            (const bf16*)logits, lse, dW1, db1, dW2, db2, dD, dbD, (bf16*)dX, ws, st);
+  return backward_t<float>(p, n, (const float*)Xs, offsets, perm, inv, y, (const float*)H1s, (const float*)H,
+                           (const float*)logits, lse, dW1, db1, dW2, db2, dD, dbD, (float*)dX, ws, st);
 }
 
 }  // namespace hmoe

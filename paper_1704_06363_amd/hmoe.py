@@ -78,10 +78,10 @@ def lib():
                                         _P, _SZ, _P]
         L.hmoe_permute_rows.argtypes = [_P, _P, _P, _I64, _I32, _c.c_int, _P]
         L.hmoe_moe_forward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P,
-                                       _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _SZ, _P]
+                                       _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                        _P, _P, _SZ, _P]
+                                        _P, _P, _P, _SZ, _P]
         L.hmoe_timer_enable.argtypes = [_c.c_int]
         L.hmoe_timer_enable.restype = _c.c_int
         L.hmoe_timer_report.argtypes = [_c.c_char_p, _SZ]
@@ -280,8 +280,10 @@ def moe_workspace(params: MoeParams, n) -> int:
     return lib().hmoe_moe_workspace(ctypes.byref(params), n)
 
 
-def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None):
-    """Expert MLPs + shared decoder + multilabel softmax loss (Eq. 3)."""
+def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None,
+                save_logits=False):
+    """Expert MLPs + shared decoder + multilabel softmax loss (Eq. 3).  With save_logits the
+    [n, V] logits are returned too (for a backward that does not recompute them)."""
     prm = make_params(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
@@ -292,17 +294,21 @@ def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=Non
     lse = o.get("lse", torch.empty(n, dtype=torch.float32, device=dev))
     loss = o.get("loss", torch.empty(n, dtype=torch.float32, device=dev))
     lm = o.get("loss_mean", torch.empty(1, dtype=torch.float32, device=dev))
+    lg = o.get("logits")
+    if lg is None and save_logits:
+        lg = torch.empty(n, prm.vocab, dtype=dt, device=dev)
     lab = Labels(_ptr(row_ptr), _ptr(tag))
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
     _chk(lib().hmoe_moe_forward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
-                                ctypes.byref(lab), _ptr(H1s), _ptr(H), _ptr(lse), _ptr(loss),
-                                _ptr(lm), _ptr(w), wb, _stream()), "moe_forward")
-    return {"H1_sorted": H1s, "H": H, "lse": lse, "loss": loss, "loss_mean": lm}
+                                ctypes.byref(lab), _ptr(H1s), _ptr(H), _ptr(lg), _ptr(lse),
+                                _ptr(loss), _ptr(lm), _ptr(w), wb, _stream()), "moe_forward")
+    return {"H1_sorted": H1s, "H": H, "lse": lse, "loss": loss, "loss_mean": lm, "logits": lg}
 
 
 def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted, H, lse,
-                 want_dX=True, out=None, ws=None):
-    """Gradients of the mean loss for all expert and decoder parameters (fp32) and dX."""
+                 want_dX=True, out=None, ws=None, logits=None):
+    """Gradients of the mean loss for all expert and decoder parameters (fp32) and dX.  With
+    logits (saved by the forward) the decoder logits are not recomputed."""
     prm = make_params(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
@@ -320,7 +326,8 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
     lab = Labels(_ptr(row_ptr), _ptr(tag))
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
     _chk(lib().hmoe_moe_backward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
-                                 _ptr(inv), ctypes.byref(lab), _ptr(H1_sorted), _ptr(H), _ptr(lse),
+                                 _ptr(inv), ctypes.byref(lab), _ptr(H1_sorted), _ptr(H),
+                                 _ptr(logits), _ptr(lse),
                                  _ptr(g["dW1"]), _ptr(g["db1"]), _ptr(g["dW2"]), _ptr(g["db2"]),
                                  _ptr(g["dD"]), _ptr(g["dbD"]), _ptr(g["dX"]), _ptr(w), wb,
                                  _stream()), "moe_backward")

@@ -72,8 +72,8 @@ def test_argument_errors_are_reported_before_launch(lib):
     # moe forward with vocab not a multiple of 8
     p = hmoe.MoeParams(2, 64, 128, 64, 1001, 0, 16, None, 16, None, 16, None)
     lab = hmoe.Labels(16, 16)
-    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, 16, 16,
-                              16, None, 0, None)
+    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, 16,
+                              16, 16, None, 0, None)
     assert rc == -3 and "vocab" in hmoe.last_error()
     # update with an unknown mode
     rc = lib.hmoe_kmeans_update(16, 0, 10, 16, 3, 16, 16, 16, 16, 16, 9, 0, None, 0, None)

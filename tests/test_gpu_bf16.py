@@ -14,22 +14,26 @@ pytestmark = pytest.mark.gpu
 RT = RTOL["bf16"]
 
 
-def _step(X, ids, K, p, rp, tg, want_dX=True):
+def _step(X, ids, K, p, rp, tg, saved=False):
     a = torch.as_tensor(ids, dtype=torch.int32).cuda()
     d = hmoe.moe_dispatch(a, K, rows=X)
     row_ptr = torch.tensor(rp, device="cuda")
     tag = torch.tensor(tg, device="cuda")
-    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag)
+    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag,
+                         save_logits=saved)
     return d, f, row_ptr, tag
 
 
-def _check_step(X, ids, K, p, rp, tg, rt=RT):
-    """Forward on the HIP path vs the oracle; backward from the oracle's saved activations."""
-    d, f, row_ptr, tag = _step(X, ids, K, p, rp, tg)
+def _check_step(X, ids, K, p, rp, tg, rt=RT, saved=False):
+    """Forward on the HIP path vs the oracle; backward from the oracle's saved activations
+    (with the saved-logits path, from the oracle's bf16 logits)."""
+    d, f, row_ptr, tag = _step(X, ids, K, p, rp, tg, saved)
     Xh = np64(X)
     ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
     ref = O.moe_forward(Xh, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
-                        store="bf16")
+                        store="bf16", want_logits=saved)
+    if saved:
+        assert_close(f["logits"], ref["logits"], rt, "logits")
     perm = npi(d["perm"])
     counts, offsets, perm_ref, inv_ref = O.dispatch(ids, K)
     assert np.array_equal(perm, perm_ref)
@@ -41,31 +45,34 @@ def _check_step(X, ids, K, p, rp, tg, rt=RT):
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(torch.bfloat16).cuda()
     H = torch.tensor(ref["H"], dtype=torch.float32).to(torch.bfloat16).cuda()
     lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
+    Lg = (torch.tensor(ref["logits"], dtype=torch.float32).to(torch.bfloat16).cuda()
+          if saved else None)
     g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag,
-                          H1s, H, lse)
+                          H1s, H, lse, logits=Lg)
     gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
-                        ref["lse"], store="bf16")
+                        ref["lse"], store="bf16", logit_round=saved)
     for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
         assert_close(g[k], gr[k], rt, k)
     return g, counts
 
 
-def test_routed_step_ragged_tiles():
-    # n, h, o, V all leave ragged tails in the 128-wide tiles; biases exercised
+@pytest.mark.parametrize("saved", [False, True])
+def test_routed_step_ragged_tiles(saved):
+    # n, h, o, V all leave ragged tails in the 256-wide tiles; biases exercised
     inp = W.balanced_inputs(device="cuda", seed=3, n=600, d=256, h=384, o=136, V=1000, K=5,
                             bias=True)
     C = inp["C"]
     a, _ = hmoe.kmeans_assign(inp["X"], C)
     a_ref, d1, d2 = O.assign(np64(inp["X"]), np64(C))
     assert_assign(a, a_ref, d1, d2)
-    _check_step(inp["X"], a_ref, 5, inp["params"], inp["row_ptr"], inp["tag"])
+    _check_step(inp["X"], a_ref, 5, inp["params"], inp["row_ptr"], inp["tag"], saved=saved)
 
 
 def test_skewed_routing_with_empty_experts():
     n, K = 900, 24
     inp = W.skewed_inputs(device="cuda", seed=5, n=n, d=128, h=256, o=64, V=520, K=K)
     ids = inp["ids"]
-    g, counts = _check_step(inp["X"], ids, K, inp["params"], inp["row_ptr"], inp["tag"])
+    g, counts = _check_step(inp["X"], ids, K, inp["params"], inp["row_ptr"], inp["tag"], saved=True)
     empty = np.flatnonzero(counts == 0)
     assert len(empty) >= 2
     for k in ("dW1", "db1", "dW2", "db2"):

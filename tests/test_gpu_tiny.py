@@ -68,8 +68,8 @@ def _params(tiny, bias):
     return inp["params"]
 
 
-@pytest.mark.parametrize("bias", [False, True])
-def test_forward_backward_match_oracle(tiny, bias):
+@pytest.mark.parametrize("bias,saved", [(False, False), (True, False), (True, True)])
+def test_forward_backward_match_oracle(tiny, bias, saved):
     c = tiny["cfg"]
     X, Xh = tiny["X"], tiny["Xh"]
     p = _params(tiny, bias)
@@ -79,10 +79,13 @@ def test_forward_backward_match_oracle(tiny, bias):
     d = hmoe.moe_dispatch(a, c.K, rows=X)
     row_ptr = torch.tensor(rp, device="cuda")
     tag = torch.tensor(tg, device="cuda")
-    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag)
+    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag,
+                         save_logits=saved)
     ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
     ref = O.moe_forward(Xh, a_np, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
-                        store="f32")
+                        store="f32", want_logits=saved)
+    if saved:
+        assert_close(f["logits"], ref["logits"], RT, "logits")
     perm = npi(d["perm"])
     assert_close(f["H1_sorted"], ref["H1"][perm], RT, "H1_sorted")
     assert_close(f["H"], ref["H"], RT, "H")
@@ -93,10 +96,11 @@ def test_forward_backward_match_oracle(tiny, bias):
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32, device="cuda")
     H = torch.tensor(ref["H"], dtype=torch.float32, device="cuda")
     lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
+    Lg = torch.tensor(ref["logits"], dtype=torch.float32, device="cuda") if saved else None
     g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag,
-                          H1s, H, lse)
+                          H1s, H, lse, logits=Lg)
     gr = O.moe_backward(Xh, a_np, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"],
-                        ref["H"], ref["lse"], store="f32")
+                        ref["H"], ref["lse"], store="f32", logit_round=saved)
     for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
         assert_close(g[k], gr[k], RT, k)
     # invariants: the softmax rows sum to one, so the decoder-bias gradient sums to zero
