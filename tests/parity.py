@@ -1,8 +1,10 @@
 """Comparison helpers for the HIP-vs-oracle parity tests.
 
 Floats: |gpu - ref| <= rtol * max(|ref|, rms(ref)) elementwise (rtol 1e-4 for fp32 data,
-2e-2 for bf16).  Integer / index outputs: bit-exact, except assignment rows whose oracle
-runner-up distance is within 1e-5 (relative) of the minimum."""
+2e-2 for bf16).  Where a result is a short sum whose terms may cancel, the caller passes the
+sum of the terms' magnitudes (`mass`), the usual scale of a summation error bound, and the
+bound becomes rtol * max(|ref|, rms(ref), mass).  Integer / index outputs: bit-exact, except
+assignment rows whose oracle runner-up distance is within 1e-5 (relative) of the minimum."""
 import numpy as np
 import torch
 
@@ -22,14 +24,18 @@ def npi(t) -> np.ndarray:
     return t.detach().cpu().numpy() if isinstance(t, torch.Tensor) else np.asarray(t)
 
 
-def assert_close(gpu, ref, rtol, what=""):
+def assert_close(gpu, ref, rtol, what="", mass=None):
     g = np64(gpu)
     r = np64(ref)
     assert g.shape == r.shape, (what, g.shape, r.shape)
     if r.size == 0:
         return
     rms = float(np.sqrt(np.mean(r * r)))
-    bound = rtol * np.maximum(np.abs(r), rms)
+    scale = np.maximum(np.abs(r), rms)
+    if mass is not None:
+        assert mass.shape == r.shape, (what, mass.shape, r.shape)
+        scale = np.maximum(scale, mass)
+    bound = rtol * scale
     err = np.abs(g - r)
     bad = ~(err <= bound)
     if bad.any():
