@@ -16,8 +16,10 @@ and the large streamed assignment (2^24 bf16 rows, K = 1024).
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -34,6 +36,51 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ HBM traffic record
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decoder_forward_hbm_traffic.md")
+
+
+def kernel_source_digest():
+    """sha256 over the HIP sources and the C header, so a traffic figure measured on older
+    kernels is recognised as stale."""
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_1704_06363_amd", "csrc")
+    files = sorted(f for f in os.listdir(src) if f.endswith((".hip", ".hpp")))
+    for f in files + ["../../include/hmoe.h"]:
+        with open(os.path.join(src, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(label):
+    """HBM bytes per launch of `label` from the committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, scaled by the same counters on a plain copy), or None when there is no record
+    for this kernel or the kernel sources changed since it was taken."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    with open(TRAFFIC_PROFILE) as fh:
+        m = re.search(r"^traffic-record: (\{.*\})$", fh.read(), re.M)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("kernel") != label or rec.get("source_digest") != kernel_source_digest():
+        return None
+    return rec
+
+
+def calib_copy(mib):
+    """A plain device-to-device copy of `mib` MiB (twice), the known-size reference for the
+    HBM byte counters."""
+    import torch
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 # ------------------------------------------------------------------ routed step
@@ -314,6 +361,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is "
@@ -325,6 +374,9 @@ def main():
     from paper_1704_06363_amd import workloads as W
     torch.cuda.set_device(0)
     hmoe.lib()
+    if args.calib_copy_mib > 0:
+        log(f"calibration copy: {args.calib_copy_mib} MiB")
+        calib_copy(args.calib_copy_mib)
 
     log("balanced step: generating inputs")
     inp = W.balanced_inputs(device="cuda", seed=0)
@@ -339,6 +391,7 @@ def main():
     avg = tot_ms / cnt
     achieved = fl[dom] / (avg * 1e-3) / 1e12
     tot_flops = step_flops(s)
+    tr = recorded_traffic(dom)
     res = {
         "metric": METRIC,
         "value": round(s["n"] / (ms * 1e-3), 1),
@@ -356,7 +409,8 @@ def main():
         "step_frac_bf16_peak": round(tot_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": tr["bytes_per_launch"] if tr else None,
                      "avg_ms": round(avg, 4), "flop_per_launch": fl[dom]},
         "kernels": kern,
     }
