@@ -33,6 +33,7 @@ constexpr int kStageRowBytes = 128;  // K extent of one stage, in bytes
 template <typename T, int BM_, int BN_, int WM_, int WN_>
 struct Cfg {
   using type = T;
+  static constexpr bool DMA = false;  // register-staged engine
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int WAVES_N = BN / WN, WAVES_M = BM / WM;
   static constexpr int WAVES = WAVES_M * WAVES_N;
@@ -219,12 +220,13 @@ __device__ __forceinline__ void mfma_stage(const lds<char>* ldsA, const lds<char
 // Full K loop for one tile.  A rows [0, a_rows), B rows [0, b_rows), K positions [0, k_len).
 // With ROWNORM (K-contiguous A only) xs[] collects squared row norms of A (see add_sq).
 template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
-__device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
+__device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
                                           const typename C::type* __restrict__ B, int64_t ldb, int b_rows,
                                           int k_len, lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
                                           float* xs = nullptr) {
   using T = typename C::type;
   using SA = Stager<T, C::BM, C::THREADS, A_KC>;
+  static_assert(!C::DMA, "register-staged engine");
   using SB = Stager<T, C::BN, C::THREADS, B_KC>;
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
@@ -263,6 +265,233 @@ __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A
       sb.store(bufB0 + (cur ^ 1) * C::B_BYTES);
     }
     __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------ direct-to-LDS engine (bf16)
+//
+// The same BM x BN tile and wave split, but operands travel from HBM to LDS without passing
+// through registers: global_load_lds_dwordx4 writes lane l's 16 bytes to LDS at (wave-uniform
+// base) + 16 l, so the LDS layout -- including its bank swizzle -- is chosen by the global
+// address each lane loads.  A stage covers 32 K (64 bytes per row); NS stages form a ring and
+// the loads for stage kt + NS - 1 are issued while stage kt feeds the MFMAs, each wave waiting
+// (vmcnt) only for its own loads of the stage it is about to read.
+//   K-contiguous operand: LDS [rows][32 K] (64-byte rows, chunk c of row r at c ^ ((r >> 2) & 3));
+//                         MFMA operands come from one ds_read_b128 per 16 x 32 fragment.
+//   K-strided operand:    LDS [32 K][rows] as in HBM (rows contiguous, 16-byte chunk c of K-row
+//                         k at c ^ 2 ((k & 3) | ((k >> 1) & 4))); MFMA operands come from two
+//                         ds_read_b64_tr_b16 per fragment.  Within each 16-lane group that read
+//                         returns to lane i, slot s, element i % 4 of the 8 bytes addressed by lane
+//                         4 s + i / 4 (verified on gfx950), so lane j addressing K-row
+//                         8 (l / 16) + 4 h + j / 4, rows 4 (j % 4) .. + 3 gives every lane the 4
+//                         consecutive K of its own row that the MFMA layout expects.
+// Both swizzles make the MFMA operand reads conflict-free (16 rows, or 8 K-rows x 32 bytes, per
+// bank sweep).  Rows past the valid range load a clamped (valid) address -- they only feed
+// output rows / columns that are never stored -- and a last partial K stage is staged through
+// registers with zero fill.  Needs every row width (ld) and valid row count in the row
+// direction of a K-strided operand to be a multiple of 8 elements.
+
+template <typename T, int BM_, int BN_, int WM_, int WN_, int NS_>
+struct CfgD {
+  using type = T;
+  static constexpr bool DMA = true;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int WAVES_N = BN / WN, WAVES_M = BM / WM;
+  static constexpr int WAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int MI = WM / 16, NJ = WN / 16;
+  static constexpr int BK = 32, NS = NS_;
+  static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int LDS = NS * STAGE;
+  static_assert(sizeof(T) == 2, "direct-to-LDS engine is bf16 only");
+};
+
+#ifndef HMOE_DMA_STAGES
+#define HMOE_DMA_STAGES 4
+#endif
+typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
+
+__device__ __forceinline__ int kc_off(int row, int chunk) {
+  return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
+}
+template <int R>
+__device__ __forceinline__ int ks_off(int k, int byte) {
+  const int sw = ((k & 3) | ((k >> 1) & 4)) << 1;
+  return k * (R * 2) + ((((byte >> 4) ^ sw)) << 4) + (byte & 15);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+__device__ __forceinline__ void wg_barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// One operand of R rows: per-thread slot offsets and the per-stage DMA / tail staging.
+template <int R, int THREADS, bool KC>
+struct DmaOperand {
+  static constexpr int SLOTS = KC ? R * 4 : 32 * (R / 8);  // 16-byte slots per stage
+  static constexpr int NQ = SLOTS / THREADS;
+  static_assert(SLOTS % THREADS == 0, "slots/threads");
+  int64_t off[NQ];   // element offset of the slot's source for k0 = 0
+  bool live[NQ];     // KC: chunk K-position tracking is per stage; KS: column valid
+  int kk[NQ];        // KC: K offset of the chunk (0..31); KS: K-row within the stage
+
+  // KC: element (r, k) at base + r * ld + k.  KS: element (r, k) at base + k * ld + r.
+  __device__ __forceinline__ void init(int64_t ld, int rows_valid) {
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int slot = (q * (THREADS / 64) + w) * 64 + l;
+      if constexpr (KC) {
+        const int r = slot >> 2, p = slot & 3;
+        const int c = p ^ ((r >> 2) & 3);
+        const int gr = r < rows_valid ? r : rows_valid - 1;
+        off[q] = (int64_t)gr * ld + c * 8;
+        kk[q] = c * 8;
+        live[q] = r < rows_valid;
+      } else {
+        constexpr int CPR = R / 8;  // chunks per K-row
+        const int k = slot / CPR, p = slot % CPR;
+        const int sw = ((k & 3) | ((k >> 1) & 4)) << 1;
+        const int col = (p ^ sw) * 8;
+        live[q] = col < rows_valid;
+        off[q] = (int64_t)k * ld + (live[q] ? col : 0);
+        kk[q] = k;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void issue(const bf16* __restrict__ base, int64_t ld, int k0, lds<char>* buf) const {
+    const int w = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int64_t o = off[q] + (KC ? (int64_t)k0 : (int64_t)k0 * ld);
+      lds<char>* dst = buf + (q * (THREADS / 64) + w) * 1024;
+      __builtin_amdgcn_global_load_lds((const void*)(base + o), (lds<void>*)dst, 16, 0, 0);
+    }
+  }
+
+  // Last partial stage [k0, k_len): through registers, zero outside the valid range.
+  __device__ __forceinline__ void tail(const bf16* __restrict__ base, int64_t ld, int k0, int k_len,
+                                       lds<char>* buf) const {
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int slot = (q * (THREADS / 64) + w) * 64 + l;
+      i32x4 v = i32x4{0, 0, 0, 0};
+      const bool ok = KC ? (k0 + kk[q] < k_len) : (live[q] && k0 + kk[q] < k_len);
+      if (ok) v = *reinterpret_cast<const i32x4*>(base + off[q] + (KC ? (int64_t)k0 : (int64_t)k0 * ld));
+      *reinterpret_cast<lds<i32x4>*>(buf + slot * 16) = v;
+    }
+  }
+};
+
+template <bool KC, int R>
+__device__ __forceinline__ bf16x8 dma_frag(const lds<char>* buf, int r0, int lr, int lg) {
+  if constexpr (KC) {
+    return *reinterpret_cast<const lds<bf16x8>*>(buf + kc_off(r0 + lr, lg));
+  } else {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    const int byte = (r0 + 4 * (lr & 3)) * 2;
+    const int k = 8 * lg + (lr >> 2);
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds<s4>*)(buf + ks_off<R>(k, byte)));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds<s4>*)(buf + ks_off<R>(k + 4, byte)));
+    typedef short s8 __attribute__((ext_vector_type(8)));
+    const s8 v = s8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  }
+}
+
+template <class C, bool A_KC, bool B_KC>
+__device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<char>* bB,
+                                               floatx4 (&acc)[C::MI][C::NJ]) {
+  const int l = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wm = w / C::WAVES_N, wn = w % C::WAVES_N;
+  const int lr = l & 15, lg = l >> 4;
+  bf16x8 a[C::MI], b[C::NJ];
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i) a[i] = dma_frag<A_KC, C::BM>(bA, wm * C::WM + 16 * i, lr, lg);
+#pragma unroll
+  for (int j = 0; j < C::NJ; ++j) b[j] = dma_frag<B_KC, C::BN>(bB, wn * C::WN + 16 * j, lr, lg);
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+}
+
+template <class C, int LOADS>
+__device__ __forceinline__ void wait_stage(int pending_stages) {
+  static_assert(C::NS <= 5 && LOADS * (C::NS - 2) <= 63, "vmcnt range");
+  switch (pending_stages) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<LOADS>(); break;
+    case 2: wait_vmcnt<2 * LOADS>(); break;
+    default: wait_vmcnt<3 * LOADS>(); break;
+  }
+}
+
+template <class C, bool A_KC, bool B_KC>
+__device__ __forceinline__ void gemm_tile_dma(const bf16* __restrict__ A, int64_t lda, int a_rows,
+                                              const bf16* __restrict__ B, int64_t ldb, int b_rows, int k_len,
+                                              lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ]) {
+  using OA = DmaOperand<C::BM, C::THREADS, A_KC>;
+  using OB = DmaOperand<C::BN, C::THREADS, B_KC>;
+  constexpr int LOADS = OA::NQ + OB::NQ;
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  OA oa;
+  OB ob;
+  oa.init(lda, a_rows);
+  ob.init(ldb, b_rows);
+  const int nfull = k_len / C::BK;
+  auto bufA = [&](int s) { return smem + s * C::STAGE; };
+  auto bufB = [&](int s) { return smem + s * C::STAGE + C::A_BYTES; };
+#pragma unroll
+  for (int s = 0; s < C::NS - 1; ++s)
+    if (s < nfull) {
+      oa.issue(A, lda, s * C::BK, bufA(s));
+      ob.issue(B, ldb, s * C::BK, bufB(s));
+    }
+  for (int kt = 0; kt < nfull; ++kt) {
+    const int ahead = nfull - 1 - kt;
+    wait_stage<C, LOADS>(ahead < C::NS - 2 ? ahead : C::NS - 2);
+    wg_barrier();
+    const int nx = kt + C::NS - 1;
+    if (nx < nfull) {
+      const int sb = nx % C::NS;
+      oa.issue(A, lda, nx * C::BK, bufA(sb));
+      ob.issue(B, ldb, nx * C::BK, bufB(sb));
+    }
+    const int sc = kt % C::NS;
+    dma_mfma_stage<C, A_KC, B_KC>(bufA(sc), bufB(sc), acc);
+  }
+  if (nfull * C::BK < k_len) {
+    const int sb = nfull % C::NS;
+    oa.tail(A, lda, nfull * C::BK, k_len, bufA(sb));
+    ob.tail(B, ldb, nfull * C::BK, k_len, bufB(sb));
+    wg_barrier_lds();
+    dma_mfma_stage<C, A_KC, B_KC>(bufA(sb), bufB(sb), acc);
+  }
+  wg_barrier_lds();
+}
+
+// Full K loop for one tile on whichever engine the configuration names.
+template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
+__device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
+                                          const typename C::type* __restrict__ B, int64_t ldb, int b_rows,
+                                          int k_len, lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
+                                          float* xs = nullptr) {
+  if constexpr (C::DMA) {
+    static_assert(!ROWNORM, "row norms need the register-staged engine");
+    gemm_tile_dma<C, A_KC, B_KC>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc);
+  } else {
+    gemm_tile_reg<C, A_KC, B_KC, ROWNORM>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc, xs);
   }
 }
 

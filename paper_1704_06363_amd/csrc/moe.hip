@@ -22,14 +22,15 @@
 
 namespace hmoe {
 
-// Tile configuration per data type: bf16 runs the 256 x 256 engine, fp32 the 128 x 128 one.
+// Tile configuration per data type: bf16 runs the 256 x 256 direct-to-LDS engine, fp32 the
+// register-staged 128 x 128 one.
 template <typename T>
 struct Pick {
   using C = CfgSmall<float>;
 };
 template <>
 struct Pick<bf16> {
-  using C = CfgBig;
+  using C = CfgDma;
 };
 
 // ------------------------------------------------------------------ expert forward
