@@ -276,7 +276,7 @@ __device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict
 // address each lane loads.  A stage covers 32 K (64 bytes per row); NS stages form a ring and
 // the loads for stage kt + NS - 1 are issued while stage kt feeds the MFMAs, each wave waiting
 // (vmcnt) only for its own loads of the stage it is about to read.
-//   K-contiguous operand: LDS [rows][32 K] (64-byte rows, chunk c of row r at c ^ ((r >> 2) & 3));
+//   K-contiguous operand: LDS [rows][32 K] (64-byte rows, chunk c of row r at c ^ ((r >> 1) & 3));
 //                         MFMA operands come from one ds_read_b128 per 16 x 32 fragment.
 //   K-strided operand:    LDS [32 K][rows] as in HBM (rows contiguous, 16-byte chunk c of K-row
 //                         k at c ^ 2 ((k & 3) | ((k >> 1) & 4))); MFMA operands come from two
@@ -285,8 +285,8 @@ __device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict
 //                         4 s + i / 4 (verified on gfx950), so lane j addressing K-row
 //                         8 (l / 16) + 4 h + j / 4, rows 4 (j % 4) .. + 3 gives every lane the 4
 //                         consecutive K of its own row that the MFMA layout expects.
-// Both swizzles make the MFMA operand reads conflict-free (16 rows, or 8 K-rows x 32 bytes, per
-// bank sweep).  Rows past the valid range load a clamped (valid) address -- they only feed
+// Both swizzles make the MFMA operand reads conflict-free (checked with the LDS bank-conflict
+// counter).  Rows past the valid range load a clamped (valid) address -- they only feed
 // output rows / columns that are never stored -- and a last partial K stage is staged through
 // registers with zero fill.  Needs every row width (ld) and valid row count in the row
 // direction of a K-strided operand to be a multiple of 8 elements.
@@ -312,9 +312,12 @@ struct CfgD {
 #endif
 typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
 
-__device__ __forceinline__ int kc_off(int row, int chunk) {
-  return row * 64 + ((chunk ^ ((row >> 2) & 3)) << 4);
-}
+// 16-byte chunk swizzle of the 64-byte K-contiguous rows (used by the DMA slot mapping and the
+// operand reads alike).  Measured with the LDS bank-conflict counter on gfx950 for the MFMA
+// operand read (16 rows x 4 chunks per ds_read_b128): (r >> 1) & 3 is conflict-free, while no
+// swizzle, r & 3, (r >> 2) & 3, (r ^ (r >> 2)) & 3 and (r >> 3) & 3 are all 2-way conflicted.
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 3; }
+__device__ __forceinline__ int kc_off(int row, int chunk) { return row * 64 + ((chunk ^ kc_swz(row)) << 4); }
 template <int R>
 __device__ __forceinline__ int ks_off(int k, int byte) {
   const int sw = ((k & 3) | ((k >> 1) & 4)) << 1;
@@ -346,7 +349,7 @@ struct DmaOperand {
       const int slot = (q * (THREADS / 64) + w) * 64 + l;
       if constexpr (KC) {
         const int r = slot >> 2, p = slot & 3;
-        const int c = p ^ ((r >> 2) & 3);
+        const int c = p ^ kc_swz(r);
         const int gr = r < rows_valid ? r : rows_valid - 1;
         off[q] = (int64_t)gr * ld + c * 8;
         kk[q] = c * 8;
