@@ -34,6 +34,7 @@ template <typename T, int BM_, int BN_, int WM_, int WN_>
 struct Cfg {
   using type = T;
   static constexpr bool DMA = false;  // register-staged engine
+  static constexpr bool TRANS = false;  // accumulator element (i, j, r) at row 16 i + 4 (l / 16) + r, col 16 j + l % 16
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int WAVES_N = BN / WN, WAVES_M = BM / WM;
   static constexpr int WAVES = WAVES_M * WAVES_N;
@@ -295,6 +296,7 @@ template <typename T, int BM_, int BN_, int WM_, int WN_, int NS_>
 struct CfgD {
   using type = T;
   static constexpr bool DMA = true;
+  static constexpr bool TRANS = true;  // accumulator element (i, j, r) at row 16 i + l % 16, col 16 j + 4 (l / 16) + r
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int WAVES_N = BN / WN, WAVES_M = BM / WM;
   static constexpr int WAVES = WAVES_M * WAVES_N;
@@ -419,11 +421,13 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
   for (int i = 0; i < C::MI; ++i) a[i] = dma_frag<A_KC, C::BM>(bA, wm * C::WM + 16 * i, lr, lg);
 #pragma unroll
   for (int j = 0; j < C::NJ; ++j) b[j] = dma_frag<B_KC, C::BN>(bB, wn * C::WN + 16 * j, lr, lg);
+  // B as the MFMA's first operand: the 16 x 16 result is the transposed sub-tile, so each lane
+  // ends up with four consecutive output columns of one row (see TRANS).
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
 }
 
 template <class C, int LOADS>
@@ -603,8 +607,13 @@ __device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ se
 
 // ------------------------------------------------------------------ epilogue helpers
 
+// Where accumulator element (i, j, r) of this lane sits in the tile, for either orientation.
+// A lane holds MI rows x NCOL columns (TRANS: one row per i and four consecutive columns per j;
+// otherwise four rows per i and one column per j); qidx(j, r) numbers the lane's columns.
 template <class C>
 struct Frag {
+  static constexpr bool T = C::TRANS;
+  static constexpr int NCOL = T ? C::NJ * 4 : C::NJ;
   int wm, wn, lr, lg;
   __device__ __forceinline__ Frag() {
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -613,9 +622,15 @@ struct Frag {
     lr = l & 15;
     lg = l >> 4;
   }
-  __device__ __forceinline__ int row(int i, int r) const { return wm * C::WM + 16 * i + 4 * lg + r; }
-  __device__ __forceinline__ int col(int j) const { return wn * C::WN + 16 * j + lr; }
+  __device__ __forceinline__ int row(int i, int r) const { return wm * C::WM + 16 * i + (T ? lr : 4 * lg + r); }
+  __device__ __forceinline__ int col(int j, int r) const { return wn * C::WN + 16 * j + (T ? 4 * lg + r : lr); }
+  __device__ __forceinline__ static constexpr int qidx(int j, int r) { return T ? 4 * j + r : j; }
+  __device__ __forceinline__ int colq(int q) const { return T ? col(q >> 2, q & 3) : col(q, 0); }
 };
+
+// Four consecutive output values of one type, as stored by store_direct.
+template <typename O>
+using vec4 = O __attribute__((ext_vector_type(4)));
 
 // Epilogue store through LDS: the tile is written to LDS row-major (padded rows, conflict-free
 // for the accumulator layout) in bands of rows, then copied out so that every lane stores whole
@@ -625,7 +640,8 @@ struct Frag {
 //   vec(dst_row, local_row, col, raw)  last transform of a 16-byte vector (e.g. a mask)
 // n_cols must be a multiple of 16 / sizeof(O).
 struct NoVec {
-  __device__ __forceinline__ i32x4 operator()(int64_t, int, int, i32x4 v) const { return v; }
+  template <typename V>
+  __device__ __forceinline__ V operator()(int64_t, int, int, V v) const { return v; }
 };
 
 template <class C, typename O, class Elem, class RowMap, class Vec>
@@ -649,7 +665,7 @@ __device__ __forceinline__ void store_tile(const TileCoord& tc, const floatx4 (&
         if (row < 0 || row >= BAND) continue;
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j)
-          *reinterpret_cast<lds<O>*>(smem + row * ROWB + f.col(j) * (int)sizeof(O)) =
+          *reinterpret_cast<lds<O>*>(smem + row * ROWB + f.col(j, r) * (int)sizeof(O)) =
               from_f32<O>(elem(i, j, r, acc[i][j][r]));
       }
     __syncthreads();
@@ -665,6 +681,43 @@ __device__ __forceinline__ void store_tile(const TileCoord& tc, const floatx4 (&
     }
     __syncthreads();
   }
+}
+
+// Epilogue store straight from registers (TRANS orientation): every lane writes its four
+// consecutive columns of a row as one 8-byte (bf16) or 16-byte (fp32) store; no LDS, no
+// barrier, and the stores drain while the next tile starts.  Same functors as store_tile, with
+// vec applied to the 4-element vector.
+template <class C, typename O, class Elem, class RowMap, class Vec>
+__device__ __forceinline__ void store_direct(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                             O* __restrict__ out, int64_t ldo, Elem elem, RowMap rowmap, Vec vec) {
+  static_assert(C::TRANS, "direct stores need the transposed accumulator layout");
+  const Frag<C> f;
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i) {
+    const int row = f.row(i, 0);
+    if (row >= tc.m_rows) continue;
+    const int64_t dr = rowmap(row);
+    O* orow = out + dr * ldo + tc.n0;
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j) {
+      const int col = f.col(j, 0);
+      if (col >= tc.n_cols) continue;
+      vec4<O> v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = from_f32<O>(elem(i, j, r, acc[i][j][r]));
+      *reinterpret_cast<vec4<O>*>(orow + col) = vec(dr, row, col, v);
+    }
+  }
+}
+
+// The epilogue store for the configuration's orientation.
+template <class C, typename O, class Elem, class RowMap, class Vec>
+__device__ __forceinline__ void store_out(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ], lds<char>* smem,
+                                          O* __restrict__ out, int64_t ldo, Elem elem, RowMap rowmap, Vec vec) {
+  if constexpr (C::TRANS)
+    store_direct<C, O>(tc, acc, out, ldo, elem, rowmap, vec);
+  else
+    store_tile<C, O>(tc, acc, smem, out, ldo, elem, rowmap, vec);
 }
 
 }  // namespace hmoe

@@ -66,7 +66,7 @@ __global__ void __launch_bounds__(C::THREADS)
       int bi = INT_MAX;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j) {
-        const int col = f.col(j);
+        const int col = f.col(j, 0);
         if (col < tc.n_cols) argmin_merge(best, bi, cn[tc.n0 + col] - 2.f * acc[i][j][r], tc.n0 + col);
       }
 #pragma unroll

@@ -63,22 +63,23 @@ __global__ void __launch_bounds__(C::THREADS)
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, true>(A + tc.m0 * Kd, Kd, tc.m_rows, W + ((int64_t)tc.group * N + tc.n0) * Kd, Kd,
                            tc.n_cols, Kd, smem, acc);
-  const Frag<C> f;
+  using F = Frag<C>;
+  const F f;
   const T* be = bias ? bias + (int64_t)tc.group * N : nullptr;
-  float bv[C::NJ];
+  float bv[F::NCOL];
 #pragma unroll
-  for (int j = 0; j < C::NJ; ++j) {
-    const int col = f.col(j);
-    bv[j] = (be && col < tc.n_cols) ? to_f32(be[tc.n0 + col]) : 0.f;
+  for (int q = 0; q < F::NCOL; ++q) {
+    const int col = f.colq(q);
+    bv[q] = (be && col < tc.n_cols) ? to_f32(be[tc.n0 + col]) : 0.f;
   }
-  auto elem = [&](int, int j, int, float v) {
-    v += bv[j];
+  auto elem = [&](int, int j, int r, float v) {
+    v += bv[F::qidx(j, r)];
     return LAYER == 1 ? fmaxf(v, 0.f) : v;
   };
   if (LAYER == 1)
-    store_tile<C, T>(tc, acc, smem, out, N, elem, RowId{tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, out, N, elem, RowId{tc.m0}, NoVec{});
   else
-    store_tile<C, T>(tc, acc, smem, out, N, elem, RowVia{perm, tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, out, N, elem, RowVia{perm, tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ decoder forward
@@ -97,36 +98,65 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
-  const Frag<C> f;
-  float bias[C::NJ];
+  using F = Frag<C>;
+  const F f;
+  float bias[F::NCOL];
 #pragma unroll
-  for (int j = 0; j < C::NJ; ++j) {
-    const int col = f.col(j);
-    bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
+  for (int q = 0; q < F::NCOL; ++q) {
+    const int col = f.colq(q);
+    bias[q] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
   }
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // [WAVES_N][BM]
-  lds<float>* rs = rm + C::WAVES_N * C::BM;         // [WAVES_N][BM]
+  lds<float>* rs = rm + C::WAVES_N * C::BM;              // [WAVES_N][BM]
+  if constexpr (F::T) {
+    // one row per i; its WN columns of this wave sit in lanes lr, lr + 16, lr + 32, lr + 48
 #pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int i = 0; i < C::MI; ++i) {
       float mx = -FLT_MAX;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j)
-        if (f.col(j) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[j]);
 #pragma unroll
-      for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
+        for (int r = 0; r < 4; ++r)
+          if (f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[F::qidx(j, r)]);
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
       float s = 0.f;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j)
-        if (f.col(j) < tc.n_cols) s += __expf(acc[i][j][r] + bias[j] - mx);
 #pragma unroll
-      for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
-      if (f.lr == 0) {
-        rm[f.wn * C::BM + f.row(i, r)] = mx;
-        rs[f.wn * C::BM + f.row(i, r)] = s;
+        for (int r = 0; r < 4; ++r)
+          if (f.col(j, r) < tc.n_cols) s += __expf(acc[i][j][r] + bias[F::qidx(j, r)] - mx);
+      s += shfl_xor(s, 16);
+      s += shfl_xor(s, 32);
+      if (f.lg == 0) {
+        rm[f.wn * C::BM + f.row(i, 0)] = mx;
+        rs[f.wn * C::BM + f.row(i, 0)] = s;
       }
     }
+  } else {
+    // four rows per i; a row's WN columns of this wave sit in the 16 lanes of one lane group
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float mx = -FLT_MAX;
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j)
+          if (f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[j]);
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j)
+          if (f.col(j, r) < tc.n_cols) s += __expf(acc[i][j][r] + bias[j] - mx);
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
+        if (f.lr == 0) {
+          rm[f.wn * C::BM + f.row(i, r)] = mx;
+          rs[f.wn * C::BM + f.row(i, r)] = s;
+        }
+      }
+  }
   __syncthreads();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     float M = rm[t];
@@ -140,9 +170,9 @@ __global__ void __launch_bounds__(C::THREADS)
     ps[at] = S;
   }
   if (L) {
-    __syncthreads();
-    store_tile<C, T>(tc, acc, smem, L, V, [&](int, int j, int, float v) { return v + bias[j]; }, RowId{tc.m0},
-                     NoVec{});
+    if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
+    store_out<C, T>(tc, acc, smem, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
+                    RowId{tc.m0}, NoVec{});
   }
 }
 
@@ -197,12 +227,13 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
-  const Frag<C> f;
-  float bias[C::NJ];
+  using F = Frag<C>;
+  const F f;
+  float bias[F::NCOL];
 #pragma unroll
-  for (int j = 0; j < C::NJ; ++j) {
-    const int col = f.col(j);
-    bias[j] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
+  for (int q = 0; q < F::NCOL; ++q) {
+    const int col = f.colq(q);
+    bias[q] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
   }
   // Per-row data of the tile, staged once in LDS (the operand buffers are free now).
   constexpr int MAXT = 16;
@@ -221,43 +252,80 @@ __global__ void __launch_bounds__(C::THREADS)
   }
   __syncthreads();
   const int wcol0 = tc.n0 + f.wn * C::WN;  // first column of this wave
+  // g for accumulator element (i, j, r) of row `row`; rows past the tile give 0
+  auto grad_row = [&](int i, int row, auto owns, auto pick) {
+    const float Lr = s_lse[row];
 #pragma unroll
-  for (int i = 0; i < C::MI; ++i)
+    for (int j = 0; j < C::NJ; ++j)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = f.row(i, r);
+      for (int r = 0; r < 4; ++r)
+        if (pick(r)) acc[i][j][r] = __expf(acc[i][j][r] + bias[F::qidx(j, r)] - Lr);
+    const int32_t cnt = s_cnt[row];
+    const float y = 1.f / (float)cnt;
+    for (int32_t q = 0; q < cnt; ++q) {
+      const int lc = (q < MAXT ? s_tag[row * MAXT + q] : tag[s_p0[row] + q]) - wcol0;
+      if (lc >= 0 && lc < C::WN && owns(lc)) {
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (pick(r) && f.col(j, r) - f.wn * C::WN == lc) acc[i][j][r] -= y;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (pick(r)) acc[i][j][r] = (f.col(j, r) < tc.n_cols) ? acc[i][j][r] * inv_n : 0.f;
+  };
+  if constexpr (F::T) {
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i) {
+      const int row = f.row(i, 0);
       if (row >= tc.m_rows) {
 #pragma unroll
-        for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = 0.f;
+        for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
         continue;
       }
-      const float Lr = s_lse[row];
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = __expf(acc[i][j][r] + bias[j] - Lr);
-      const int32_t cnt = s_cnt[row];
-      const float y = 1.f / (float)cnt;
-      for (int32_t q = 0; q < cnt; ++q) {
-        const int lc = (q < MAXT ? s_tag[row * MAXT + q] : tag[s_p0[row] + q]) - wcol0;
-        if (lc >= 0 && lc < C::WN && (lc & 15) == f.lr) {
-#pragma unroll
-          for (int j = 0; j < C::NJ; ++j)
-            if ((lc >> 4) == j) acc[i][j][r] -= y;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = (f.col(j) < tc.n_cols) ? acc[i][j][r] * inv_n : 0.f;
+      grad_row(i, row, [&](int lc) { return ((lc & 15) >> 2) == f.lg; }, [](int) { return true; });
     }
-  // column sums over this tile's rows: lanes of one column group, then the row waves
+    // column sums over this tile's rows: the 16 lanes of a column's lane group, then the row waves
 #pragma unroll
-  for (int j = 0; j < C::NJ; ++j) {
-    float s = 0.f;
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < C::MI; ++i) s += acc[i][j][r];
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
+        if (f.lr == 0) cs[f.wm * C::BN + f.col(j, r)] = s;
+      }
+  } else {
 #pragma unroll
     for (int i = 0; i < C::MI; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) s += acc[i][j][r];
-    s += shfl_xor(s, 16);
-    s += shfl_xor(s, 32);
-    if (f.lg == 0) cs[f.wm * C::BN + f.col(j)] = s;
+      for (int r = 0; r < 4; ++r) {
+        const int row = f.row(i, r);
+        if (row >= tc.m_rows) {
+#pragma unroll
+          for (int j = 0; j < C::NJ; ++j) acc[i][j][r] = 0.f;
+          continue;
+        }
+        grad_row(i, row, [&](int lc) { return (lc & 15) == f.lr; }, [r](int rr) { return rr == r; });
+      }
+    // column sums over this tile's rows: the lane groups, then the row waves
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s += acc[i][j][r];
+      s += shfl_xor(s, 16);
+      s += shfl_xor(s, 32);
+      if (f.lg == 0) cs[f.wm * C::BN + f.col(j, 0)] = s;
+    }
   }
   __syncthreads();
   for (int t = threadIdx.x; t < tc.n_cols; t += C::THREADS) {
@@ -266,8 +334,8 @@ __global__ void __launch_bounds__(C::THREADS)
     for (int w = 0; w < C::WAVES_M; ++w) s += cs[w * C::BN + t];
     part_db[(tc.m0 / C::BM) * (int64_t)V + tc.n0 + t] = s;
   }
-  __syncthreads();
-  store_tile<C, T>(tc, acc, smem, G, V, Ident{}, RowId{tc.m0}, NoVec{});
+  if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses the row data
+  store_out<C, T>(tc, acc, smem, G, V, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
 // Saved-logits path: g = (exp(L - lse) - y) / n elementwise over [n x V]; each thread owns one
@@ -350,7 +418,7 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
-  store_tile<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
+  store_out<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
 }
 
 // dD = G^T H (fp32).
@@ -364,7 +432,7 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
-  store_tile<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
+  store_out<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ expert backward
@@ -382,22 +450,24 @@ __global__ void __launch_bounds__(C::THREADS)
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
                              smem, acc);
-  store_tile<C, float>(tc, acc, smem, out + (int64_t)tc.group * M * N, N, Ident{}, RowId{tc.m0}, NoVec{});
+  store_out<C, float>(tc, acc, smem, out + (int64_t)tc.group * M * N, N, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
-// Zeroes the bf16 / fp32 lanes of a 16-byte vector where the saved activation is not positive.
+// Zeroes the elements of a stored vector (16 bytes from store_tile, four elements from
+// store_direct) where the saved activation is not positive.
 template <typename T>
 struct ReluMask {
   const T* __restrict__ H1s;
   int64_t m0;
   int N, n0;
-  __device__ __forceinline__ i32x4 operator()(int64_t, int row, int col, i32x4 v) const {
-    constexpr int EPV = 16 / sizeof(T);
-    const i32x4 h = *reinterpret_cast<const i32x4*>(H1s + (m0 + row) * N + n0 + col);
+  template <typename V>
+  __device__ __forceinline__ V operator()(int64_t, int row, int col, V v) const {
+    constexpr int E = sizeof(V) / sizeof(T);
+    const V h = *reinterpret_cast<const V*>(H1s + (m0 + row) * N + n0 + col);
     const T* hv = reinterpret_cast<const T*>(&h);
     T* vv = reinterpret_cast<T*>(&v);
 #pragma unroll
-    for (int e = 0; e < EPV; ++e)
+    for (int e = 0; e < E; ++e)
       if (!(to_f32(hv[e]) > 0.f)) vv[e] = from_f32<T>(0.f);
     return v;
   }
@@ -421,9 +491,9 @@ __global__ void __launch_bounds__(C::THREADS)
   gemm_tile<C, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
                             Kd, smem, acc);
   if (MASK)
-    store_tile<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, ReluMask<T>{H1s, tc.m0, N, tc.n0});
+    store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, ReluMask<T>{H1s, tc.m0, N, tc.n0});
   else
-    store_tile<C, T>(tc, acc, smem, out, N, Ident{}, RowVia{perm, tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowVia{perm, tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ launchers
