@@ -312,6 +312,12 @@ struct CfgD {
 #ifndef HMOE_DMA_STAGES
 #define HMOE_DMA_STAGES 4
 #endif
+#ifndef HMOE_EAGER_READS
+#define HMOE_EAGER_READS 1
+#endif
+#ifndef HMOE_SETPRIO
+#define HMOE_SETPRIO 0
+#endif
 typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
 
 // 16-byte chunk swizzle of the 64-byte K-contiguous rows (used by the DMA slot mapping and the
@@ -421,6 +427,12 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
   for (int i = 0; i < C::MI; ++i) a[i] = dma_frag<A_KC, C::BM>(bA, wm * C::WM + 16 * i, lr, lg);
 #pragma unroll
   for (int j = 0; j < C::NJ; ++j) b[j] = dma_frag<B_KC, C::BN>(bB, wn * C::WN + 16 * j, lr, lg);
+#if HMOE_EAGER_READS
+  __builtin_amdgcn_sched_barrier(0);
+#endif
+#if HMOE_SETPRIO
+  __builtin_amdgcn_s_setprio(1);
+#endif
   // B as the MFMA's first operand: the 16 x 16 result is the transposed sub-tile, so each lane
   // ends up with four consecutive output columns of one row (see TRANS).
 #pragma unroll
@@ -428,6 +440,9 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j)
       acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
+#if HMOE_SETPRIO
+  __builtin_amdgcn_s_setprio(0);
+#endif
 }
 
 template <class C, int LOADS>
