@@ -366,31 +366,42 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
   float cs[EPV];
 #pragma unroll
   for (int e = 0; e < EPV; ++e) cs[e] = 0.f;
-  for (int t = 0; t < rows; ++t) {
-    const int64_t off = (r0 + t) * V + c0;
-    const i32x4 raw = *reinterpret_cast<const i32x4*>(L + off);
-    const T* lv = reinterpret_cast<const T*>(&raw);
-    const float Lr = s_lse[t];
-    float g[EPV];
+  // rows in groups of U: all U loads in flight before the arithmetic of the group
+  constexpr int U = 4;
+  for (int t0 = 0; t0 < rows; t0 += U) {
+    i32x4 raw[U];
 #pragma unroll
-    for (int e = 0; e < EPV; ++e) g[e] = __expf(to_f32(lv[e]) - Lr);
-    const int32_t cnt = s_cnt[t];
-    const float y = 1.f / (float)cnt;
-    for (int32_t q = 0; q < cnt; ++q) {
-      const int d = (q < MAXT ? s_tag[t * MAXT + q] : tag[s_p0[t] + q]) - c0;
+    for (int u = 0; u < U; ++u)
+      if (t0 + u < rows) raw[u] = *reinterpret_cast<const i32x4*>(L + (r0 + t0 + u) * V + c0);
 #pragma unroll
-      for (int e = 0; e < EPV; ++e)
-        if (d == e) g[e] -= y;
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u;
+      if (t >= rows) break;
+      const T* lv = reinterpret_cast<const T*>(&raw[u]);
+      const float Lr = s_lse[t];
+      float g[EPV];
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) g[e] = __expf(to_f32(lv[e]) - Lr);
+      const int32_t cnt = s_cnt[t];
+      const float y = 1.f / (float)cnt;
+      for (int32_t q = 0; q < cnt; ++q) {
+        const int d = (q < MAXT ? s_tag[t * MAXT + q] : tag[s_p0[t] + q]) - c0;
+        if ((unsigned)d < (unsigned)EPV) {
+#pragma unroll
+          for (int e = 0; e < EPV; ++e)
+            if (d == e) g[e] -= y;
+        }
+      }
+      i32x4 outv;
+      T* ov = reinterpret_cast<T*>(&outv);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        g[e] *= inv_n;
+        cs[e] += g[e];
+        ov[e] = from_f32<T>(g[e]);
+      }
+      *reinterpret_cast<i32x4*>(G + (r0 + t) * V + c0) = outv;
     }
-    i32x4 outv;
-    T* ov = reinterpret_cast<T*>(&outv);
-#pragma unroll
-    for (int e = 0; e < EPV; ++e) {
-      g[e] *= inv_n;
-      cs[e] += g[e];
-      ov[e] = from_f32<T>(g[e]);
-    }
-    *reinterpret_cast<i32x4*>(G + off) = outv;
   }
   float* dst = part_db + (int64_t)blockIdx.x * V + c0;
 #pragma unroll
