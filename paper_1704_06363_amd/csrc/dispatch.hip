@@ -4,8 +4,9 @@
 // Three passes over the int32 ids, all fixed-size blocks of 1024 ids (4 waves x 4 chunks of
 // 64 lanes):
 //   hist    per-wave bucket counts via ballot-built peer masks (lanes with the same id),
-//           summed into block_counts[b][k];
-//   colscan per expert, exclusive prefix of block_counts over blocks -> counts[k];
+//           summed into block_counts[k][b];
+//   colscan per expert (one wave each), exclusive prefix of block_counts[k][*] over blocks
+//           -> counts[k];
 //   offsets exclusive scan of counts (one block);
 //   scatter recomputes the peer masks and writes each id's slot = offsets[k] + earlier blocks
 //           + earlier waves + earlier chunks + rank among earlier peer lanes: the order of
@@ -59,20 +60,38 @@ __global__ void __launch_bounds__(256) k_dispatch_hist(const int32_t* __restrict
   wave_hist(e, n, K, bits, hist + (threadIdx.x >> 6) * K, err);
   __syncthreads();
   for (int k = threadIdx.x; k < K; k += 256)
-    block_counts[(int64_t)blockIdx.x * K + k] = hist[k] + hist[K + k] + hist[2 * K + k] + hist[3 * K + k];
+    block_counts[(int64_t)k * gridDim.x + blockIdx.x] = hist[k] + hist[K + k] + hist[2 * K + k] + hist[3 * K + k];
 }
 
+// One wave per expert k: exclusive prefix over the blocks of block_counts[k][*] (in place) and
+// counts[k] = its total.  Lane l scans a contiguous run of the blocks, the runs are combined by
+// a wave scan.
 __global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ block_counts, int nb, int K,
                                                           int32_t* __restrict__ counts) {
-  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
   if (k >= K) return;
-  int32_t run = 0;
-  for (int b = 0; b < nb; ++b) {
-    const int32_t t = block_counts[(int64_t)b * K + k];
-    block_counts[(int64_t)b * K + k] = run;
-    run += t;
+  int32_t* col = block_counts + (int64_t)k * nb;
+  const int per = (nb + 63) / 64;
+  const int b0 = l * per;
+  int32_t loc = 0;
+  for (int q = 0; q < per; ++q)
+    if (b0 + q < nb) loc += col[b0 + q];
+  // wave exclusive scan of loc
+  int32_t inc = loc;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    const int32_t o = __shfl_up(inc, m, 64);
+    if (l >= m) inc += o;
   }
-  counts[k] = run;
+  int32_t run = inc - loc;
+  for (int q = 0; q < per; ++q)
+    if (b0 + q < nb) {
+      const int32_t t = col[b0 + q];
+      col[b0 + q] = run;
+      run += t;
+    }
+  if (l == 63) counts[k] = inc;
 }
 
 __global__ void __launch_bounds__(1024) k_dispatch_offsets(const int32_t* __restrict__ counts, int K,
@@ -105,7 +124,7 @@ __global__ void __launch_bounds__(256) k_dispatch_scatter(const int32_t* __restr
   wave_hist(e, n, K, bits, hist + w * K, nullptr);
   __syncthreads();
   for (int k = threadIdx.x; k < K; k += 256) {
-    int32_t run = offsets[k] + block_base[(int64_t)blockIdx.x * K + k];
+    int32_t run = offsets[k] + block_base[(int64_t)k * gridDim.x + blockIdx.x];
     for (int q = 0; q < 4; ++q) {
       const int32_t t = hist[q * K + k];
       hist[q * K + k] = run;
@@ -158,7 +177,7 @@ int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int
     HMOE_LAUNCH("dispatch hist", k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        (int32_t*)nullptr);
   }
-  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, bc, (int)nb, K,
+  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, bc, (int)nb, K,
                      counts);
   HMOE_LAUNCH("dispatch offsets", k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
   if (nb > 0) {

@@ -54,6 +54,10 @@ typedef Cfg<bf16, 256, 256, 128, HMOE_BIG_WN> CfgBig;
 // fp32 GEMMs and narrow problems: 128 x 128 tiles, four waves of 64 x 64.
 template <typename T>
 using CfgSmall = Cfg<T, 128, 128, 64, 64>;
+// Few columns (the gater's assignment with K <= 64 centres): 256 x 64 tiles, four waves of
+// 64 x 64 stacked along the rows, so no MFMA work is spent on absent centres.
+template <typename T>
+using CfgNarrow = Cfg<T, 256, 64, 64, 64>;
 
 __device__ __forceinline__ int swz(int row, int chunk) {
   return row * kStageRowBytes + ((chunk ^ ((row ^ (row >> 2)) & 7)) << 4);

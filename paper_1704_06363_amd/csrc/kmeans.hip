@@ -114,8 +114,12 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
   if (min_dist) min_dist[row] = fmaxf(v + xnorm[row], 0.f);
 }
 
-// Centre-tile width of the assignment: bf16 with many centres runs the 256 x 256 engine.
-static int assign_bn(hmoe_dtype_t dt, int32_t K) { return (dt == HMOE_BF16 && K > 128) ? CfgBig::BN : 128; }
+// Centre-tile width of the assignment: up to 64 centres run the narrow 256 x 64 tiles, bf16
+// with many centres the 256 x 256 engine, the rest 128 x 128.
+static int assign_bn(hmoe_dtype_t dt, int32_t K) {
+  if (K <= 64) return 64;
+  return (dt == HMOE_BF16 && K > 128) ? CfgBig::BN : 128;
+}
 
 static size_t assign_ws_bytes(int64_t n, int32_t K, hmoe_dtype_t dt) {
   Workspace ws(nullptr, 0);
@@ -156,11 +160,14 @@ static int assign_t(const typename C::type* X, int64_t n, int32_t d, const typen
 
 int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const void* C, int32_t K, int32_t* assign,
                   float* min_dist, Workspace& ws, hipStream_t st) {
+  const int bn = assign_bn(dt, K);
   if (dt == HMOE_BF16) {
-    if (assign_bn(dt, K) == CfgBig::BN)
+    if (bn == 64) return assign_t<CfgNarrow<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+    if (bn == CfgBig::BN)
       return assign_t<CfgBig>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
   }
+  if (bn == 64) return assign_t<CfgNarrow<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
   return assign_t<CfgSmall<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
 }
 
@@ -176,39 +183,63 @@ __global__ void k_kpp_first(const double* __restrict__ u, int64_t n, int32_t* __
 }
 
 // D2[i] = min(D2[i], |x_i - X[idx[t]]|^2) (fp64 direct differences; t == 0 initialises) and
-// bsum[b] = sum of D2 over the block's rows in row order.
+// bsum[b] = sum of D2 over the block's kKppRows rows, in a fixed order.  16 lanes share a row
+// (16-byte loads, fp64 partial sums reduced over the 16 lanes), so each wave streams 4 rows at
+// once and the block 16.
 template <typename T>
 __global__ void __launch_bounds__(256) k_kpp_update(const T* __restrict__ X, int64_t n, int d,
                                                     const int32_t* __restrict__ idx, int t,
                                                     double* __restrict__ D2, double* __restrict__ bsum) {
-  __shared__ double wsum[4];
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  constexpr int EPV = 16 / sizeof(T);
+  constexpr int G = 16;  // lanes per row
+  __shared__ double rowv[kKppRows];
+  const int lane = threadIdx.x % G;         // position inside the row group
+  const int grp = threadIdx.x / G;          // 16 row groups per block
   const T* c = X + (int64_t)idx[t] * d;
   const int64_t r0 = (int64_t)blockIdx.x * kKppRows;
-  double run = 0.0;  // lane 0: this wave's rows in order
-  for (int q = 0; q < kKppRows / 4; ++q) {
-    const int64_t i = r0 + w * (kKppRows / 4) + q;
-    if (i >= n) break;
-    const T* x = X + i * d;
+  const int vpr = d / EPV;                  // 16-byte vectors per row
+  for (int q = 0; q < kKppRows / 16; ++q) {
+    const int lr = q * 16 + grp;
+    const int64_t i = r0 + lr;
     double s = 0.0;
-    for (int j = l; j < d; j += 64) {
-      const double df = (double)to_f32(x[j]) - (double)to_f32(c[j]);
-      s += df * df;
+    if (i < n) {
+      const T* x = X + i * d;
+      for (int v = lane; v < vpr; v += G) {
+        const i32x4 xr = *reinterpret_cast<const i32x4*>(x + v * EPV);
+        const i32x4 cr = *reinterpret_cast<const i32x4*>(c + v * EPV);
+        const T* xe = reinterpret_cast<const T*>(&xr);
+        const T* ce = reinterpret_cast<const T*>(&cr);
+#pragma unroll
+        for (int z = 0; z < EPV; ++z) {
+          const double df = (double)to_f32(xe[z]) - (double)to_f32(ce[z]);
+          s += df * df;
+        }
+      }
     }
-    s = wave_sum(s);
-    double v = s;
-    if (t > 0) {
-      const double old = D2[i];
-      v = old < s ? old : s;
-    }
-    if (l == 0) {
-      D2[i] = v;
-      run += v;
+#pragma unroll
+    for (int m = 1; m < G; m <<= 1) s += shfl_xor(s, m);
+    if (lane == 0) {
+      double v = 0.0;
+      if (i < n) {
+        v = s;
+        if (t > 0) {
+          const double old = D2[i];
+          v = old < s ? old : s;
+        }
+        D2[i] = v;
+      }
+      rowv[lr] = v;
     }
   }
-  if (l == 0) wsum[w] = run;
   __syncthreads();
-  if (threadIdx.x == 0) bsum[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+  // block sum in row order, split over the first wave: lane l adds rows 4l..4l+3, then the
+  // lanes are combined by the wave's fixed butterfly
+  if (threadIdx.x < 64) {
+    double s = ((rowv[4 * threadIdx.x] + rowv[4 * threadIdx.x + 1]) + rowv[4 * threadIdx.x + 2]) +
+               rowv[4 * threadIdx.x + 3];
+    s = wave_sum(s);
+    if (threadIdx.x == 0) bsum[blockIdx.x] = s;
+  }
 }
 
 // Picks centre t: the first row whose running D^2 sum exceeds u[t] * total (lowest unchosen row

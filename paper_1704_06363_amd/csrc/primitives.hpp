@@ -78,7 +78,7 @@ __device__ __forceinline__ int find_segment(const int32_t* __restrict__ tile_sta
 //
 // out[e][j] = sum over rows p in [seg[e], seg[e+1]) of X[rowmap ? rowmap[p] : p][j], computed
 // deterministically: pieces of at most kSegPiece rows are summed in fp64 in row order, then
-// the pieces of each segment are added in order.
+// the pieces of each segment are added in a fixed order (k_segsum_final).
 
 constexpr int kSegPiece = 256;
 constexpr int kSegMaxVec = 4;  // vectors per thread: w <= 1024 * 16 / sizeof(T)
@@ -147,7 +147,9 @@ __global__ void __launch_bounds__(256) k_segsum_partial(const T* __restrict__ X,
   }
 }
 
-// out[e][j] (=, or += when accumulate) sum of the pieces of segment e, in order.
+// out[e][j] (=, or += when accumulate) sum of the pieces of segment e in a fixed order: the
+// segment's piece number m goes to partial sum m % 8 (each summed in piece order), then the 8
+// partials are added pairwise -- 8 independent chains keep the loads in flight.
 template <typename O>
 __global__ void __launch_bounds__(256) k_segsum_final(const double* __restrict__ part,
                                                       const int32_t* __restrict__ tile_start, int G,
@@ -155,8 +157,16 @@ __global__ void __launch_bounds__(256) k_segsum_final(const double* __restrict__
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)G * w) return;
   const int e = (int)(idx / w), j = (int)(idx % w);
-  double s = 0.0;
-  for (int32_t q = tile_start[e]; q < tile_start[e + 1]; ++q) s += part[(int64_t)q * w + j];
+  const int32_t q0 = tile_start[e], q1 = tile_start[e + 1];
+  double p[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int32_t q = q0;
+  for (; q + 8 <= q1; q += 8)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) p[u] += part[(int64_t)(q + u) * w + j];
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+    if (q + u < q1) p[u] += part[(int64_t)(q + u) * w + j];
+  const double s = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
   if (accumulate) out[idx] = (O)((double)out[idx] + s);
   else out[idx] = (O)s;
 }
