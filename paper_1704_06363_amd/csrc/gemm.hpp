@@ -46,11 +46,6 @@ struct Cfg {
   static constexpr int LDS = 2 * (A_BYTES + B_BYTES);
 };
 
-// bf16 GEMMs: 256 x 256 tiles, eight waves of 128 x 64 (one workgroup, two waves per SIMD).
-#ifndef HMOE_BIG_WN
-#define HMOE_BIG_WN 64
-#endif
-typedef Cfg<bf16, 256, 256, 128, HMOE_BIG_WN> CfgBig;
 // fp32 GEMMs and narrow problems: 128 x 128 tiles, four waves of 64 x 64.
 template <typename T>
 using CfgSmall = Cfg<T, 128, 128, 64, 64>;
@@ -261,9 +256,6 @@ __device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict
       sb.load(B, ldb, b_rows, (kt + 1) * C::BK, k_len);
     }
     mfma_stage<C>(bufA0 + cur * C::A_BYTES, bufB0 + cur * C::B_BYTES, acc);
-#if defined(HMOE_IGLP)
-    __builtin_amdgcn_iglp_opt(HMOE_IGLP);
-#endif
     if (more) {
       if constexpr (ROWNORM) sa.add_sq(xs);
       sa.store(bufA0 + (cur ^ 1) * C::A_BYTES);
@@ -316,12 +308,7 @@ struct CfgD {
 #ifndef HMOE_DMA_STAGES
 #define HMOE_DMA_STAGES 4
 #endif
-#ifndef HMOE_EAGER_READS
-#define HMOE_EAGER_READS 1
-#endif
-#ifndef HMOE_SETPRIO
-#define HMOE_SETPRIO 0
-#endif
+
 typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
 
 // 16-byte chunk swizzle of the 64-byte K-contiguous rows (used by the DMA slot mapping and the
@@ -419,9 +406,12 @@ __device__ __forceinline__ bf16x8 dma_frag(const lds<char>* buf, int r0, int lr,
   }
 }
 
-template <class C, bool A_KC, bool B_KC>
+// ROWNORM: xs[i] += squares of this lane's 8 elements of A fragment i, for the fragments
+// i = wn (mod WAVES_N) that this wave is responsible for (the work is spread over the waves
+// that share the rows; each row's sum stays within one wave).
+template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
 __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<char>* bB,
-                                               floatx4 (&acc)[C::MI][C::NJ]) {
+                                               floatx4 (&acc)[C::MI][C::NJ], float* xs = nullptr) {
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wm = w / C::WAVES_N, wn = w % C::WAVES_N;
@@ -431,12 +421,9 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
   for (int i = 0; i < C::MI; ++i) a[i] = dma_frag<A_KC, C::BM>(bA, wm * C::WM + 16 * i, lr, lg);
 #pragma unroll
   for (int j = 0; j < C::NJ; ++j) b[j] = dma_frag<B_KC, C::BN>(bB, wn * C::WN + 16 * j, lr, lg);
-#if HMOE_EAGER_READS
+  // all of the stage's fragment reads go out before its MFMAs (measured faster than letting
+  // the scheduler interleave them)
   __builtin_amdgcn_sched_barrier(0);
-#endif
-#if HMOE_SETPRIO
-  __builtin_amdgcn_s_setprio(1);
-#endif
   // B as the MFMA's first operand: the 16 x 16 result is the transposed sub-tile, so each lane
   // ends up with four consecutive output columns of one row (see TRANS).
 #pragma unroll
@@ -444,9 +431,17 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j)
       acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
-#if HMOE_SETPRIO
-  __builtin_amdgcn_s_setprio(0);
-#endif
+  if constexpr (ROWNORM) {
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+      if ((i % C::WAVES_N) == wn) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = (float)a[i][e];
+          xs[i] += v * v;
+        }
+      }
+  }
 }
 
 template <class C, int LOADS>
@@ -460,10 +455,16 @@ __device__ __forceinline__ void wait_stage(int pending_stages) {
   }
 }
 
-template <class C, bool A_KC, bool B_KC>
+template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
 __device__ __forceinline__ void gemm_tile_dma(const bf16* __restrict__ A, int64_t lda, int a_rows,
                                               const bf16* __restrict__ B, int64_t ldb, int b_rows, int k_len,
-                                              lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ]) {
+                                              lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
+                                              float* xs = nullptr) {
+  static_assert(!ROWNORM || A_KC, "row norms need a K-contiguous A");
+  if constexpr (ROWNORM) {
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i) xs[i] = 0.f;
+  }
   using OA = DmaOperand<C::BM, C::THREADS, A_KC>;
   using OB = DmaOperand<C::BN, C::THREADS, B_KC>;
   constexpr int LOADS = OA::NQ + OB::NQ;
@@ -495,14 +496,14 @@ __device__ __forceinline__ void gemm_tile_dma(const bf16* __restrict__ A, int64_
       ob.issue(B, ldb, nx * C::BK, bufB(sb));
     }
     const int sc = kt % C::NS;
-    dma_mfma_stage<C, A_KC, B_KC>(bufA(sc), bufB(sc), acc);
+    dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(sc), bufB(sc), acc, xs);
   }
   if (nfull * C::BK < k_len) {
     const int sb = nfull % C::NS;
     oa.tail(A, lda, nfull * C::BK, k_len, bufA(sb));
     ob.tail(B, ldb, nfull * C::BK, k_len, bufB(sb));
     wg_barrier_lds();
-    dma_mfma_stage<C, A_KC, B_KC>(bufA(sb), bufB(sb), acc);
+    dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(sb), bufB(sb), acc, xs);
   }
   wg_barrier_lds();
 }
@@ -514,8 +515,7 @@ __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A
                                           int k_len, lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
                                           float* xs = nullptr) {
   if constexpr (C::DMA) {
-    static_assert(!ROWNORM, "row norms need the register-staged engine");
-    gemm_tile_dma<C, A_KC, B_KC>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc);
+    gemm_tile_dma<C, A_KC, B_KC, ROWNORM>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc, xs);
   } else {
     gemm_tile_reg<C, A_KC, B_KC, ROWNORM>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc, xs);
   }

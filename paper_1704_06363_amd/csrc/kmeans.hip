@@ -101,6 +101,84 @@ __global__ void __launch_bounds__(C::THREADS)
   }
 }
 
+// The same tile on the direct-to-LDS engine (bf16, many centres).  Each lane holds four
+// consecutive centres of one row per fragment; the row norms come from the A fragments the
+// engine already reads (fragment i summed by wave i mod WAVES_N).
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_assign_dma(const bf16* __restrict__ X, int64_t n, int d, const bf16* __restrict__ Cn, int K,
+                 const float* __restrict__ cn, int32_t* __restrict__ assign, float* __restrict__ min_dist,
+                 float* __restrict__ part_v, int32_t* __restrict__ part_i, float* __restrict__ xnorm) {
+  static_assert(C::DMA && C::TRANS, "direct-to-LDS configuration expected");
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  const TileCoord tc = tile_plain<C>(n, K, d);
+  if (!tc.valid) return;
+  floatx4 acc[C::MI][C::NJ];
+  float xs[C::MI];
+  gemm_tile<C, true, true, true>(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem, acc,
+                                 xs);
+  using F = Frag<C>;
+  const F f;
+  lds<float>* xn = reinterpret_cast<lds<float>*>(smem);  // [BM]
+  lds<float>* rv = xn + C::BM;                           // [WAVES_N][BM]
+  lds<int32_t>* ri = reinterpret_cast<lds<int32_t>*>(rv + C::WAVES_N * C::BM);
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+    if ((i % C::WAVES_N) == f.wn) {
+      float s = xs[i];
+      s += shfl_xor(s, 16);
+      s += shfl_xor(s, 32);
+      if (f.lg == 0) xn[f.row(i, 0)] = s;
+    }
+  float cv[F::NCOL];
+#pragma unroll
+  for (int q = 0; q < F::NCOL; ++q) {
+    const int col = f.colq(q);
+    cv[q] = col < tc.n_cols ? cn[tc.n0 + col] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i) {
+    float best = FLT_MAX;
+    int bi = INT_MAX;
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int col = f.col(j, r);
+        if (col < tc.n_cols) argmin_merge(best, bi, cv[F::qidx(j, r)] - 2.f * acc[i][j][r], tc.n0 + col);
+      }
+#pragma unroll
+    for (int m = 16; m < 64; m <<= 1) {
+      const float v2 = shfl_xor(best, m);
+      const int i2 = shfl_xor(bi, m);
+      argmin_merge(best, bi, v2, i2);
+    }
+    if (f.lg == 0) {
+      rv[f.wn * C::BM + f.row(i, 0)] = best;
+      ri[f.wn * C::BM + f.row(i, 0)] = bi;
+    }
+  }
+  __syncthreads();
+  const int nt = (int)cdiv(K, C::BN);
+  for (int q = threadIdx.x; q < tc.m_rows; q += C::THREADS) {
+    float v = rv[q];
+    int bi = ri[q];
+#pragma unroll
+    for (int w = 1; w < C::WAVES_N; ++w) argmin_merge(v, bi, rv[w * C::BM + q], ri[w * C::BM + q]);
+    const int64_t row = tc.m0 + q;
+    if (nt == 1) {
+      assign[row] = bi;
+      if (min_dist) min_dist[row] = fmaxf(v + xn[q], 0.f);
+    } else {
+      const int ti = tc.n0 / C::BN;
+      part_v[(int64_t)ti * n + row] = v;
+      part_i[(int64_t)ti * n + row] = bi;
+      if (ti == 0) xnorm[row] = xn[q];
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ part_v,
                                                       const int32_t* __restrict__ part_i,
                                                       const float* __restrict__ xnorm, int64_t n, int nt,
@@ -115,10 +193,10 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
 }
 
 // Centre-tile width of the assignment: up to 64 centres run the narrow 256 x 64 tiles, bf16
-// with many centres the 256 x 256 engine, the rest 128 x 128.
+// with many centres the 256 x 256 direct-to-LDS engine, the rest 128 x 128.
 static int assign_bn(hmoe_dtype_t dt, int32_t K) {
   if (K <= 64) return 64;
-  return (dt == HMOE_BF16 && K > 128) ? CfgBig::BN : 128;
+  return (dt == HMOE_BF16 && K > 128) ? CfgDma::BN : 128;
 }
 
 static size_t assign_ws_bytes(int64_t n, int32_t K, hmoe_dtype_t dt) {
@@ -150,8 +228,12 @@ static int assign_t(const typename C::type* X, int64_t n, int32_t d, const typen
   HMOE_LAUNCH("centre norms", k_cnorm<T>, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, Cn, K, d, cn);
   if (n == 0) return HMOE_OK;
   const int64_t tiles = cdiv(n, C::BM) * nt;
-  HMOE_LAUNCH("assign", k_assign<C>, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, st, X, n, d, Cn, K, cn, assign,
-              min_dist, pv, pi, xn);
+  if constexpr (C::DMA)
+    HMOE_LAUNCH("assign", k_assign_dma<C>, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, st, X, n, d, Cn, K, cn,
+                assign, min_dist, pv, pi, xn);
+  else
+    HMOE_LAUNCH("assign", k_assign<C>, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, st, X, n, d, Cn, K, cn,
+                assign, min_dist, pv, pi, xn);
   if (nt > 1)
     HMOE_LAUNCH("assign merge", k_assign_merge, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, pv, pi, xn, n, nt,
                 assign, min_dist);
@@ -163,8 +245,8 @@ int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const vo
   const int bn = assign_bn(dt, K);
   if (dt == HMOE_BF16) {
     if (bn == 64) return assign_t<CfgNarrow<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
-    if (bn == CfgBig::BN)
-      return assign_t<CfgBig>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+    if (bn == CfgDma::BN)
+      return assign_t<CfgDma>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
   }
   if (bn == 64) return assign_t<CfgNarrow<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
