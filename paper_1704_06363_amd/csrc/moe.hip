@@ -176,7 +176,8 @@ __global__ void __launch_bounds__(C::THREADS)
   }
 }
 
-// lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row.
+// lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row (row
+// widths are multiples of 8, so o / (16 / sizeof(T)) vectors cover a row exactly).
 template <typename T>
 __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, const float* __restrict__ ps,
                                                   int nt, const T* __restrict__ H, const T* __restrict__ D,
@@ -193,17 +194,29 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
   for (int t = l; t < nt; t += 64) S += ps[(int64_t)t * n + row] * __expf(pm[(int64_t)t * n + row] - M);
   S = wave_sum(S);
   const float Lv = M + __logf(S);
+  // positive logits: lane group g (8 lanes) takes tags g, g + 8, ...; each lane covers every
+  // 8th 16-byte chunk of the rows; the partial sums are combined over the wave in a fixed order
+  constexpr int EPV = 16 / sizeof(T);
   const int32_t p0 = row_ptr[row], p1 = row_ptr[row + 1];
+  const int g = l >> 3, gl = l & 7;
   const T* h = H + row * o;
+  const int vpr = o / EPV;
   float pos = 0.f;
-  for (int32_t q = p0; q < p1; ++q) {
+  for (int32_t q = p0 + g; q < p1; q += 8) {
     const int32_t tg = tag[q];
     const T* dv = D + (int64_t)tg * o;
     float s = 0.f;
-    for (int j = l; j < o; j += 64) s += to_f32(h[j]) * to_f32(dv[j]);
-    s = wave_sum(s);
-    pos += s + (bD ? to_f32(bD[tg]) : 0.f);
+    for (int v = gl; v < vpr; v += 8) {
+      const i32x4 hr = *reinterpret_cast<const i32x4*>(h + v * EPV);
+      const i32x4 dr = *reinterpret_cast<const i32x4*>(dv + v * EPV);
+      const T* he = reinterpret_cast<const T*>(&hr);
+      const T* de = reinterpret_cast<const T*>(&dr);
+#pragma unroll
+      for (int z = 0; z < EPV; ++z) s += to_f32(he[z]) * to_f32(de[z]);
+    }
+    pos += s + ((bD && gl == 0) ? to_f32(bD[tg]) : 0.f);
   }
+  pos = wave_sum(pos);
   if (l == 0) {
     lse[row] = Lv;
     loss[row] = Lv - pos / (float)(p1 - p0);

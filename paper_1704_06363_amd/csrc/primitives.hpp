@@ -101,21 +101,33 @@ __global__ void __launch_bounds__(256) k_segsum_partial(const T* __restrict__ X,
   const int RG = VPR >= 256 ? 1 : 256 / VPR;
   const int rg = VPR >= 256 ? 0 : t / VPR;
   const int v0 = VPR >= 256 ? t : t % VPR;
+  __shared__ int64_t rows_s[kSegPiece];  // the piece's source rows, staged once
+  for (int64_t p = r0 + t; p < r1; p += 256) rows_s[p - r0] = rowmap ? rowmap[p] : p;
+  __syncthreads();
   double acc[kSegMaxVec][EPV];
 #pragma unroll
   for (int q = 0; q < kSegMaxVec; ++q)
 #pragma unroll
     for (int z = 0; z < EPV; ++z) acc[q][z] = 0.0;
   if (rg < RG) {
-    for (int64_t p = r0 + rg; p < r1; p += RG) {
-      const int64_t row = rowmap ? rowmap[p] : p;
-      const T* src = X + row * ld;
+    // rows in groups of U (loads of the group in flight together), added in row order
+    constexpr int U = 4;
+    const int cnt = (int)(r1 - r0);
+    for (int p0 = rg; p0 < cnt; p0 += U * RG) {
 #pragma unroll
       for (int q = 0; q < kSegMaxVec; ++q) {
         const int v = v0 + q * 256;
-        if (v < VPR && (q == 0 || VPR > 256)) {
-          const i32x4 raw = *reinterpret_cast<const i32x4*>(src + v * EPV);
-          const T* e8 = reinterpret_cast<const T*>(&raw);
+        if (!(v < VPR && (q == 0 || VPR > 256))) continue;
+        i32x4 raw[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int p = p0 + u * RG;
+          if (p < cnt) raw[u] = *reinterpret_cast<const i32x4*>(X + rows_s[p] * ld + v * EPV);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (p0 + u * RG >= cnt) break;
+          const T* e8 = reinterpret_cast<const T*>(&raw[u]);
 #pragma unroll
           for (int z = 0; z < EPV; ++z) acc[q][z] += (double)to_f32(e8[z]);
         }
