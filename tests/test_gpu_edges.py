@@ -1,0 +1,120 @@
+"""Edge cases of the HIP path against the fp64 oracle: rows with more tags than the gradient
+kernels stage in LDS, the narrowest widths the ABI allows, a single sample, the largest K, and
+exactly duplicated centres (ties must go to the lower index)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_1704_06363_amd import hmoe
+from paper_1704_06363_amd import workloads as W
+from tests.parity import RTOL, assert_assign, assert_close, assert_scalar_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+
+
+def _step_vs_oracle(X, ids, K, p, rp, tg, store, saved):
+    """Forward on the HIP path vs the oracle, then the backward from the oracle's saved
+    activations (and, with `saved`, its stored logits)."""
+    rt = RTOL[store]
+    a = torch.as_tensor(ids, dtype=torch.int32).cuda()
+    d = hmoe.moe_dispatch(a, K, rows=X)
+    row_ptr = torch.tensor(rp, device="cuda")
+    tag = torch.tensor(tg, device="cuda")
+    f = hmoe.moe_forward(p, d["rows_sorted"], d["offsets"], d["perm"], row_ptr, tag, save_logits=saved)
+    Xh = np64(X)
+    ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
+    ref = O.moe_forward(Xh, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
+                        store=store, want_logits=saved)
+    perm = npi(d["perm"])
+    assert_close(f["H1_sorted"], ref["H1"][perm], rt, "H1_sorted")
+    assert_close(f["H"], ref["H"], rt, "H")
+    assert_close(f["lse"], ref["lse"], rt, "lse")
+    assert_close(f["loss"], ref["loss"], rt, "loss")
+    assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
+    tdt = torch.bfloat16 if store == "bf16" else torch.float32
+    H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(tdt).cuda()
+    H = torch.tensor(ref["H"], dtype=torch.float32).to(tdt).cuda()
+    lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
+    Lg = torch.tensor(ref["logits"], dtype=torch.float32).to(tdt).cuda() if saved else None
+    g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag, H1s, H,
+                          lse, logits=Lg)
+    gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
+                        ref["lse"], store=store, logit_round=saved)
+    for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
+        assert_close(g[k], gr[k], rt, k)
+
+
+@pytest.mark.parametrize("saved", [False, True])
+def test_rows_with_many_tags(saved):
+    # 17..24 tags on every other row: past the 16 tags per row the gradient kernels stage in LDS
+    n, d, h, o, V, K = 300, 64, 128, 64, 264, 3
+    rp_few, tg_few = W.zipf_labels(n, V, 3, seed=40)
+    rp_many, tg_many = W.zipf_labels(n, V, 24, seed=41, min_tags=17)
+    rows = []
+    for i in range(n):
+        src = (rp_many, tg_many) if i % 2 == 0 else (rp_few, tg_few)
+        rows.append(src[1][src[0][i]:src[0][i + 1]])
+    rp = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
+    tg = np.concatenate(rows).astype(np.int32)
+    assert (rp[1:] - rp[:-1]).max() > 16
+    X = W.rectified_gaussian(n, d, seed=42, dtype="bf16", device="cuda")
+    ids = np.random.default_rng(43).integers(0, K, n).astype(np.int32)
+    p = W.moe_params(K, d, h, o, V, seed=44, dtype="bf16", device="cuda", bias=True)
+    _step_vs_oracle(X, ids, K, p, rp, tg, "bf16", saved)
+
+
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+def test_narrowest_widths(store):
+    # every width at the ABI's minimum of 8; n leaves a ragged tail in every tile size
+    n, K = 37, 3
+    X = W.rectified_gaussian(n, 8, seed=50, dtype=store, device="cuda")
+    ids = np.random.default_rng(51).integers(0, K, n).astype(np.int32)
+    rp, tg = W.zipf_labels(n, 8, 3, seed=52)
+    p = W.moe_params(K, 8, 8, 8, 8, seed=53, dtype=store, device="cuda", bias=True)
+    _step_vs_oracle(X, ids, K, p, rp, tg, store, saved=(store == "bf16"))
+    C = X[:K].contiguous()
+    a, md = hmoe.kmeans_assign(X, C)
+    a_ref, d1, d2 = O.assign(np64(X), np64(C))
+    assert_assign(a, a_ref, d1, d2)
+    assert_close(md, d1, 1e-4, "min_dist")
+
+
+def test_single_sample():
+    X = W.rectified_gaussian(1, 64, seed=60, dtype="bf16", device="cuda")
+    rp, tg = W.zipf_labels(1, 96, 5, seed=61)
+    p = W.moe_params(4, 64, 64, 32, 96, seed=62, dtype="bf16", device="cuda")
+    _step_vs_oracle(X, np.array([2], np.int32), 4, p, rp, tg, "bf16", saved=True)
+
+
+def test_largest_K_assign_and_dispatch():
+    n, d, K = 5000, 64, 4096
+    X = W.gmm_features(n, d, 64, seed=70, dtype="bf16", device="cuda")
+    C = W.gmm_features(K, d, 64, seed=71, dtype="bf16", device="cuda")
+    a, md = hmoe.kmeans_assign(X, C)
+    a_ref, d1, d2 = O.assign(np64(X), np64(C))
+    assert_assign(a, a_ref, d1, d2)
+    assert_close(md, d1, 1e-4, "min_dist")
+    ids = np.random.default_rng(72).integers(0, K, n).astype(np.int32)
+    dd = hmoe.moe_dispatch(torch.as_tensor(ids).cuda(), K)
+    counts, offsets, perm, inv = O.dispatch(ids, K)
+    assert npi(dd["counts"]).tolist() == counts.tolist()
+    assert npi(dd["offsets"]).tolist() == offsets.tolist()
+    assert np.array_equal(npi(dd["perm"]), perm) and np.array_equal(npi(dd["inv"]), inv)
+
+
+@pytest.mark.parametrize("dtype,K", [("f32", 40), ("bf16", 40), ("bf16", 100), ("bf16", 600)])
+def test_duplicated_centres_break_ties_low(dtype, K):
+    # centre 2j+1 is an exact copy of centre 2j: identical distances, so the lower index wins
+    # on every row (the oracle's near-tie exemption would skip these rows, so check directly)
+    n, d = 3000, 128
+    X = W.gmm_features(n, d, 32, seed=80, dtype=dtype, device="cuda")
+    base = X[torch.randperm(n, generator=torch.Generator().manual_seed(81))[:K // 2].cuda()]
+    C = base.repeat_interleave(2, dim=0).contiguous()
+    a, md = hmoe.kmeans_assign(X, C)
+    a = npi(a)
+    assert np.all(a % 2 == 0)
+    # and the chosen pair is the nearest one (exact duplicates removed: plain parity)
+    a_ref, d1, d2 = O.assign(np64(X), np64(base))
+    assert_assign(a // 2, a_ref, d1, d2)
+    assert_close(md, d1, 1e-4, "min_dist")
