@@ -538,11 +538,10 @@ struct TileCoord {
 // Plain problem: M x N tiles, bands of `band` m-tiles walked m-fastest so that concurrently
 // running workgroups share both operand tiles in the caches.
 template <class C>
-__device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
+__device__ __forceinline__ TileCoord tile_plain_at(int64_t M, int N, int K, int64_t b) {
   TileCoord tc;
   const int64_t mt = cdiv(M, C::BM);
   const int nt = (int)cdiv(N, C::BN);
-  const int64_t b = blockIdx.x;
   constexpr int band = 16;
   const int64_t band_tiles = (int64_t)band * nt;
   const int64_t g = b / band_tiles;
@@ -560,6 +559,10 @@ __device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
   tc.k0 = 0;
   tc.k_len = K;
   return tc;
+}
+template <class C>
+__device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
+  return tile_plain_at<C>(M, N, K, blockIdx.x);
 }
 
 // Row-grouped problem (experts' forward / input-gradient GEMMs): group e owns rows

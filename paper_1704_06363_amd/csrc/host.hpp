@@ -47,6 +47,19 @@ inline size_t dtype_size(hmoe_dtype_t dt) { return dt == HMOE_BF16 ? 2 : 4; }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Compute units of the current device; cached per device.
+inline int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    cache[dev] = cus;
+  }
+  return cache[dev];
+}
+
 // Optional per-launch HIP-event timing (off unless hmoe_timer_enable(1) was called).
 void timer_pre(const char* label, hipStream_t st);
 void timer_post(hipStream_t st);

@@ -445,18 +445,59 @@ __global__ void __launch_bounds__(C::THREADS)
   store_out<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
 }
 
-// dD = G^T H (fp32).
+// dD = G^T H (fp32), reduction over the n samples.  The tiles are run in rounds of one per
+// resident workgroup; when the last round is only partly filled, its tiles are split over K
+// instead: tiles b < t_full run whole, tile t_full + r (r < R) is computed as `split` K-chunks
+// (work items t_full + r * split + c) whose fp32 partials go to part[r * split + c] and are
+// added in chunk order by k_split_reduce.
+constexpr int kMaxSplitItems = 512;
+
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_dD(const typename C::type* __restrict__ G, const typename C::type* __restrict__ H, int64_t n, int V, int o,
-             float* __restrict__ dD) {
+             float* __restrict__ dD, int64_t t_full, int split, float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_plain<C>(V, o, (int)n);
-  if (!tc.valid) return;
+  const int64_t T = cdiv(V, C::BM) * cdiv(o, C::BN);
+  const int64_t b = blockIdx.x;
   floatx4 acc[C::MI][C::NJ];
-  gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
-  store_out<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
+  if (b < t_full) {
+    const TileCoord tc = tile_plain_at<C>(V, o, (int)n, b);
+    if (!tc.valid) return;
+    gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
+    store_out<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
+    return;
+  }
+  const int64_t q = b - t_full;
+  const int64_t t = t_full + q / split;
+  if (t >= T) return;
+  const int c = (int)(q % split);
+  const TileCoord tc = tile_plain_at<C>(V, o, (int)n, t);
+  const int64_t chunk = cdiv(cdiv(n, split), 32) * 32;
+  const int64_t k0 = c * chunk;
+  const int64_t kl = n - k0 < chunk ? n - k0 : chunk;
+  const int klen = kl > 0 ? (int)kl : 0;
+  gemm_tile<C, false, false>(G + tc.m0 + (k0 < n ? k0 : 0) * V, V, tc.m_rows, H + tc.n0 + (k0 < n ? k0 : 0) * o, o,
+                             tc.n_cols, klen, smem, acc);
+  TileCoord lt = tc;
+  lt.m0 = 0;
+  lt.n0 = 0;
+  store_out<C, float>(lt, acc, smem, part + q * (int64_t)(C::BM * C::BN), C::BN, Ident{}, RowId{0}, NoVec{});
+}
+
+template <class C>
+__global__ void __launch_bounds__(256) k_split_reduce(const float* __restrict__ part, int64_t n, int V, int o,
+                                                      int64_t t_full, int split, int R, float* __restrict__ dD) {
+  constexpr int TE = C::BM * C::BN;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)R * TE) return;
+  const int r = (int)(idx / TE), e = (int)(idx % TE);
+  const int i = e / C::BN, j = e % C::BN;
+  const TileCoord tc = tile_plain_at<C>(V, o, (int)n, t_full + r);
+  if (i >= tc.m_rows || j >= tc.n_cols) return;
+  float s = 0.f;
+  for (int c = 0; c < split; ++c) s += part[((int64_t)r * split + c) * TE + e];
+  dD[(tc.m0 + i) * (int64_t)o + tc.n0 + j] = s;
 }
 
 // ------------------------------------------------------------------ expert backward
@@ -553,6 +594,7 @@ static size_t bwd_ws(const MoeShape& s) {
   ws.take<T>((size_t)s.n * s.h);
   const int64_t prow = cdiv(s.n, C::BM) > cdiv(s.n, kGradRows) ? cdiv(s.n, C::BM) : cdiv(s.n, kGradRows);
   ws.take<float>((size_t)prow * s.V);
+  ws.take<float>((size_t)kMaxSplitItems * C::BM * C::BN);
   const int w = s.h > s.o ? s.h : s.o;
   return ws.off + segsum_ws(s.n, s.K, w) + 256;
 }
@@ -605,6 +647,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   const int mt = (int)cdiv(n, C::BM);
   const int gr = (int)cdiv(n, kGradRows);
   float* pdb = ws.take<float>((size_t)(mt > gr ? mt : gr) * s.V);
+  float* split_part = ws.take<float>((size_t)kMaxSplitItems * C::BM * C::BN);
   if (!ws.fits()) return HMOE_EWORKSPACE;
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
@@ -627,8 +670,21 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
                 s.V, dbD);
   HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
               (const T*)G, D, n, s.V, s.o, inv, dYs);
-  HMOE_LAUNCH("decoder dD", k_dec_dD<C>, dim3((unsigned)(cdiv(s.V, C::BM) * cdiv(s.o, C::BN))), dim3(C::THREADS),
-              C::LDS, st, (const T*)G, H, n, s.V, s.o, dD);
+  {
+    // rounds of `slots` concurrent tiles (one workgroup per 160 KB of LDS per CU); the tiles of
+    // a partial last round are split over K to fill it
+    const int64_t tiles = cdiv(s.V, C::BM) * cdiv(s.o, C::BN);
+    int64_t slots = (int64_t)device_cus() * ((160 * 1024) / C::LDS);
+    if (slots > kMaxSplitItems) slots = kMaxSplitItems;
+    const int64_t R = tiles % slots;
+    const int64_t t_full = tiles - R;
+    const int split = R > 0 ? (int)(slots / R) : 1;
+    HMOE_LAUNCH("decoder dD", k_dec_dD<C>, dim3((unsigned)(t_full + R * split)), dim3(C::THREADS), C::LDS, st,
+                (const T*)G, H, n, s.V, s.o, dD, t_full, split, split_part);
+    if (R > 0)
+      HMOE_LAUNCH("decoder dD reduce", k_split_reduce<C>, dim3((unsigned)cdiv(R * C::BM * C::BN, 256)), dim3(256), 0,
+                  st, split_part, n, s.V, s.o, t_full, split, (int)R, dD);
+  }
   // experts
   HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
   const size_t mark = ws.off;
