@@ -2,14 +2,16 @@
 // figure) and the multilabel softmax loss (Section 4.1, Eq. 3), forward and backward.
 //
 // Rows arrive grouped by expert (X_sorted, offsets).  Every contraction runs on the MFMA tile
-// engine of gemm.hpp:
+// engines of gemm.hpp (bf16: the direct-to-LDS engine; fp32: the register-staged one):
 //   experts, forward     row-grouped NT GEMMs (bias + ReLU epilogue; the second layer's
 //                        epilogue writes rows straight back to sample order = the combine)
-//   decoder, forward     NT GEMM H . D^T with a per-row (max, sum exp) epilogue; the V logits
-//                        are never stored; a merge pass forms lse and the loss
-//   decoder, backward    the logits are recomputed and turned into g = (p - y)/n (stored) with
-//                        per-tile column sums for dbD; then dH = g D (epilogue scatters rows to
-//                        expert order) and dD = g^T H
+//   decoder, forward     NT GEMM H . D^T with a per-row (max, sum exp) epilogue and, when the
+//                        caller keeps them for the backward, the logits stored in the data
+//                        dtype; a merge pass forms lse and the loss
+//   decoder, backward    g = (p - y)/n, formed elementwise from the stored logits (or, without
+//                        them, from logits recomputed by the GEMM), stored with per-tile column
+//                        sums for dbD; then dH = g D (epilogue scatters rows to expert order) and
+//                        dD = g^T H (a partly filled last round of tiles split over K)
 //   experts, backward    reduction-grouped TN GEMMs for dW (empty experts give exact zeros),
 //                        row-grouped NN GEMMs for dH1 (ReLU mask epilogue) and dX (epilogue
 //                        scatters rows back to sample order); bias gradients are deterministic
