@@ -335,12 +335,12 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
     // empty batch: every gradient is zero
     hipStream_t st = (hipStream_t)stream;
     const int64_t K = p->K, d = p->d_in, h = p->d_hid, o = p->d_out, V = p->vocab;
-    HMOE_TRY(hip_check(hipMemsetAsync(dW1, 0, sizeof(float) * K * h * d, st), "zero dW1"));
-    HMOE_TRY(hip_check(hipMemsetAsync(dW2, 0, sizeof(float) * K * o * h, st), "zero dW2"));
-    HMOE_TRY(hip_check(hipMemsetAsync(dD, 0, sizeof(float) * V * o, st), "zero dD"));
-    if (db1) HMOE_TRY(hip_check(hipMemsetAsync(db1, 0, sizeof(float) * K * h, st), "zero db1"));
-    if (db2) HMOE_TRY(hip_check(hipMemsetAsync(db2, 0, sizeof(float) * K * o, st), "zero db2"));
-    if (dbD) HMOE_TRY(hip_check(hipMemsetAsync(dbD, 0, sizeof(float) * V, st), "zero dbD"));
+    HMOE_TRY(launch_zero_f32(dW1, K * h * d, st));
+    HMOE_TRY(launch_zero_f32(dW2, K * o * h, st));
+    HMOE_TRY(launch_zero_f32(dD, V * o, st));
+    if (db1) HMOE_TRY(launch_zero_f32(db1, K * h, st));
+    if (db2) HMOE_TRY(launch_zero_f32(db2, K * o, st));
+    if (dbD) HMOE_TRY(launch_zero_f32(dbD, V, st));
     return HMOE_OK;
   }
   HMOE_TRY(check_ptr("X_sorted", X_sorted));

@@ -235,6 +235,14 @@ template int launch_segsum<float, float>(const float*, int64_t, const int32_t*, 
 template int launch_segsum<bf16, float>(const bf16*, int64_t, const int32_t*, const int32_t*, int, int,
                                         int64_t, float*, int, Workspace&, hipStream_t);
 
+int launch_zero_f32(float* x, int64_t n, hipStream_t st) {
+  if (n <= 0) return HMOE_OK;
+  int64_t grid = cdiv(n, 256);
+  if (grid > 4096) grid = 4096;
+  HMOE_LAUNCH("zero", k_zero_f32, dim3((unsigned)grid), dim3(256), 0, st, x, n);
+  return HMOE_OK;
+}
+
 int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, float* out_f32, Workspace& ws,
                    hipStream_t st) {
   double* part = ws.take<double>(kSumBlocks);

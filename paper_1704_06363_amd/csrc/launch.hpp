@@ -18,6 +18,7 @@ size_t segsum_ws(int64_t n, int G, int w);
 template <typename T, typename O>
 int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* seg, int G, int w,
                   int64_t n, O* out, int accumulate, Workspace& ws, hipStream_t st);
+int launch_zero_f32(float* x, int64_t n, hipStream_t st);
 int launch_sum_f32(const float* x, int64_t n, double scale, double* out_f64, float* out_f32,
                    Workspace& ws, hipStream_t st);
 

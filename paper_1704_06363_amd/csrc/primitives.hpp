@@ -200,6 +200,14 @@ static __global__ void __launch_bounds__(256) k_permute_rows(const i32x4* __rest
   }
 }
 
+// ------------------------------------------------------------------ fill
+
+// x[0 .. n) = 0 (fp32).  A kernel rather than a memset so that calls stay graph-capturable.
+static __global__ void __launch_bounds__(256) k_zero_f32(float* __restrict__ x, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) x[i] = 0.f;
+}
+
 // ------------------------------------------------------------------ fixed-order sums
 
 constexpr int kSumBlocks = 256;
