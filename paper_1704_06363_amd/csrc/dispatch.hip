@@ -204,6 +204,11 @@ int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, h
   return HMOE_OK;
 }
 
+int launch_seg_order(const int32_t* seg, int G, int32_t* order, hipStream_t st) {
+  HMOE_LAUNCH("segment order", k_seg_order, dim3((unsigned)cdiv(G, 256)), dim3(256), 0, st, seg, G, order);
+  return HMOE_OK;
+}
+
 template <typename T, typename O>
 int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* seg, int G, int w,
                   int64_t n, O* out, int accumulate, Workspace& ws, hipStream_t st) {

@@ -601,18 +601,22 @@ __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ se
 }
 
 // Reduction-grouped problem (experts' weight gradients): group e reduces over the rows
-// [seg[e], seg[e+1]) of both operands; output tile (m, n) of group e.
+// [seg[e], seg[e+1]) of both operands; output tile (m, n) of group e.  Groups are taken in the
+// order `order` gives (longest reduction first), so the deepest tiles start in the first round
+// instead of forming the tail of the launch.
 template <class C>
-__device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ seg, int G, int M, int N) {
+__device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ seg,
+                                                  const int32_t* __restrict__ order, int G, int M, int N) {
   TileCoord tc;
   const int mt = (int)cdiv(M, C::BM), nt = (int)cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
   const int per = mt * nt;
-  const int e = (int)(b / per);
-  const int in = (int)(b - (int64_t)e * per);
+  const int slot = (int)(b / per);
+  const int in = (int)(b - (int64_t)slot * per);
   const int mi = in / nt, ni = in % nt;
+  tc.valid = slot < G;
+  const int e = tc.valid ? order[slot] : 0;
   tc.group = e;
-  tc.valid = e < G;
   tc.m0 = (int64_t)mi * C::BM;
   tc.m_rows = (M - mi * C::BM) < C::BM ? (M - mi * C::BM) : C::BM;
   tc.n0 = ni * C::BN;

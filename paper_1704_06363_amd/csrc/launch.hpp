@@ -14,6 +14,7 @@ int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int
 int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, int32_t w,
                    hmoe_dtype_t dt, hipStream_t st);
 int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st);
+int launch_seg_order(const int32_t* seg, int G, int32_t* order, hipStream_t st);
 size_t segsum_ws(int64_t n, int G, int w);
 template <typename T, typename O>
 int launch_segsum(const T* X, int64_t ld, const int32_t* rowmap, const int32_t* seg, int G, int w,

@@ -509,10 +509,11 @@ __global__ void __launch_bounds__(256) k_split_reduce(const float* __restrict__ 
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_expert_wgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ B,
-                   const int32_t* __restrict__ seg, int G, int M, int N, float* __restrict__ out) {
+                   const int32_t* __restrict__ seg, const int32_t* __restrict__ order, int G, int M, int N,
+                   float* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_group_k<C>(seg, G, M, N);
+  const TileCoord tc = tile_group_k<C>(seg, order, G, M, N);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, false, false>(A + tc.k0 * M + tc.m0, M, tc.m_rows, B + tc.k0 * N + tc.n0, N, tc.n_cols, tc.k_len,
@@ -591,6 +592,7 @@ static size_t bwd_ws(const MoeShape& s) {
   using C = typename Pick<T>::C;
   Workspace ws(nullptr, 0);
   ws.take<int32_t>(s.K + 1);
+  ws.take<int32_t>(s.K);
   ws.take<T>((size_t)s.n * s.V);
   ws.take<T>((size_t)s.n * s.o);
   ws.take<T>((size_t)s.n * s.h);
@@ -643,6 +645,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
   int32_t* ts = ws.take<int32_t>(s.K + 1);
+  int32_t* order = ws.take<int32_t>(s.K);
   T* G = ws.take<T>((size_t)n * s.V);
   T* dYs = ws.take<T>((size_t)n * s.o);
   T* dZ = ws.take<T>((size_t)n * s.h);
@@ -689,18 +692,19 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   }
   // experts
   HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
+  HMOE_TRY(launch_seg_order(offsets, s.K, order, st));
   const size_t mark = ws.off;
   if (db2) HMOE_TRY(launch_segsum<T, float>(dYs, s.o, nullptr, offsets, s.K, s.o, n, db2, 0, ws, st));
   ws.off = mark;
   HMOE_LAUNCH("expert dW2", k_expert_wgrad<C>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, C::BM) * cdiv(s.h, C::BN))),
-              dim3(C::THREADS), C::LDS, st, (const T*)dYs, H1s, offsets, s.K, s.o, s.h, dW2);
+              dim3(C::THREADS), C::LDS, st, (const T*)dYs, H1s, offsets, order, s.K, s.o, s.h, dW2);
   const int64_t mt_bound = cdiv(n, C::BM) + s.K;
   HMOE_LAUNCH("expert dH1", (k_expert_dgrad<C, true>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
   if (db1) HMOE_TRY(launch_segsum<T, float>(dZ, s.h, nullptr, offsets, s.K, s.h, n, db1, 0, ws, st));
   ws.off = mark;
   HMOE_LAUNCH("expert dW1", k_expert_wgrad<C>, dim3((unsigned)((int64_t)s.K * cdiv(s.h, C::BM) * cdiv(s.d, C::BN))),
-              dim3(C::THREADS), C::LDS, st, (const T*)dZ, Xs, offsets, s.K, s.h, s.d, dW1);
+              dim3(C::THREADS), C::LDS, st, (const T*)dZ, Xs, offsets, order, s.K, s.h, s.d, dW1);
   if (dX)
     HMOE_LAUNCH("expert dX", (k_expert_dgrad<C, false>), dim3((unsigned)(mt_bound * cdiv(s.d, C::BN))),
                 dim3(C::THREADS), C::LDS, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm,

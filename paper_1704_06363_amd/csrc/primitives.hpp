@@ -64,6 +64,29 @@ static __global__ void __launch_bounds__(1024) k_seg_tiles(const int32_t* __rest
   if (threadIdx.x == 0) tile_start[G] = total;
 }
 
+// order[r] = the segment of rank r when segments are ranked by length, longest first, equal
+// lengths by lower index (a stable descending sort, so `order` is a permutation of 0..G-1).
+// Each thread ranks one segment against all G lengths, staged through LDS 256 at a time.
+static __global__ void __launch_bounds__(256) k_seg_order(const int32_t* __restrict__ seg, int G,
+                                                        int32_t* __restrict__ order) {
+  __shared__ int32_t len_s[256];
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int32_t mine = e < G ? seg[e + 1] - seg[e] : 0;
+  int rank = 0;
+  for (int f0 = 0; f0 < G; f0 += 256) {
+    const int f = f0 + threadIdx.x;
+    __syncthreads();
+    len_s[threadIdx.x] = f < G ? seg[f + 1] - seg[f] : 0;
+    __syncthreads();
+    const int m = (G - f0) < 256 ? (G - f0) : 256;
+    for (int q = 0; q < m; ++q) {
+      const int32_t c = len_s[q];
+      rank += (c > mine) || (c == mine && f0 + q < e);
+    }
+  }
+  if (e < G) order[rank] = e;
+}
+
 // Finds the segment owning global piece b: last e with tile_start[e] <= b (e < G).
 __device__ __forceinline__ int find_segment(const int32_t* __restrict__ tile_start, int G, int64_t b) {
   int lo = 0, hi = G - 1;
