@@ -444,68 +444,114 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
   }
 }
 
-template <class C, int LOADS>
+// Waits for this wave's loads of the stage that has `pending_stages` later stages in flight
+// behind it, plus X more memory operations issued after those (vmcnt counts loads and stores
+// alike, in issue order).
+template <class C, int LOADS, int X = 0>
 __device__ __forceinline__ void wait_stage(int pending_stages) {
-  static_assert(C::NS <= 5 && LOADS * (C::NS - 2) <= 63, "vmcnt range");
+  static_assert(C::NS <= 5 && LOADS * (C::NS - 2) + X <= 63, "vmcnt range");
   switch (pending_stages) {
-    case 0: wait_vmcnt<0>(); break;
-    case 1: wait_vmcnt<LOADS>(); break;
-    case 2: wait_vmcnt<2 * LOADS>(); break;
-    default: wait_vmcnt<3 * LOADS>(); break;
+    case 0: wait_vmcnt<X>(); break;
+    case 1: wait_vmcnt<LOADS + X>(); break;
+    case 2: wait_vmcnt<2 * LOADS + X>(); break;
+    default: wait_vmcnt<3 * LOADS + X>(); break;
   }
 }
+
+// The K loop of one tile, split in two so that a persistent kernel can start the next tile's
+// loads before it runs the current tile's epilogue:
+//   prime()  issues stages 0 .. NS-2 of a tile into the LDS ring (the ring must be free: after
+//            run()'s closing barrier, or at kernel start);
+//   run()    the main loop over the primed tile and a partial last stage; it ends with a barrier
+//            after which the ring is free again.  run<.., X>(.., after_prime) is for a caller
+//            that issued exactly X further memory operations (per wave) between prime() and
+//            run() when after_prime is true: the waits for the primed stages let those X stay
+//            in flight instead of draining them first.
+template <class C, bool A_KC, bool B_KC>
+struct DmaTile {
+  using OA = DmaOperand<C::BM, C::THREADS, A_KC>;
+  using OB = DmaOperand<C::BN, C::THREADS, B_KC>;
+  static constexpr int LOADS = OA::NQ + OB::NQ;
+  OA oa;
+  OB ob;
+  const bf16* A;
+  const bf16* B;
+  int64_t lda, ldb;
+  int k_len;
+
+  __device__ __forceinline__ static lds<char>* bufA(lds<char>* smem, int s) { return smem + s * C::STAGE; }
+  __device__ __forceinline__ static lds<char>* bufB(lds<char>* smem, int s) {
+    return smem + s * C::STAGE + C::A_BYTES;
+  }
+
+  __device__ __forceinline__ void prime(const bf16* __restrict__ A_, int64_t lda_, int a_rows,
+                                        const bf16* __restrict__ B_, int64_t ldb_, int b_rows, int k_len_,
+                                        lds<char>* smem) {
+    A = A_;
+    B = B_;
+    lda = lda_;
+    ldb = ldb_;
+    k_len = k_len_;
+    oa.init(lda, a_rows);
+    ob.init(ldb, b_rows);
+    const int nfull = k_len / C::BK;
+#pragma unroll
+    for (int s = 0; s < C::NS - 1; ++s)
+      if (s < nfull) {
+        oa.issue(A, lda, s * C::BK, bufA(smem, s));
+        ob.issue(B, ldb, s * C::BK, bufB(smem, s));
+      }
+  }
+
+  template <bool ROWNORM = false, int X = 0>
+  __device__ __forceinline__ void run(lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ], float* xs = nullptr,
+                                      bool after_prime = false) {
+    static_assert(!ROWNORM || A_KC, "row norms need a K-contiguous A");
+    if constexpr (ROWNORM) {
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i) xs[i] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int nfull = k_len / C::BK;
+    for (int kt = 0; kt < nfull; ++kt) {
+      const int ahead = nfull - 1 - kt;
+      const int pend = ahead < C::NS - 2 ? ahead : C::NS - 2;
+      if (X > 0 && after_prime && kt < C::NS - 1)
+        wait_stage<C, LOADS, X>(pend);  // stage kt was primed: the caller's X operations are younger
+      else
+        wait_stage<C, LOADS>(pend);
+      wg_barrier();
+      const int nx = kt + C::NS - 1;
+      if (nx < nfull) {
+        const int sb = nx % C::NS;
+        oa.issue(A, lda, nx * C::BK, bufA(smem, sb));
+        ob.issue(B, ldb, nx * C::BK, bufB(smem, sb));
+      }
+      const int sc = kt % C::NS;
+      dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(smem, sc), bufB(smem, sc), acc, xs);
+    }
+    if (nfull * C::BK < k_len) {
+      const int sb = nfull % C::NS;
+      oa.tail(A, lda, nfull * C::BK, k_len, bufA(smem, sb));
+      ob.tail(B, ldb, nfull * C::BK, k_len, bufB(smem, sb));
+      wg_barrier_lds();
+      dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(smem, sb), bufB(smem, sb), acc, xs);
+    }
+    wg_barrier_lds();
+  }
+};
 
 template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
 __device__ __forceinline__ void gemm_tile_dma(const bf16* __restrict__ A, int64_t lda, int a_rows,
                                               const bf16* __restrict__ B, int64_t ldb, int b_rows, int k_len,
                                               lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
                                               float* xs = nullptr) {
-  static_assert(!ROWNORM || A_KC, "row norms need a K-contiguous A");
-  if constexpr (ROWNORM) {
-#pragma unroll
-    for (int i = 0; i < C::MI; ++i) xs[i] = 0.f;
-  }
-  using OA = DmaOperand<C::BM, C::THREADS, A_KC>;
-  using OB = DmaOperand<C::BN, C::THREADS, B_KC>;
-  constexpr int LOADS = OA::NQ + OB::NQ;
-#pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  OA oa;
-  OB ob;
-  oa.init(lda, a_rows);
-  ob.init(ldb, b_rows);
-  const int nfull = k_len / C::BK;
-  auto bufA = [&](int s) { return smem + s * C::STAGE; };
-  auto bufB = [&](int s) { return smem + s * C::STAGE + C::A_BYTES; };
-#pragma unroll
-  for (int s = 0; s < C::NS - 1; ++s)
-    if (s < nfull) {
-      oa.issue(A, lda, s * C::BK, bufA(s));
-      ob.issue(B, ldb, s * C::BK, bufB(s));
-    }
-  for (int kt = 0; kt < nfull; ++kt) {
-    const int ahead = nfull - 1 - kt;
-    wait_stage<C, LOADS>(ahead < C::NS - 2 ? ahead : C::NS - 2);
-    wg_barrier();
-    const int nx = kt + C::NS - 1;
-    if (nx < nfull) {
-      const int sb = nx % C::NS;
-      oa.issue(A, lda, nx * C::BK, bufA(sb));
-      ob.issue(B, ldb, nx * C::BK, bufB(sb));
-    }
-    const int sc = kt % C::NS;
-    dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(sc), bufB(sc), acc, xs);
-  }
-  if (nfull * C::BK < k_len) {
-    const int sb = nfull % C::NS;
-    oa.tail(A, lda, nfull * C::BK, k_len, bufA(sb));
-    ob.tail(B, ldb, nfull * C::BK, k_len, bufB(sb));
-    wg_barrier_lds();
-    dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(sb), bufB(sb), acc, xs);
-  }
-  wg_barrier_lds();
+  DmaTile<C, A_KC, B_KC> t;
+  t.prime(A, lda, a_rows, B, ldb, b_rows, k_len, smem);
+  t.template run<ROWNORM>(smem, acc, xs);
 }
 
 // Full K loop for one tile on whichever engine the configuration names.

@@ -86,30 +86,16 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // ------------------------------------------------------------------ decoder forward
 
-// Per row and V-tile: m = max of the tile's logits, s = sum exp(logit - m); the logits
-// themselves are stored to L when L is given (saved for the backward).
+// Softmax statistics of one logits tile (logit = accumulator + bias): per row, m = max over the
+// tile's valid columns and s = sum exp(logit - m), merged over the WAVES_N waves that share the
+// row through rm / rs (LDS, [WAVES_N][BM] floats each) and written as the tile's partials
+// pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
 template <class C>
-__global__ void __launch_bounds__(C::THREADS)
-    k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
-              const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
-              float* __restrict__ ps, typename C::type* __restrict__ L) {
-  using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
-  lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_plain<C>(n, V, o);
-  if (!tc.valid) return;
-  floatx4 acc[C::MI][C::NJ];
-  gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                               const float (&bias)[Frag<C>::NCOL], lds<float>* rm, lds<float>* rs,
+                                               int64_t n, float* __restrict__ pm, float* __restrict__ ps) {
   using F = Frag<C>;
   const F f;
-  float bias[F::NCOL];
-#pragma unroll
-  for (int q = 0; q < F::NCOL; ++q) {
-    const int col = f.colq(q);
-    bias[q] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
-  }
-  lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // [WAVES_N][BM]
-  lds<float>* rs = rm + C::WAVES_N * C::BM;              // [WAVES_N][BM]
   if constexpr (F::T) {
     // one row per i; its WN columns of this wave sit in lanes lr, lr + 16, lr + 32, lr + 48
 #pragma unroll
@@ -159,7 +145,7 @@ __global__ void __launch_bounds__(C::THREADS)
         }
       }
   }
-  __syncthreads();
+  wg_barrier_lds();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     float M = rm[t];
 #pragma unroll
@@ -171,10 +157,117 @@ __global__ void __launch_bounds__(C::THREADS)
     pm[at] = M;
     ps[at] = S;
   }
+}
+
+template <class C>
+__device__ __forceinline__ void dec_tile_bias(const TileCoord& tc, const typename C::type* __restrict__ bD,
+                                              float (&bias)[Frag<C>::NCOL]) {
+  using F = Frag<C>;
+  const F f;
+#pragma unroll
+  for (int q = 0; q < F::NCOL; ++q) {
+    const int col = f.colq(q);
+    bias[q] = (bD && col < tc.n_cols) ? to_f32(bD[tc.n0 + col]) : 0.f;
+  }
+}
+
+// Per row and V-tile: the softmax partials (dec_tile_stats); the logits themselves are stored
+// to L when L is given (saved for the backward).  One tile per workgroup (register-staged
+// engine).
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
+              const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
+              float* __restrict__ ps, typename C::type* __restrict__ L) {
+  using T = typename C::type;
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  const TileCoord tc = tile_plain<C>(n, V, o);
+  if (!tc.valid) return;
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, true>(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem, acc);
+  using F = Frag<C>;
+  float bias[F::NCOL];
+  dec_tile_bias<C>(tc, bD, bias);
+  lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
+  dec_tile_stats<C>(tc, acc, bias, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
     store_out<C, T>(tc, acc, smem, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
                     RowId{tc.m0}, NoVec{});
+  }
+}
+
+// The same computation as a persistent kernel on the direct-to-LDS engine: gridDim.x workgroups
+// walk the tiles blockIdx.x, blockIdx.x + gridDim.x, ...  After a tile's K loop the workgroup
+// forms the tile's softmax statistics, issues the first stages of its next tile and only then
+// stores the logits, so the store drain overlaps the next tile's first stages: for a full tile
+// every wave issues exactly MI x NJ stores there, and the waits for the primed stages let
+// those stay in flight (ragged tiles wait for everything).  rm / rs sit past the operand ring
+// (dynamic LDS = C::LDS + kDecStatLds).
+constexpr int kDecStatLds = 2 * 4 * 256 * (int)sizeof(float);
+template <class C>
+__device__ __forceinline__ void dec_bias_packed(const TileCoord& tc, const bf16* __restrict__ bD,
+                                                uint2 (&bp)[C::NJ]) {
+  const Frag<C> f;
+#pragma unroll
+  for (int j = 0; j < C::NJ; ++j) {
+    const int col = f.col(j, 0);  // four consecutive columns; n_cols is a multiple of 8
+    bp[j] = (bD && col < tc.n_cols) ? *reinterpret_cast<const uint2*>(bD + tc.n0 + col) : uint2{0u, 0u};
+  }
+}
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_fwd_stream(const bf16* __restrict__ H, const bf16* __restrict__ D, const bf16* __restrict__ bD, int64_t n,
+                     int V, int o, float* __restrict__ pm, float* __restrict__ ps, bf16* __restrict__ L) {
+  static_assert(C::DMA && C::TRANS, "persistent decoder forward runs the direct-to-LDS engine");
+  static_assert(2 * C::WAVES_N * C::BM * (int)sizeof(float) <= kDecStatLds, "statistics scratch");
+  constexpr int STORES = C::MI * C::NJ;  // store_direct's stores per wave for a full tile
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  lds<float>* rm = reinterpret_cast<lds<float>*>(smem + C::LDS);
+  lds<float>* rs = rm + C::WAVES_N * C::BM;
+  using F = Frag<C>;
+  const int64_t tiles = cdiv(n, C::BM) * cdiv(V, C::BN);
+  int64_t t = blockIdx.x;
+  if (t >= tiles) return;
+  TileCoord tc = tile_plain_at<C>(n, V, o, t);
+  DmaTile<C, true, true> pipe;
+  pipe.prime(H + tc.m0 * o, o, tc.m_rows, D + (int64_t)tc.n0 * o, o, tc.n_cols, o, smem);
+  uint2 bp[C::NJ];
+  dec_bias_packed<C>(tc, bD, bp);
+  bool stores_pending = false;
+  for (;;) {
+    floatx4 acc[C::MI][C::NJ];
+    pipe.template run<false, STORES>(smem, acc, nullptr, stores_pending);
+    float bias[F::NCOL];
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j) {
+      bias[4 * j + 0] = __uint_as_float(bp[j].x << 16);
+      bias[4 * j + 1] = __uint_as_float(bp[j].x & 0xffff0000u);
+      bias[4 * j + 2] = __uint_as_float(bp[j].y << 16);
+      bias[4 * j + 3] = __uint_as_float(bp[j].y & 0xffff0000u);
+    }
+    dec_tile_stats<C>(tc, acc, bias, rm, rs, n, pm, ps);
+    const int64_t tn = t + gridDim.x;
+    const bool more = tn < tiles;
+    TileCoord nc = tc;
+    if (more) {
+      nc = tile_plain_at<C>(n, V, o, tn);
+      dec_bias_packed<C>(nc, bD, bp);
+      pipe.prime(H + nc.m0 * o, o, nc.m_rows, D + (int64_t)nc.n0 * o, o, nc.n_cols, o, smem);
+    }
+    // nothing may move between the primed loads and the stores: the next waits count them
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    if (L)
+      store_direct<C, bf16>(tc, acc, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
+                            RowId{tc.m0}, NoVec{});
+    __builtin_amdgcn_sched_barrier(0);
+    if (!more) break;
+    stores_pending = L != nullptr && tc.m_rows == C::BM && tc.n_cols == C::BN;
+    t = tn;
+    tc = nc;
   }
 }
 
@@ -630,8 +723,18 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
               dim3(C::THREADS), C::LDS, st, Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
   HMOE_LAUNCH("expert layer 2", (k_expert_fwd<C, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
-  HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS, st,
-              (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
+  if constexpr (C::DMA) {
+    // persistent: one workgroup per resident slot
+    const int64_t tiles = cdiv(n, C::BM) * ntv;
+    constexpr int lds_bytes = C::LDS + kDecStatLds;
+    int64_t slots = (int64_t)device_cus() * ((160 * 1024) / lds_bytes);
+    if (slots > tiles) slots = tiles;
+    HMOE_LAUNCH("decoder forward", k_dec_fwd_stream<C>, dim3((unsigned)slots), dim3(C::THREADS), lds_bytes, st,
+                (const bf16*)H, (const bf16*)D, (const bf16*)p->bD, n, s.V, s.o, pm, ps, (bf16*)Lg);
+  } else {
+    HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS,
+                st, (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
+  }
   HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
               (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);

@@ -1,6 +1,7 @@
 """Edge cases of the HIP path against the fp64 oracle: rows with more tags than the gradient
-kernels stage in LDS, the narrowest widths the ABI allows, a single sample, the largest K, and
-exactly duplicated centres (ties must go to the lower index)."""
+kernels stage in LDS, the narrowest widths the ABI allows, a single sample, a decoder with more
+tiles than the chip holds workgroups at once, the largest K, and exactly duplicated centres
+(ties must go to the lower index)."""
 import numpy as np
 import pytest
 import torch
@@ -85,6 +86,18 @@ def test_single_sample():
     rp, tg = W.zipf_labels(1, 96, 5, seed=61)
     p = W.moe_params(4, 64, 64, 32, 96, seed=62, dtype="bf16", device="cuda")
     _step_vs_oracle(X, np.array([2], np.int32), 4, p, rp, tg, "bf16", saved=True)
+
+
+@pytest.mark.parametrize("saved", [False, True])
+def test_decoder_tiles_outnumber_workgroups(saved):
+    # 17 x 32 = 544 decoder tiles of 256 x 256 (ragged in rows, columns and K = 136 = 4 x 32 + 8):
+    # the persistent decoder forward walks two or three tiles per workgroup
+    n, d, h, o, V, K = 4200, 64, 128, 136, 8000, 4
+    X = W.rectified_gaussian(n, d, seed=90, dtype="bf16", device="cuda")
+    ids = np.random.default_rng(91).integers(0, K, n).astype(np.int32)
+    rp, tg = W.zipf_labels(n, V, 8, seed=92)
+    p = W.moe_params(K, d, h, o, V, seed=93, dtype="bf16", device="cuda", bias=True)
+    _step_vs_oracle(X, ids, K, p, rp, tg, "bf16", saved)
 
 
 def test_largest_K_assign_and_dispatch():
