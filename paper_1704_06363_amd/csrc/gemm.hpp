@@ -755,29 +755,72 @@ __device__ __forceinline__ void store_tile(const TileCoord& tc, const floatx4 (&
   }
 }
 
-// Epilogue store straight from registers (TRANS orientation): every lane writes its four
-// consecutive columns of a row as one 8-byte (bf16) or 16-byte (fp32) store; no LDS, no
-// barrier, and the stores drain while the next tile starts.  Same functors as store_tile, with
-// vec applied to the 4-element vector.
+// Epilogue store straight from registers (TRANS orientation): no LDS, no barrier.  Same
+// functors as store_tile, with vec applied to the stored vector.
+//   2-byte outputs: lanes lg and lg ^ 1 (16 apart, same row) trade halves of their column
+//   blocks 2p and 2p + 1 with one v_permlane16_swap per dword, after which every lane holds
+//   8 consecutive columns (at 32 p + 16 (lg & 1) + 8 (lg >> 1) of the wave's columns) and
+//   stores them as one 16-byte vector: each store instruction covers 64 contiguous bytes of 16
+//   rows.
+//   4-byte outputs: every lane stores its four consecutive columns as one 16-byte vector.
+// direct_stores<C, O>() is the number of store instructions a wave issues for a full tile.
+template <class C, typename O>
+__device__ __forceinline__ constexpr bool direct_pairs() {
+  return sizeof(O) == 2 && C::NJ % 2 == 0;
+}
+template <class C, typename O>
+__device__ __forceinline__ constexpr int direct_stores() {
+  return direct_pairs<C, O>() ? C::MI * C::NJ / 2 : C::MI * C::NJ;
+}
 template <class C, typename O, class Elem, class RowMap, class Vec>
 __device__ __forceinline__ void store_direct(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
                                              O* __restrict__ out, int64_t ldo, Elem elem, RowMap rowmap, Vec vec) {
   static_assert(C::TRANS, "direct stores need the transposed accumulator layout");
   const Frag<C> f;
+  if constexpr (direct_pairs<C, O>()) {
+    typedef unsigned int u2v __attribute__((ext_vector_type(2)));
+    typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+    typedef O v8 __attribute__((ext_vector_type(8)));
+    const int cpos = 16 * (f.lg & 1) + 8 * (f.lg >> 1);
 #pragma unroll
-  for (int i = 0; i < C::MI; ++i) {
-    const int row = f.row(i, 0);
-    if (row >= tc.m_rows) continue;
-    const int64_t dr = rowmap(row);
-    O* orow = out + dr * ldo + tc.n0;
+    for (int i = 0; i < C::MI; ++i) {
+      const int row = f.row(i, 0);
+      const bool row_ok = row < tc.m_rows;  // the same for the two lanes of a swap
+      const int64_t dr = row_ok ? rowmap(row) : 0;
 #pragma unroll
-    for (int j = 0; j < C::NJ; ++j) {
-      const int col = f.col(j, 0);
-      if (col >= tc.n_cols) continue;
-      vec4<O> v;
+      for (int p = 0; p < C::NJ / 2; ++p) {
+        vec4<O> va, vb;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = from_f32<O>(elem(i, j, r, acc[i][j][r]));
-      *reinterpret_cast<vec4<O>*>(orow + col) = vec(dr, row, col, v);
+        for (int r = 0; r < 4; ++r) {
+          va[r] = from_f32<O>(elem(i, 2 * p, r, acc[i][2 * p][r]));
+          vb[r] = from_f32<O>(elem(i, 2 * p + 1, r, acc[i][2 * p + 1][r]));
+        }
+        const u2v a = __builtin_bit_cast(u2v, va), b = __builtin_bit_cast(u2v, vb);
+        // odd 16-lane rows of the first operand trade with even rows of the second
+        const u2v s0 = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+        const u2v s1 = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+        const u4v w = u4v{s0[0], s1[0], s0[1], s1[1]};
+        const int col = f.wn * C::WN + 32 * p + cpos;
+        if (row_ok && col < tc.n_cols)
+          *reinterpret_cast<v8*>(out + dr * ldo + tc.n0 + col) = vec(dr, row, col, __builtin_bit_cast(v8, w));
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i) {
+      const int row = f.row(i, 0);
+      if (row >= tc.m_rows) continue;
+      const int64_t dr = rowmap(row);
+      O* orow = out + dr * ldo + tc.n0;
+#pragma unroll
+      for (int j = 0; j < C::NJ; ++j) {
+        const int col = f.col(j, 0);
+        if (col >= tc.n_cols) continue;
+        vec4<O> v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = from_f32<O>(elem(i, j, r, acc[i][j][r]));
+        *reinterpret_cast<vec4<O>*>(orow + col) = vec(dr, row, col, v);
+      }
     }
   }
 }

@@ -202,8 +202,8 @@ __global__ void __launch_bounds__(C::THREADS)
 // walk the tiles blockIdx.x, blockIdx.x + gridDim.x, ...  After a tile's K loop the workgroup
 // forms the tile's softmax statistics, issues the first stages of its next tile and only then
 // stores the logits, so the store drain overlaps the next tile's first stages: for a full tile
-// every wave issues exactly MI x NJ stores there, and the waits for the primed stages let
-// those stay in flight (ragged tiles wait for everything).  rm / rs sit past the operand ring
+// every wave issues exactly direct_stores() stores there, and the waits for the primed stages
+// let those stay in flight (ragged tiles wait for everything).  rm / rs sit past the operand ring
 // (dynamic LDS = C::LDS + kDecStatLds).
 constexpr int kDecStatLds = 2 * 4 * 256 * (int)sizeof(float);
 template <class C>
@@ -222,7 +222,7 @@ __global__ void __launch_bounds__(C::THREADS)
                      int V, int o, float* __restrict__ pm, float* __restrict__ ps, bf16* __restrict__ L) {
   static_assert(C::DMA && C::TRANS, "persistent decoder forward runs the direct-to-LDS engine");
   static_assert(2 * C::WAVES_N * C::BM * (int)sizeof(float) <= kDecStatLds, "statistics scratch");
-  constexpr int STORES = C::MI * C::NJ;  // store_direct's stores per wave for a full tile
+  constexpr int STORES = direct_stores<C, bf16>();  // per wave, for a full tile
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem + C::LDS);

@@ -33,6 +33,8 @@ def _step_vs_oracle(X, ids, K, p, rp, tg, store, saved):
     assert_close(f["lse"], ref["lse"], rt, "lse")
     assert_close(f["loss"], ref["loss"], rt, "loss")
     assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
+    if saved:
+        assert_close(f["logits"], ref["logits"], rt, "logits")
     tdt = torch.bfloat16 if store == "bf16" else torch.float32
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(tdt).cuda()
     H = torch.tensor(ref["H"], dtype=torch.float32).to(tdt).cuda()
