@@ -203,7 +203,8 @@ __global__ void __launch_bounds__(C::THREADS)
 // forms the tile's softmax statistics, issues the first stages of its next tile and only then
 // stores the logits, so the store drain overlaps the next tile's first stages: for a full tile
 // every wave issues exactly direct_stores() stores there, and the waits for the primed stages
-// let those stay in flight (ragged tiles wait for everything).  rm / rs sit past the operand ring
+// let those stay in flight (ragged tiles wait for everything).  The logits are stored
+// non-temporally (read only by the backward), which leaves the L2 to the operand tiles.  rm / rs sit past the operand ring
 // (dynamic LDS = C::LDS + kDecStatLds).
 constexpr int kDecStatLds = 2 * 4 * 256 * (int)sizeof(float);
 template <class C>
@@ -261,7 +262,7 @@ __global__ void __launch_bounds__(C::THREADS)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
     if (L)
-      store_direct<C, bf16>(tc, acc, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
+      store_direct<C, bf16, true>(tc, acc, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
                             RowId{tc.m0}, NoVec{});
     __builtin_amdgcn_sched_barrier(0);
     if (!more) break;
@@ -448,6 +449,11 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // Saved-logits path: g = (exp(L - lse) - y) / n elementwise over [n x V]; each thread owns one
 // 16-byte column vector over kGradRows rows and writes its column sums to part_db[rowblock][V].
+// A block covers a slab of 256 x EPV columns; per row it keeps (in LDS) only the tags that fall
+// inside its slab, so the per-element work is an fma and an exp, and a tag costs one compare
+// per row in the few rows that have one here.  A row with more than MAXT tags in the slab
+// (flag -1) reads its tags from global memory instead.  g is stored non-temporally: it is only
+// read back by the next kernels, long after it has left the caches (measured 3.07 -> 2.91 ms).
 constexpr int kGradRows = 256;
 
 template <typename T>
@@ -457,20 +463,31 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
                                                        float inv_n, T* __restrict__ G, float* __restrict__ part_db) {
   constexpr int EPV = 16 / sizeof(T);
   constexpr int MAXT = 16;
-  __shared__ float s_lse[kGradRows];
-  __shared__ int32_t s_p0[kGradRows], s_cnt[kGradRows], s_tag[kGradRows * MAXT];
+  constexpr float kLog2e = 1.4426950408889634f;
+  __shared__ float s_lse2[kGradRows], s_yn[kGradRows];
+  __shared__ int32_t s_cnt[kGradRows];
+  __shared__ int16_t s_tag[kGradRows * MAXT];  // column within the slab
   const int64_t r0 = (int64_t)blockIdx.x * kGradRows;
   const int rows = (int)((n - r0) < kGradRows ? (n - r0) : kGradRows);
+  const int slab0 = blockIdx.y * 256 * EPV;
   for (int t = threadIdx.x; t < rows; t += 256) {
     const int32_t p0 = row_ptr[r0 + t], cnt = row_ptr[r0 + t + 1] - p0;
-    s_lse[t] = lse[r0 + t];
-    s_p0[t] = p0;
-    s_cnt[t] = cnt;
-    for (int q = 0; q < cnt && q < MAXT; ++q) s_tag[t * MAXT + q] = tag[p0 + q];
+    s_lse2[t] = lse[r0 + t] * kLog2e;
+    s_yn[t] = inv_n / (float)cnt;
+    int k = 0;
+    for (int q = 0; q < cnt; ++q) {
+      const int d = tag[p0 + q] - slab0;
+      if ((unsigned)d < (unsigned)(256 * EPV)) {
+        if (k < MAXT) s_tag[t * MAXT + k] = (int16_t)d;
+        ++k;
+      }
+    }
+    s_cnt[t] = k <= MAXT ? k : -1;
   }
   __syncthreads();
-  const int c0 = (blockIdx.y * 256 + threadIdx.x) * EPV;
+  const int c0 = slab0 + threadIdx.x * EPV;
   if (c0 >= V) return;
+  const int cl = threadIdx.x * EPV;  // this thread's first column within the slab
   float cs[EPV];
 #pragma unroll
   for (int e = 0; e < EPV; ++e) cs[e] = 0.f;
@@ -486,29 +503,42 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
       const int t = t0 + u;
       if (t >= rows) break;
       const T* lv = reinterpret_cast<const T*>(&raw[u]);
-      const float Lr = s_lse[t];
+      const float l2 = s_lse2[t];
       float g[EPV];
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) g[e] = __expf(to_f32(lv[e]) - Lr);
-      const int32_t cnt = s_cnt[t];
-      const float y = 1.f / (float)cnt;
-      for (int32_t q = 0; q < cnt; ++q) {
-        const int d = (q < MAXT ? s_tag[t * MAXT + q] : tag[s_p0[t] + q]) - c0;
-        if ((unsigned)d < (unsigned)EPV) {
+      for (int e = 0; e < EPV; ++e) g[e] = __builtin_amdgcn_exp2f(fmaf(to_f32(lv[e]), kLog2e, -l2)) * inv_n;
+      const int32_t k = s_cnt[t];
+      if (k != 0) {
+        const float yn = s_yn[t];
+        if (k > 0) {
+          for (int32_t q = 0; q < k; ++q) {
+            const int d = s_tag[t * MAXT + q] - cl;
+            if ((unsigned)d < (unsigned)EPV) {
 #pragma unroll
-          for (int e = 0; e < EPV; ++e)
-            if (d == e) g[e] -= y;
+              for (int e = 0; e < EPV; ++e)
+                if (d == e) g[e] -= yn;
+            }
+          }
+        } else {
+          const int32_t p0 = row_ptr[r0 + t], cnt = row_ptr[r0 + t + 1] - p0;
+          for (int32_t q = 0; q < cnt; ++q) {
+            const int d = tag[p0 + q] - c0;
+            if ((unsigned)d < (unsigned)EPV) {
+#pragma unroll
+              for (int e = 0; e < EPV; ++e)
+                if (d == e) g[e] -= yn;
+            }
+          }
         }
       }
       i32x4 outv;
       T* ov = reinterpret_cast<T*>(&outv);
 #pragma unroll
       for (int e = 0; e < EPV; ++e) {
-        g[e] *= inv_n;
         cs[e] += g[e];
         ov[e] = from_f32<T>(g[e]);
       }
-      *reinterpret_cast<i32x4*>(G + (r0 + t) * V + c0) = outv;
+      __builtin_nontemporal_store(outv, reinterpret_cast<i32x4*>(G + (r0 + t) * V + c0));
     }
   }
   float* dst = part_db + (int64_t)blockIdx.x * V + c0;
