@@ -305,6 +305,10 @@ struct CfgD {
   static_assert(sizeof(T) == 2, "direct-to-LDS engine is bf16 only");
 };
 
+#ifndef HMOE_PINGPONG
+#define HMOE_PINGPONG 1
+#endif
+
 #ifndef HMOE_DMA_STAGES
 #define HMOE_DMA_STAGES 4
 #endif
@@ -406,32 +410,35 @@ __device__ __forceinline__ bf16x8 dma_frag(const lds<char>* buf, int r0, int lr,
   }
 }
 
-// ROWNORM: xs[i] += squares of this lane's 8 elements of A fragment i, for the fragments
-// i = wn (mod WAVES_N) that this wave is responsible for (the work is spread over the waves
-// that share the rows; each row's sum stays within one wave).
-template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
-__device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<char>* bB,
-                                               floatx4 (&acc)[C::MI][C::NJ], float* xs = nullptr) {
+// A stage's MFMA operands for this wave: fragments of its WM rows of A and WN rows of B.
+template <class C, bool A_KC, bool B_KC>
+__device__ __forceinline__ void dma_read_frags(const lds<char>* bA, const lds<char>* bB, bf16x8 (&a)[C::MI],
+                                               bf16x8 (&b)[C::NJ]) {
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wm = w / C::WAVES_N, wn = w % C::WAVES_N;
   const int lr = l & 15, lg = l >> 4;
-  bf16x8 a[C::MI], b[C::NJ];
 #pragma unroll
   for (int i = 0; i < C::MI; ++i) a[i] = dma_frag<A_KC, C::BM>(bA, wm * C::WM + 16 * i, lr, lg);
 #pragma unroll
   for (int j = 0; j < C::NJ; ++j) b[j] = dma_frag<B_KC, C::BN>(bB, wn * C::WN + 16 * j, lr, lg);
-  // all of the stage's fragment reads go out before its MFMAs (measured faster than letting
-  // the scheduler interleave them)
-  __builtin_amdgcn_sched_barrier(0);
-  // B as the MFMA's first operand: the 16 x 16 result is the transposed sub-tile, so each lane
-  // ends up with four consecutive output columns of one row (see TRANS).
+}
+
+// The stage's MFMAs.  B is the MFMA's first operand: the 16 x 16 result is the transposed
+// sub-tile, so each lane ends up with four consecutive output columns of one row (see TRANS).
+// ROWNORM: xs[i] += squares of this lane's 8 elements of A fragment i, for the fragments
+// i = wn (mod WAVES_N) that this wave is responsible for (the work is spread over the waves
+// that share the rows; each row's sum stays within one wave).
+template <class C, bool ROWNORM>
+__device__ __forceinline__ void dma_mfmas(const bf16x8 (&a)[C::MI], const bf16x8 (&b)[C::NJ],
+                                          floatx4 (&acc)[C::MI][C::NJ], float* xs) {
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j)
       acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
   if constexpr (ROWNORM) {
+    const int wn = (threadIdx.x >> 6) % C::WAVES_N;
 #pragma unroll
     for (int i = 0; i < C::MI; ++i)
       if ((i % C::WAVES_N) == wn) {
@@ -442,6 +449,17 @@ __device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<ch
         }
       }
   }
+}
+
+template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
+__device__ __forceinline__ void dma_mfma_stage(const lds<char>* bA, const lds<char>* bB,
+                                               floatx4 (&acc)[C::MI][C::NJ], float* xs = nullptr) {
+  bf16x8 a[C::MI], b[C::NJ];
+  dma_read_frags<C, A_KC, B_KC>(bA, bB, a, b);
+  // all of the stage's fragment reads go out before its MFMAs (measured faster than letting
+  // the scheduler interleave them)
+  __builtin_amdgcn_sched_barrier(0);
+  dma_mfmas<C, ROWNORM>(a, b, acc, xs);
 }
 
 // Waits for this wave's loads of the stage that has `pending_stages` later stages in flight
@@ -516,22 +534,67 @@ struct DmaTile {
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
     const int nfull = k_len / C::BK;
-    for (int kt = 0; kt < nfull; ++kt) {
-      const int ahead = nfull - 1 - kt;
+    // Ping-pong schedule for contractions with at least one K-contiguous operand.  With both
+    // operands K-strided (two ds_read_b64_tr_b16 per fragment) the read phase outlasts the
+    // MFMA phase and the single-group schedule below measured faster (dD, weight gradients).
+    constexpr bool PP = HMOE_PINGPONG && (A_KC || B_KC);
+    auto wait_own = [&](int k) {  // this wave's loads of stage k
+      const int ahead = nfull - 1 - k;
       const int pend = ahead < C::NS - 2 ? ahead : C::NS - 2;
-      if (X > 0 && after_prime && kt < C::NS - 1)
-        wait_stage<C, LOADS, X>(pend);  // stage kt was primed: the caller's X operations are younger
+      if (X > 0 && after_prime && k < C::NS - 1)
+        wait_stage<C, LOADS, X>(pend);  // stage k was primed: the caller's X operations are younger
       else
         wait_stage<C, LOADS>(pend);
-      wg_barrier();
-      const int nx = kt + C::NS - 1;
-      if (nx < nfull) {
-        const int sb = nx % C::NS;
-        oa.issue(A, lda, nx * C::BK, bufA(smem, sb));
-        ob.issue(B, ldb, nx * C::BK, bufB(smem, sb));
+    };
+    if constexpr (PP) {
+      // Two wave groups (waves 0 .. WAVES/2-1 and the rest; each SIMD holds one wave of each)
+      // run the same stage sequence  [barrier] read fragments + issue loads [barrier] MFMAs
+      // with group 1 one phase behind group 0, so that while one group reads, the other feeds
+      // the SIMD's matrix unit.  The offset comes from one extra barrier, taken by group 1
+      // before the loop and by group 0 after it (the group index is wave-uniform, so those are
+      // scalar branches and both groups execute the same number of barriers).  Stage kt is
+      // read first by group 0, after barrier 2 kt + 1, which for group 1 is the second barrier
+      // of its stage kt - 1 (or the extra one): each wave waits for its own loads of stage kt
+      // before that barrier; the count of its younger loads is the same in both places.  The
+      // slot of stage kt - 1 gets new loads only after barrier 2 kt + 1, when both groups'
+      // reads of it have completed (lgkmcnt(0) before every second barrier).
+      static_assert(C::WAVES % 2 == 0, "two wave groups");
+      const bool g1 = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) >= C::WAVES / 2;
+      if (nfull > 0 && g1) {
+        wait_own(0);
+        wg_barrier();
       }
-      const int sc = kt % C::NS;
-      dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(smem, sc), bufB(smem, sc), acc, xs);
+      for (int kt = 0; kt < nfull; ++kt) {
+        if (!g1) wait_own(kt);
+        wg_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 fa[C::MI], fb[C::NJ];
+        const int sc = kt % C::NS;
+        dma_read_frags<C, A_KC, B_KC>(bufA(smem, sc), bufB(smem, sc), fa, fb);
+        const int nx = kt + C::NS - 1;
+        if (nx < nfull) {
+          oa.issue(A, lda, nx * C::BK, bufA(smem, nx % C::NS));
+          ob.issue(B, ldb, nx * C::BK, bufB(smem, nx % C::NS));
+        }
+        if (g1 && kt + 1 < nfull) wait_own(kt + 1);
+        wg_barrier_lds();
+        __builtin_amdgcn_sched_barrier(0);
+        dma_mfmas<C, ROWNORM>(fa, fb, acc, xs);
+      }
+      if (nfull > 0 && !g1) wg_barrier();
+    } else {
+      for (int kt = 0; kt < nfull; ++kt) {
+        wait_own(kt);
+        wg_barrier();
+        const int nx = kt + C::NS - 1;
+        if (nx < nfull) {
+          const int sb = nx % C::NS;
+          oa.issue(A, lda, nx * C::BK, bufA(smem, sb));
+          ob.issue(B, ldb, nx * C::BK, bufB(smem, sb));
+        }
+        const int sc = kt % C::NS;
+        dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(smem, sc), bufB(smem, sc), acc, xs);
+      }
     }
     if (nfull * C::BK < k_len) {
       const int sb = nfull % C::NS;
