@@ -826,8 +826,7 @@ __device__ __forceinline__ void store_tile(const TileCoord& tc, const floatx4 (&
 //   stores them as one 16-byte vector: each store instruction covers 64 contiguous bytes of 16
 //   rows.
 //   4-byte outputs: every lane stores its four consecutive columns as one 16-byte vector.
-// direct_stores<C, O>() is the number of store instructions a wave issues for a full tile.  NT
-// marks the 2-byte stores non-temporal (outputs that are not read again soon).
+// direct_stores<C, O>() is the number of store instructions a wave issues for a full tile.
 template <class C, typename O>
 __device__ __forceinline__ constexpr bool direct_pairs() {
   return sizeof(O) == 2 && C::NJ % 2 == 0;
@@ -836,7 +835,7 @@ template <class C, typename O>
 __device__ __forceinline__ constexpr int direct_stores() {
   return direct_pairs<C, O>() ? C::MI * C::NJ / 2 : C::MI * C::NJ;
 }
-template <class C, typename O, bool NT = false, class Elem, class RowMap, class Vec>
+template <class C, typename O, class Elem, class RowMap, class Vec>
 __device__ __forceinline__ void store_direct(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
                                              O* __restrict__ out, int64_t ldo, Elem elem, RowMap rowmap, Vec vec) {
   static_assert(C::TRANS, "direct stores need the transposed accumulator layout");
@@ -865,14 +864,8 @@ __device__ __forceinline__ void store_direct(const TileCoord& tc, const floatx4 
         const u2v s1 = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
         const u4v w = u4v{s0[0], s1[0], s0[1], s1[1]};
         const int col = f.wn * C::WN + 32 * p + cpos;
-        if (row_ok && col < tc.n_cols) {
-          v8* dst = reinterpret_cast<v8*>(out + dr * ldo + tc.n0 + col);
-          const v8 val = vec(dr, row, col, __builtin_bit_cast(v8, w));
-          if constexpr (NT)
-            __builtin_nontemporal_store(val, dst);
-          else
-            *dst = val;
-        }
+        if (row_ok && col < tc.n_cols)
+          *reinterpret_cast<v8*>(out + dr * ldo + tc.n0 + col) = vec(dr, row, col, __builtin_bit_cast(v8, w));
       }
     }
   } else {
