@@ -299,24 +299,27 @@ int hmoe_orc_dispatch(int64_t n, int32_t K, const int32_t* e, int32_t* counts,
 
 /* ------------------------------------------------- O8 + O9: experts, decoder, loss */
 
-/* Forward pass of the shared-decoder hard mixture (Section 2, shared-decoder figure) with
- * the multilabel softmax loss of Section 4.1, Eq. 3.  For every sample i routed to expert
- * e = a[i]:
+/* Forward pass of the hard mixture (Section 2) with the multilabel softmax loss of Section
+ * 4.1, Eq. 3.  ndec = 1: one decoder shared by the experts (D [V][o], bD [V]; the
+ * shared-decoder figure); ndec = K: every expert has its own (D [K][V][o], bD [K][V]; the
+ * independent-decoder figure), and sample i is decoded by its expert's.  For every sample i
+ * routed to expert e = a[i], with D_i, bD_i the decoder it uses:
  *   h1 = relu(W1_e x + b1_e)            (stored, rounded by `store`)
  *   y  = W2_e h1 + b2_e                 (stored as H[i], rounded by `store`)
- *   l  = D H[i] + bD                    (all V logits)
+ *   l  = D_i H[i] + bD_i                (all V logits)
  *   lse = log sum_j exp(l_j);  loss_i = lse - (1/|P_i|) sum_{j in P_i} l_j
  * The target mass is spread uniformly over the positive tags P_i (tags listed in
  * tag[row_ptr[i] .. row_ptr[i+1]), distinct); the batch loss is the mean over samples.
  * b1, b2, bD may be NULL (no bias).  probs (n x V) is optional; logits (n x V), optional, receives
  * the logits rounded by `store` (the tensor a device saves for the backward). */
 int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
-                         const double* X, const int32_t* a, const double* W1, const double* b1,
-                         const double* W2, const double* b2, const double* D,
+                         int32_t ndec, const double* X, const int32_t* a, const double* W1,
+                         const double* b1, const double* W2, const double* b2, const double* D,
                          const double* bD, const int32_t* row_ptr, const int32_t* tag,
                          int store, double* H1, double* H, double* lse, double* loss,
                          double* loss_mean, double* probs, double* logits) {
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
+  if (ndec != 1 && ndec != K) return -1;
   for (int64_t i = 0; i < n; ++i) {
     if (a[i] < 0 || a[i] >= K) return -3;
     if (row_ptr[i + 1] <= row_ptr[i]) return -4; /* every sample has a positive tag */
@@ -348,10 +351,13 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
         for (int32_t j = 0; j < h; ++j) s += w2[(int64_t)k * h + j] * h1[j];
         y[k] = store_round(s, store);
       }
+      /* the sample's decoder: the shared one, or its expert's own (Section 2) */
+      const double* De = D + (ndec > 1 ? (int64_t)e * V * o : 0);
+      const double* bDe = bD ? bD + (ndec > 1 ? (int64_t)e * V : 0) : NULL;
       double m = -INFINITY;
       for (int32_t v = 0; v < V; ++v) {
-        double s = bD ? bD[v] : 0.0;
-        const double* dv = D + (int64_t)v * o;
+        double s = bDe ? bDe[v] : 0.0;
+        const double* dv = De + (int64_t)v * o;
         for (int32_t j = 0; j < o; ++j) s += dv[j] * y[j];
         lg[v] = s;
         if (s > m) m = s;
@@ -380,13 +386,15 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
 
 /* --------------------------------------------------------------- O10: backward */
 
-/* Gradient of the mean multilabel softmax loss (Section 4.1, Eq. 3) through the shared
- * decoder and the selected expert (Section 2).  The gater is fixed (Section 2.2: the model
- * is not trained end to end), so nothing flows to the centroids.  Saved activations H1, H
- * and lse are inputs (per sample, in sample order).  With p = softmax(D H[i] + bD) and the
- * uniform target y_i (mass 1/|P_i| on each positive):
+/* Gradient of the mean multilabel softmax loss (Section 4.1, Eq. 3) through the decoder
+ * (shared, ndec = 1, or the expert's own, ndec = K; as in the forward) and the selected
+ * expert (Section 2).  The gater is fixed (Section 2.2: the model is not trained end to
+ * end), so nothing flows to the centroids.  Saved activations H1, H and lse are inputs (per
+ * sample, in sample order).  With p = softmax(D_i H[i] + bD_i) and the uniform target y_i
+ * (mass 1/|P_i| on each positive):
  *   g_i  = (p_i - y_i) * scale            (scale = 1/n for the batch mean)
- *   dbD  = sum_i g_i,  dD = sum_i g_i H[i]^T,  dh_i = D^T g_i
+ *   dbD  = sum_i g_i,  dD = sum_i g_i H[i]^T,  dh_i = D_i^T g_i
+ *          (per decoder: decoder e sums over the samples of expert e when ndec = K)
  *   db2_e = sum dh,  dW2_e = sum dh h1^T,  dh1 = W2_e^T dh,  dz = dh1 * [h1 > 0]
  *   db1_e = sum dz,  dW1_e = sum dz x^T,   dx = W1_e^T dz
  * The activation gradients g (as used by dD and dh), dh, dz and dx are the tensors a device
@@ -394,13 +402,14 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
  * recomputed logits are rounded by `store` first, as when a device saved them in the forward.
  * Experts that receive no sample get zero gradients.  dX may be NULL. */
 int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
-                          const double* X, const int32_t* a, const double* W1,
+                          int32_t ndec, const double* X, const int32_t* a, const double* W1,
                           const double* W2, const double* D, const double* bD,
                           const int32_t* row_ptr, const int32_t* tag, const double* H1,
                           const double* H, const double* lse, double scale, int store,
                           int logit_round, double* dW1, double* db1, double* dW2, double* db2,
                           double* dD, double* dbD, double* dX) {
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
+  if (ndec != 1 && ndec != K) return -1;
   for (int64_t i = 0; i < n; ++i) {
     if (a[i] < 0 || a[i] >= K) return -3;
     if (row_ptr[i + 1] <= row_ptr[i]) return -4;
@@ -415,11 +424,13 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
     const int32_t e = a[i];
+    const double* De = D + (ndec > 1 ? (int64_t)e * V * o : 0);
+    const double* bDe = bD ? bD + (ndec > 1 ? (int64_t)e * V : 0) : NULL;
     const double* y = H + i * (int64_t)o;
     double* g = G + i * (int64_t)V;
     for (int32_t v = 0; v < V; ++v) {
-      double s = bD ? bD[v] : 0.0;
-      const double* dv = D + (int64_t)v * o;
+      double s = bDe ? bDe[v] : 0.0;
+      const double* dv = De + (int64_t)v * o;
       for (int32_t j = 0; j < o; ++j) s += dv[j] * y[j];
       if (logit_round) s = store_round(s, store);
       g[v] = exp(s - lse[i]);
@@ -432,7 +443,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     double* dh = dH + i * (int64_t)o;
     for (int32_t j = 0; j < o; ++j) dh[j] = 0.0;
     for (int32_t v = 0; v < V; ++v) {
-      const double* dv = D + (int64_t)v * o;
+      const double* dv = De + (int64_t)v * o;
       for (int32_t j = 0; j < o; ++j) dh[j] += gs[v] * dv[j];
     }
     for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], store);
@@ -453,19 +464,22 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     }
   }
 
-  /* Decoder parameters: one vocabulary row per iteration, samples in ascending order. */
+  /* Decoder parameters: one (decoder, vocabulary row) per iteration, samples in ascending
+   * order; decoder e sums the samples routed to expert e when every expert has its own. */
 #pragma omp parallel for schedule(static)
-  for (int32_t v = 0; v < V; ++v) {
-    double* dd = dD + (int64_t)v * o;
+  for (int64_t r = 0; r < (int64_t)ndec * V; ++r) {
+    const int32_t e = (int32_t)(r / V), v = (int32_t)(r % V);
+    double* dd = dD + r * o;
     double sb = 0.0;
     for (int32_t j = 0; j < o; ++j) dd[j] = 0.0;
     for (int64_t i = 0; i < n; ++i) {
+      if (ndec > 1 && a[i] != e) continue;
       sb += G[i * (int64_t)V + v];
       const double g = GS[i * (int64_t)V + v];
       const double* y = H + i * (int64_t)o;
       for (int32_t j = 0; j < o; ++j) dd[j] += g * y[j];
     }
-    if (dbD) dbD[v] = sb;
+    if (dbD) dbD[r] = sb;
   }
 
   /* Expert parameters: one (expert, output unit) row per iteration. */

@@ -164,15 +164,25 @@ def dispatch(e, K: int):
     return counts, offsets, perm, inv
 
 
+def _ndec(D, K):
+    """Decoders in D: [V][o] is one shared decoder, [K][V][o] one per expert."""
+    D = np.asarray(D)
+    if D.ndim == 2:
+        return 1, D.shape[0]
+    assert D.ndim == 3 and D.shape[0] == K, D.shape
+    return K, D.shape[1]
+
+
 def moe_forward(X, a, W1, b1, W2, b2, D, bD, row_ptr, tag, store: str = "f64",
                 want_probs: bool = False, want_logits: bool = False):
-    """Shared-decoder hard MoE forward with the multilabel softmax loss (Section 2, shared
-    decoder; Section 4.1, Eq. 3).  Per-sample outputs in sample order."""
+    """Hard MoE forward with the multilabel softmax loss (Section 2; Section 4.1, Eq. 3).
+    D [V][o] (bD [V]) is the shared decoder; D [K][V][o] (bD [K][V]) gives every expert its
+    own, and each sample is decoded by its expert's.  Per-sample outputs in sample order."""
     X = _f64(X)
     n, d = X.shape
     K, h, _ = W1.shape
     o = W2.shape[1]
-    V = D.shape[0]
+    ndec, V = _ndec(D, K)
     W1 = _f64(W1); W2 = _f64(W2); D = _f64(D)
     b1 = _f64(b1) if b1 is not None else None
     b2 = _f64(b2) if b2 is not None else None
@@ -184,7 +194,7 @@ def moe_forward(X, a, W1, b1, W2, b2, D, bD, row_ptr, tag, store: str = "f64",
     logits = np.empty((n, V)) if want_logits else None
     rc = _load().hmoe_orc_moe_forward(
         ctypes.c_int64(n), ctypes.c_int32(d), ctypes.c_int32(h), ctypes.c_int32(o),
-        ctypes.c_int32(V), ctypes.c_int32(K), _p(X), _p(a), _p(W1), _p(b1), _p(W2), _p(b2),
+        ctypes.c_int32(V), ctypes.c_int32(K), ctypes.c_int32(ndec), _p(X), _p(a), _p(W1), _p(b1), _p(W2), _p(b2),
         _p(D), _p(bD), _p(row_ptr), _p(tag), ctypes.c_int(_STORE[store]), _p(H1), _p(H),
         _p(lse), _p(loss), _p(lm), _p(probs), _p(logits))
     _check(rc, "moe_forward")
@@ -200,12 +210,13 @@ def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
                  store: str = "f64", want_dX: bool = True, logit_round: bool = False):
     """Gradients of the mean loss w.r.t. every expert and decoder parameter (and X) given the
     saved activations (Section 2; Section 4.1, Eq. 3; the gater gets none, Section 2.2).
+    Decoders as in moe_forward; dD and dbD have D's and bD's shapes.
     logit_round: the logits are taken as stored in `store` precision (saved-logits path)."""
     X = _f64(X)
     n, d = X.shape
     K, h, _ = W1.shape
     o = W2.shape[1]
-    V = D.shape[0]
+    ndec, V = _ndec(D, K)
     W1 = _f64(W1); W2 = _f64(W2); D = _f64(D)
     bD = _f64(bD) if bD is not None else None
     a = _i32(a); row_ptr = _i32(row_ptr); tag = _i32(tag)
@@ -213,11 +224,14 @@ def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
     if scale is None:
         scale = 1.0 / max(n, 1)
     dW1 = np.empty((K, h, d)); db1 = np.empty((K, h)); dW2 = np.empty((K, o, h))
-    db2 = np.empty((K, o)); dD = np.empty((V, o)); dbD = np.empty(V)
+    db2 = np.empty((K, o))
+    per_expert = np.asarray(D).ndim == 3
+    dD = np.empty((K, V, o)) if per_expert else np.empty((V, o))
+    dbD = np.empty((K, V)) if per_expert else np.empty(V)
     dX = np.empty((n, d)) if want_dX else None
     rc = _load().hmoe_orc_moe_backward(
         ctypes.c_int64(n), ctypes.c_int32(d), ctypes.c_int32(h), ctypes.c_int32(o),
-        ctypes.c_int32(V), ctypes.c_int32(K), _p(X), _p(a), _p(W1), _p(W2), _p(D), _p(bD),
+        ctypes.c_int32(V), ctypes.c_int32(K), ctypes.c_int32(ndec), _p(X), _p(a), _p(W1), _p(W2), _p(D), _p(bD),
         _p(row_ptr), _p(tag), _p(H1), _p(H), _p(lse), ctypes.c_double(scale),
         ctypes.c_int(_STORE[store]), ctypes.c_int(1 if logit_round else 0), _p(dW1), _p(db1),
         _p(dW2), _p(db2), _p(dD), _p(dbD), _p(dX))

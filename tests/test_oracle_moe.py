@@ -186,3 +186,99 @@ def test_store_rounding_points(orc):
     f64 = _fwd(orc, c, store="f64")
     # the stored H differs from the unrounded one by at most half a bf16 ulp chain
     assert np.max(np.abs(f["H"] - f64["H"])) < 0.05
+
+
+# ------------------------------------------------------------------ independent decoders
+
+def _case_indep(seed, K=3, empty=None, **kw):
+    """_case with one decoder per expert (D [K][V][o], bD [K][V]; Section 2's
+    independent-decoder figure)."""
+    c = _case(seed, K=K, empty=empty, **kw)
+    rs = np.random.default_rng(seed + 1000)
+    V, o = c["D"].shape
+    c["D"] = rs.normal(size=(K, V, o)) / np.sqrt(o)
+    c["bD"] = rs.normal(size=(K, V)) * 0.3
+    return c
+
+
+def _torch_loss_indep(c):
+    """Per-sample decoder selection written with PyTorch ops (fp64 CPU) for autograd."""
+    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True)
+         for k, v in c.items() if k not in ("row_ptr", "tag", "a")}
+    a = torch.tensor(c["a"], dtype=torch.long)
+    h1 = torch.relu(torch.einsum("nhd,nd->nh", t["W1"][a], t["X"]) + t["b1"][a])
+    y = torch.einsum("noh,nh->no", t["W2"][a], h1) + t["b2"][a]
+    logits = torch.einsum("nvo,no->nv", t["D"][a], y) + t["bD"][a]
+    n, V = logits.shape
+    target = torch.zeros(n, V, dtype=torch.float64)
+    for i in range(n):
+        tg = c["tag"][c["row_ptr"][i]:c["row_ptr"][i + 1]]
+        target[i, torch.tensor(tg, dtype=torch.long)] = 1.0 / len(tg)
+    loss = torch.nn.functional.cross_entropy(logits, target)
+    loss.backward()
+    return t, loss, logits
+
+
+@pytest.mark.parametrize("K,empty", [(1, None), (3, None), (4, 1)])
+def test_independent_decoders_match_torch_autograd(orc, K, empty):
+    c = _case_indep(20 + K, K=K, empty=empty)
+    f = _fwd(orc, c, want_logits=True)
+    b = _bwd(orc, c, f)
+    t, loss, logits = _torch_loss_indep(c)
+    assert np.isclose(f["loss_mean"], loss.item(), rtol=1e-12)
+    np.testing.assert_allclose(f["logits"], logits.detach().numpy(), rtol=1e-12, atol=1e-13)
+    assert b["dD"].shape == c["D"].shape and b["dbD"].shape == c["bD"].shape
+    for k in ("W1", "b1", "W2", "b2", "D", "bD", "X"):
+        np.testing.assert_allclose(b["d" + k], t[k].grad.numpy(), rtol=1e-10, atol=1e-13,
+                                   err_msg=k)
+    if empty is not None:
+        for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD"):
+            assert np.all(b[k][empty] == 0.0), k
+
+
+def test_independent_decoders_finite_differences(orc):
+    c = _case_indep(31, n=12, d=4, h=6, o=3, V=7, K=2, max_tags=3)
+    f = _fwd(orc, c)
+    b = _bwd(orc, c, f)
+    rs = np.random.default_rng(1)
+    eps = 1e-6
+    for key, gkey in (("D", "dD"), ("bD", "dbD"), ("W2", "dW2"), ("X", "dX")):
+        for _ in range(6):
+            idx = tuple(rs.integers(0, s) for s in c[key].shape)
+            cp = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in c.items()}
+            cm = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in c.items()}
+            cp[key][idx] += eps
+            cm[key][idx] -= eps
+            fd = (_fwd(orc, cp)["loss_mean"] - _fwd(orc, cm)["loss_mean"]) / (2 * eps)
+            an = b[gkey][idx]
+            assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (key, idx, fd, an)
+
+
+def test_independent_decoders_equal_to_shared_reduce_to_it(orc):
+    """K copies of one decoder decode exactly as the shared decoder does; each copy's
+    gradient is the shared gradient restricted to its expert's samples, so they sum to it."""
+    c = _case(41, K=3)
+    ci = dict(c)
+    ci["D"] = np.stack([c["D"]] * 3)
+    ci["bD"] = np.stack([c["bD"]] * 3)
+    f, fi = _fwd(orc, c, want_logits=True), _fwd(orc, ci, want_logits=True)
+    for k in ("H1", "H", "lse", "loss", "logits"):
+        np.testing.assert_array_equal(fi[k], f[k], err_msg=k)
+    b, bi = _bwd(orc, c, f), _bwd(orc, ci, fi)
+    for k in ("dW1", "db1", "dW2", "db2", "dX"):
+        np.testing.assert_array_equal(bi[k], b[k], err_msg=k)
+    np.testing.assert_allclose(bi["dD"].sum(axis=0), b["dD"], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(bi["dbD"].sum(axis=0), b["dbD"], rtol=1e-12, atol=1e-15)
+    for e in range(3):
+        sel = c["a"] == e
+        assert np.all(bi["dbD"][e] == 0.0) == (not sel.any())
+
+
+def test_independent_zero_decoders_give_log_v(orc):
+    c = _case_indep(51, K=3)
+    c["D"][:] = 0.0
+    c["bD"][:] = 0.0
+    f = _fwd(orc, c)
+    V = c["D"].shape[1]
+    np.testing.assert_allclose(f["lse"], np.log(V), rtol=1e-15)
+    np.testing.assert_allclose(f["loss"], np.log(V), rtol=1e-15)
