@@ -121,13 +121,20 @@ int hmoe_permute_rows(const void* in, void* out, const int32_t* index, int64_t n
 
 /* ------------------------------------------------------------------ experts + decoder */
 
-/* Parameters of K expert MLPs and the shared decoder (Section 2, shared-decoder figure).
- *   W1 [K][d_hid][d_in], b1 [K][d_hid], W2 [K][d_out][d_hid], b2 [K][d_out],
- *   D [vocab][d_out], bD [vocab]; all in dtype dt; biases may be NULL (no bias). */
+/* Parameters of K expert MLPs and their decoder(s) (Section 2).
+ *   W1 [K][d_hid][d_in], b1 [K][d_hid], W2 [K][d_out][d_hid], b2 [K][d_out]; all in dtype dt;
+ *   biases may be NULL (no bias).
+ *   decoders = 1 (or 0): one decoder shared by all experts (the shared-decoder figure),
+ *     D [vocab][d_out], bD [vocab].
+ *   decoders = K: every expert has its own decoder (the independent-decoder figure), and a
+ *     sample is decoded by its expert's: D [K][vocab][d_out], bD [K][vocab].  The forward then
+ *     stores its logits in expert (slot) order, and the backward needs them (logits != NULL)
+ *     and writes dD [K][vocab][d_out], dbD [K][vocab]. */
 typedef struct {
   int32_t K, d_in, d_hid, d_out, vocab;
   hmoe_dtype_t dt;
   const void *W1, *b1, *W2, *b2, *D, *bD;
+  int32_t decoders;
 } hmoe_moe_params_t;
 
 /* Multilabel targets as CSR: sample i has the distinct positive tags
@@ -138,13 +145,15 @@ typedef struct {
   const int32_t* tag;     /* int32[nnz], 0 <= tag < vocab */
 } hmoe_labels_t;
 
-/* Forward pass of the shared-decoder hard mixture with the loss of Eq. 3.
+/* Forward pass of the hard mixture with the loss of Eq. 3.
  *   X_sorted [n x d_in]: samples in expert order (from hmoe_moe_dispatch), offsets int32[K+1],
  *   perm int32[n] (slot -> sample).
  *   H1_sorted [n x d_hid] out: relu(W1_e x + b1_e) in expert order (saved for backward).
  *   H [n x d_out] out: expert outputs W2_e h1 + b2_e in SAMPLE order (the combine).
  *   logits [n x vocab] out or NULL: D H_i + bD in dtype dt, saved so that the backward does
- *     not recompute them (n * vocab * 2 bytes in bf16; pass NULL to save the memory).
+ *     not recompute them (n * vocab * 2 bytes in bf16; pass NULL to save the memory).  Rows
+ *     in sample order with a shared decoder; in slot order (row p is sample perm[p]) with
+ *     per-expert decoders, where they are required by the backward.
  *   lse float[n] out: log-sum-exp of the V logits (from the fp32 logits).
  *   loss float[n] out: lse_i - mean of the logits of the positive tags.
  *   loss_mean float[1] out: mean over the batch. */
@@ -161,7 +170,8 @@ int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted
  *   dW2 = dH^T H1, dZ = (dH W2) * [H1 > 0]; db1 = sum dZ; dW1 = dZ^T X; dX = dZ W1.
  *   Inputs are the forward's saved tensors (H1_sorted, H, lse, and logits if it saved them:
  *   then p is formed from the stored logits; NULL recomputes them from H) and inv int32[n].
- *   dW1, db1, dW2, db2, dD, dbD: float out (overwritten; experts without samples get 0);
+ *   dW1, db1, dW2, db2, dD, dbD: float out (overwritten; experts without samples get 0, and
+ *   so do their decoders when each expert has its own; dD and dbD have D's and bD's shapes);
  *   db1, db2, dbD may be NULL.  dX [n x d_in] in dtype dt, SAMPLE order, or NULL. */
 int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
                       const int32_t* offsets, const int32_t* perm, const int32_t* inv,

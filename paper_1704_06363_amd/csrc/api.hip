@@ -288,6 +288,8 @@ static int check_params(const hmoe_moe_params_t* p) {
   HMOE_TRY(check_ptr("W1", p->W1));
   HMOE_TRY(check_ptr("W2", p->W2));
   HMOE_TRY(check_ptr("D", p->D));
+  if (p->decoders != 0 && p->decoders != 1 && p->decoders != p->K)
+    return fail(HMOE_EINVAL, "decoders must be 1 (shared) or K (one per expert)");
   return HMOE_OK;
 }
 
@@ -335,12 +337,13 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
     // empty batch: every gradient is zero
     hipStream_t st = (hipStream_t)stream;
     const int64_t K = p->K, d = p->d_in, h = p->d_hid, o = p->d_out, V = p->vocab;
+    const int64_t nd = p->decoders > 1 ? p->decoders : 1;
     HMOE_TRY(launch_zero_f32(dW1, K * h * d, st));
     HMOE_TRY(launch_zero_f32(dW2, K * o * h, st));
-    HMOE_TRY(launch_zero_f32(dD, V * o, st));
+    HMOE_TRY(launch_zero_f32(dD, nd * V * o, st));
     if (db1) HMOE_TRY(launch_zero_f32(db1, K * h, st));
     if (db2) HMOE_TRY(launch_zero_f32(db2, K * o, st));
-    if (dbD) HMOE_TRY(launch_zero_f32(dbD, V, st));
+    if (dbD) HMOE_TRY(launch_zero_f32(dbD, nd * V, st));
     return HMOE_OK;
   }
   HMOE_TRY(check_ptr("X_sorted", X_sorted));
@@ -354,6 +357,8 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
   HMOE_TRY(check_ptr("H", H));
   HMOE_TRY(check_ptr("lse", lse, false));
   if (logits) HMOE_TRY(check_ptr("logits", logits));
+  else if (p->decoders > 1)
+    return fail(HMOE_EINVAL, "with one decoder per expert the backward needs the forward's saved logits");
   if (dX) HMOE_TRY(check_ptr("dX", dX));
   HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
   Workspace w(ws, ws_bytes);

@@ -198,6 +198,35 @@ __global__ void __launch_bounds__(C::THREADS)
   }
 }
 
+// One decoder per expert (row-grouped): the slot rows of expert e against D_e [V][o] and
+// bD_e; the softmax partials (dec_tile_stats, rows in slot order) and, when L is given, the
+// logits in slot order.  One tile per workgroup.
+template <class C>
+__global__ void __launch_bounds__(C::THREADS)
+    k_dec_fwd_grouped(const typename C::type* __restrict__ Hs, const typename C::type* __restrict__ D,
+                      const typename C::type* __restrict__ bD, const int32_t* __restrict__ seg,
+                      const int32_t* __restrict__ tile_start, int G, int64_t n, int V, int o, float* __restrict__ pm,
+                      float* __restrict__ ps, typename C::type* __restrict__ L) {
+  using T = typename C::type;
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, V, o);
+  if (!tc.valid) return;
+  floatx4 acc[C::MI][C::NJ];
+  gemm_tile<C, true, true>(Hs + tc.m0 * o, o, tc.m_rows, D + ((int64_t)tc.group * V + tc.n0) * o, o, tc.n_cols, o,
+                           smem, acc);
+  using F = Frag<C>;
+  float bias[F::NCOL];
+  dec_tile_bias<C>(tc, bD ? bD + (int64_t)tc.group * V : nullptr, bias);
+  lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
+  dec_tile_stats<C>(tc, acc, bias, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
+  if (L) {
+    if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
+    store_out<C, T>(tc, acc, smem, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
+                    RowId{tc.m0}, NoVec{});
+  }
+}
+
 // The same computation as a persistent kernel on the direct-to-LDS engine: gridDim.x workgroups
 // walk the tiles blockIdx.x, blockIdx.x + gridDim.x, ...  After a tile's K loop the workgroup
 // forms the tile's softmax statistics, issues the first stages of its next tile and only then
@@ -276,15 +305,26 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row (row
 // widths are multiples of 8, so o / (16 / sizeof(T)) vectors cover a row exactly).
+// With per-expert decoders the rows (partials and H) are in slot order: row r is sample
+// perm[r], decoded by D_e, bD_e of the expert e whose segment of `seg` holds r; lse and loss
+// are written in sample order.  Shared decoder: perm = seg = NULL.
 template <typename T>
 __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, const float* __restrict__ ps,
                                                   int nt, const T* __restrict__ H, const T* __restrict__ D,
-                                                  const T* __restrict__ bD, int64_t n, int o,
-                                                  const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ tag,
-                                                  float* __restrict__ lse, float* __restrict__ loss) {
+                                                  const T* __restrict__ bD, int64_t n, int o, int V,
+                                                  const int32_t* __restrict__ perm, const int32_t* __restrict__ seg,
+                                                  int G, const int32_t* __restrict__ row_ptr,
+                                                  const int32_t* __restrict__ tag, float* __restrict__ lse,
+                                                  float* __restrict__ loss) {
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
   if (row >= n) return;
+  const int64_t smp = perm ? perm[row] : row;
+  if (seg) {
+    const int e = find_segment(seg, G, row);
+    D += (int64_t)e * V * o;
+    if (bD) bD += (int64_t)e * V;
+  }
   float M = -FLT_MAX;
   for (int t = l; t < nt; t += 64) M = fmaxf(M, pm[(int64_t)t * n + row]);
   M = wave_max(M);
@@ -295,7 +335,7 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
   // positive logits: lane group g (8 lanes) takes tags g, g + 8, ...; each lane covers every
   // 8th 16-byte chunk of the rows; the partial sums are combined over the wave in a fixed order
   constexpr int EPV = 16 / sizeof(T);
-  const int32_t p0 = row_ptr[row], p1 = row_ptr[row + 1];
+  const int32_t p0 = row_ptr[smp], p1 = row_ptr[smp + 1];
   const int g = l >> 3, gl = l & 7;
   const T* h = H + row * o;
   const int vpr = o / EPV;
@@ -316,8 +356,8 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
   }
   pos = wave_sum(pos);
   if (l == 0) {
-    lse[row] = Lv;
-    loss[row] = Lv - pos / (float)(p1 - p0);
+    lse[smp] = Lv;
+    loss[smp] = Lv - pos / (float)(p1 - p0);
   }
 }
 
@@ -456,25 +496,43 @@ __global__ void __launch_bounds__(C::THREADS)
 // per row in the few rows that have one here.  A row with more than MAXT tags in the slab
 // (flag -1) reads its tags from global memory instead.  g is stored non-temporally: it is only
 // read back by the next kernels, long after it has left the caches (measured 3.07 -> 2.91 ms).
+// Per-expert decoders: the rows (L, g) are in slot order, row r being sample perm[r], and a
+// block takes a piece of at most kGradRows rows of one expert (pieces numbered by
+// piece_start, as in the segmented sums), so its column sums belong to one decoder's dbD.
+// Shared decoder: perm = piece_start = NULL and block b takes rows [b, b + 1) * kGradRows.
 constexpr int kGradRows = 256;
 
 template <typename T>
 __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, const float* __restrict__ lse,
                                                        const int32_t* __restrict__ row_ptr,
                                                        const int32_t* __restrict__ tag, int64_t n, int V,
-                                                       float inv_n, T* __restrict__ G, float* __restrict__ part_db) {
+                                                       float inv_n, const int32_t* __restrict__ perm,
+                                                       const int32_t* __restrict__ seg,
+                                                       const int32_t* __restrict__ piece_start, int NG,
+                                                       T* __restrict__ G, float* __restrict__ part_db) {
   constexpr int EPV = 16 / sizeof(T);
   constexpr int MAXT = 16;
   constexpr float kLog2e = 1.4426950408889634f;
   __shared__ float s_lse2[kGradRows], s_yn[kGradRows];
-  __shared__ int32_t s_cnt[kGradRows];
+  __shared__ int32_t s_cnt[kGradRows], s_smp[kGradRows];
   __shared__ int16_t s_tag[kGradRows * MAXT];  // column within the slab
-  const int64_t r0 = (int64_t)blockIdx.x * kGradRows;
-  const int rows = (int)((n - r0) < kGradRows ? (n - r0) : kGradRows);
+  int64_t r0, rend;
+  if (piece_start) {
+    if ((int64_t)blockIdx.x >= piece_start[NG]) return;
+    const int e = find_segment(piece_start, NG, blockIdx.x);
+    r0 = seg[e] + (int64_t)(blockIdx.x - piece_start[e]) * kGradRows;
+    rend = seg[e + 1];
+  } else {
+    r0 = (int64_t)blockIdx.x * kGradRows;
+    rend = n;
+  }
+  const int rows = (int)((rend - r0) < kGradRows ? (rend - r0) : kGradRows);
   const int slab0 = blockIdx.y * 256 * EPV;
   for (int t = threadIdx.x; t < rows; t += 256) {
-    const int32_t p0 = row_ptr[r0 + t], cnt = row_ptr[r0 + t + 1] - p0;
-    s_lse2[t] = lse[r0 + t] * kLog2e;
+    const int64_t smp = perm ? perm[r0 + t] : r0 + t;
+    const int32_t p0 = row_ptr[smp], cnt = row_ptr[smp + 1] - p0;
+    s_smp[t] = (int32_t)smp;
+    s_lse2[t] = lse[smp] * kLog2e;
     s_yn[t] = inv_n / (float)cnt;
     int k = 0;
     for (int q = 0; q < cnt; ++q) {
@@ -522,7 +580,7 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
             }
           }
         } else {
-          const int32_t p0 = row_ptr[r0 + t], cnt = row_ptr[r0 + t + 1] - p0;
+          const int32_t p0 = row_ptr[s_smp[t]], cnt = row_ptr[s_smp[t] + 1] - p0;
           for (int32_t q = 0; q < cnt; ++q) {
             const int d = tag[p0 + q] - c0;
             if ((unsigned)d < (unsigned)EPV) {
@@ -546,6 +604,19 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
   float* dst = part_db + (int64_t)blockIdx.x * V + c0;
 #pragma unroll
   for (int e = 0; e < EPV; ++e) dst[e] = cs[e];
+}
+
+// dbD_e[v] = sum of the piece partials of expert e (pieces piece_start[e] .. piece_start[e+1]),
+// in piece order.  Grid: (ceil(V / 256), NG).
+__global__ void __launch_bounds__(256) k_piece_colsum(const float* __restrict__ part,
+                                                      const int32_t* __restrict__ piece_start, int V,
+                                                      float* __restrict__ out) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int e = blockIdx.y;
+  if (c >= V) return;
+  float s = 0.f;
+  for (int q = piece_start[e]; q < piece_start[e + 1]; ++q) s += part[(int64_t)q * V + c];
+  out[(int64_t)e * V + c] = s;
 }
 
 __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int rows, int V,
@@ -667,7 +738,8 @@ struct ReluMask {
 };
 
 // Row-grouped input gradients.  MASK: dZ[m] = (dYs[m] W2_e) * [H1s[m] > 0], stored in expert
-// order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order.
+// order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order (in slot order, row m, when
+// perm is NULL: the per-expert decoders' dH = g D_e).
 //   A: [rows][Kd] (ld Kd), W: [G][Kd][N] (the layer's [out][in] weights seen as [K][N]).
 template <class C, bool MASK>
 __global__ void __launch_bounds__(C::THREADS)
@@ -685,8 +757,10 @@ __global__ void __launch_bounds__(C::THREADS)
                             Kd, smem, acc);
   if (MASK)
     store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, ReluMask<T>{H1s, tc.m0, N, tc.n0});
-  else
+  else if (perm)
     store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowVia{perm, tc.m0}, NoVec{});
+  else
+    store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
 // ------------------------------------------------------------------ launchers
@@ -694,10 +768,11 @@ __global__ void __launch_bounds__(C::THREADS)
 struct MoeShape {
   int64_t n;
   int K, d, h, o, V;
+  int nd;  // decoders: 1 shared, or K (one per expert)
 };
 
 static MoeShape shape_of(const hmoe_moe_params_t* p, int64_t n) {
-  return MoeShape{n, p->K, p->d_in, p->d_hid, p->d_out, p->vocab};
+  return MoeShape{n, p->K, p->d_in, p->d_hid, p->d_out, p->vocab, p->decoders > 1 ? p->decoders : 1};
 }
 
 template <typename T>
@@ -708,6 +783,7 @@ static size_t fwd_ws(const MoeShape& s) {
   ws.take<int32_t>(s.K + 1);
   ws.take<float>((size_t)ntv * s.n);
   ws.take<float>((size_t)ntv * s.n);
+  if (s.nd > 1) ws.take<T>((size_t)s.n * s.o);
   ws.take<double>(kSumBlocks);
   return ws.off;
 }
@@ -722,8 +798,12 @@ static size_t bwd_ws(const MoeShape& s) {
   ws.take<T>((size_t)s.n * s.o);
   ws.take<T>((size_t)s.n * s.h);
   const int64_t prow = cdiv(s.n, C::BM) > cdiv(s.n, kGradRows) ? cdiv(s.n, C::BM) : cdiv(s.n, kGradRows);
-  ws.take<float>((size_t)prow * s.V);
+  ws.take<float>((size_t)(prow + s.K) * s.V);
   ws.take<float>((size_t)kMaxSplitItems * C::BM * C::BN);
+  if (s.nd > 1) {
+    ws.take<T>((size_t)s.n * s.o);
+    ws.take<int32_t>(s.K + 1);
+  }
   const int w = s.h > s.o ? s.h : s.o;
   return ws.off + segsum_ws(s.n, s.K, w) + 256;
 }
@@ -745,6 +825,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   int32_t* ts = ws.take<int32_t>(s.K + 1);
   float* pm = ws.take<float>((size_t)ntv * n);
   float* ps = ws.take<float>((size_t)ntv * n);
+  T* Hs = s.nd > 1 ? ws.take<T>((size_t)n * s.o) : nullptr;  // H in slot order
   if (!ws.fits()) return HMOE_EWORKSPACE;
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
@@ -755,6 +836,15 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
               dim3(C::THREADS), C::LDS, st, Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
   HMOE_LAUNCH("expert layer 2", (k_expert_fwd<C, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
+  if (s.nd > 1) {
+    // one decoder per expert: decode in slot order
+    HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
+    HMOE_LAUNCH("decoder forward", k_dec_fwd_grouped<C>, dim3((unsigned)(mt_bound * ntv)), dim3(C::THREADS), C::LDS,
+                st, (const T*)Hs, D, (const T*)p->bD, offsets, ts, s.K, n, s.V, s.o, pm, ps, Lg);
+    HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv,
+                (const T*)Hs, D, (const T*)p->bD, n, s.o, s.V, perm, offsets, s.K, y->row_ptr, y->tag, lse, loss);
+    return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
+  }
   if constexpr (C::DMA) {
     // persistent: one workgroup per resident slot
     const int64_t tiles = cdiv(n, C::BM) * ntv;
@@ -768,7 +858,8 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
                 st, (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
   }
   HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
-              (const T*)p->bD, n, s.o, y->row_ptr, y->tag, lse, loss);
+              (const T*)p->bD, n, s.o, s.V, (const int32_t*)nullptr, (const int32_t*)nullptr, 0, y->row_ptr,
+              y->tag, lse, loss);
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
 }
 
@@ -786,19 +877,47 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   T* dZ = ws.take<T>((size_t)n * s.h);
   const int mt = (int)cdiv(n, C::BM);
   const int gr = (int)cdiv(n, kGradRows);
-  float* pdb = ws.take<float>((size_t)(mt > gr ? mt : gr) * s.V);
+  float* pdb = ws.take<float>((size_t)((mt > gr ? mt : gr) + s.K) * s.V);
   float* split_part = ws.take<float>((size_t)kMaxSplitItems * C::BM * C::BN);
+  T* Hs = nullptr;
+  int32_t* gts = nullptr;
+  if (s.nd > 1) {
+    Hs = ws.take<T>((size_t)n * s.o);  // H in slot order
+    gts = ws.take<int32_t>(s.K + 1);   // first gradient piece of each expert
+  }
   if (!ws.fits()) return HMOE_EWORKSPACE;
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
   const T* D = (const T*)p->D;
   const int ntv = (int)cdiv(s.V, C::BN);
-  // decoder
+  const int64_t mt_bound = cdiv(n, C::BM) + s.K;
+  HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
+  HMOE_TRY(launch_seg_order(offsets, s.K, order, st));
+  constexpr int EPV = 16 / sizeof(T);
+  if (s.nd > 1) {
+    // One decoder per expert, everything in slot order (the API guarantees saved logits):
+    // g from the stored logits in pieces that stay within one expert, dbD_e from the pieces'
+    // column sums, dH = g D_e (row-grouped), dD_e = g_e^T H_e (reduction-grouped).
+    HMOE_TRY(launch_seg_tiles(offsets, s.K, kGradRows, gts, st));
+    HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)(gr + s.K), (unsigned)cdiv(s.V, 256 * EPV)),
+                dim3(256), 0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), perm, offsets,
+                gts, s.K, G, pdb);
+    if (dbD)
+      HMOE_LAUNCH("decoder bias grad", k_piece_colsum, dim3((unsigned)cdiv(s.V, 256), (unsigned)s.K), dim3(256), 0,
+                  st, pdb, gts, s.V, dbD);
+    HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
+    HMOE_LAUNCH("decoder dH", (k_expert_dgrad<C, false>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
+                dim3(C::THREADS), C::LDS, st, (const T*)G, D, offsets, ts, s.K, s.o, s.V, (const T*)nullptr,
+                (const int32_t*)nullptr, dYs);
+    HMOE_LAUNCH("decoder dD", k_expert_wgrad<C>,
+                dim3((unsigned)((int64_t)s.K * cdiv(s.V, C::BM) * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
+                (const T*)G, (const T*)Hs, offsets, order, s.K, s.V, s.o, dD);
+  } else {
   int prow;
   if (Lg) {
-    constexpr int EPV = 16 / sizeof(T);
     HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)gr, (unsigned)cdiv(s.V, 256 * EPV)), dim3(256),
-                0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), G, pdb);
+                0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), (const int32_t*)nullptr,
+                (const int32_t*)nullptr, (const int32_t*)nullptr, 0, G, pdb);
     prow = gr;
   } else {
     HMOE_LAUNCH("decoder grad", k_dec_grad<C>, dim3((unsigned)(mt * ntv)), dim3(C::THREADS), C::LDS, st, H, D,
@@ -825,15 +944,13 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
       HMOE_LAUNCH("decoder dD reduce", k_split_reduce<C>, dim3((unsigned)cdiv(R * C::BM * C::BN, 256)), dim3(256), 0,
                   st, split_part, n, s.V, s.o, t_full, split, (int)R, dD);
   }
+  }
   // experts
-  HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
-  HMOE_TRY(launch_seg_order(offsets, s.K, order, st));
   const size_t mark = ws.off;
   if (db2) HMOE_TRY(launch_segsum<T, float>(dYs, s.o, nullptr, offsets, s.K, s.o, n, db2, 0, ws, st));
   ws.off = mark;
   HMOE_LAUNCH("expert dW2", k_expert_wgrad<C>, dim3((unsigned)((int64_t)s.K * cdiv(s.o, C::BM) * cdiv(s.h, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)dYs, H1s, offsets, order, s.K, s.o, s.h, dW2);
-  const int64_t mt_bound = cdiv(n, C::BM) + s.K;
   HMOE_LAUNCH("expert dH1", (k_expert_dgrad<C, true>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
               dim3(C::THREADS), C::LDS, st, (const T*)dYs, W2, offsets, ts, s.K, s.h, s.o, H1s, perm, dZ);
   if (db1) HMOE_TRY(launch_segsum<T, float>(dZ, s.h, nullptr, offsets, s.K, s.h, n, db1, 0, ws, st));

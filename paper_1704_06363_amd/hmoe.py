@@ -38,7 +38,8 @@ class MoeParams(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("d_in", ctypes.c_int32), ("d_hid", ctypes.c_int32),
                 ("d_out", ctypes.c_int32), ("vocab", ctypes.c_int32), ("dt", ctypes.c_int),
                 ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("W2", ctypes.c_void_p),
-                ("b2", ctypes.c_void_p), ("D", ctypes.c_void_p), ("bD", ctypes.c_void_p)]
+                ("b2", ctypes.c_void_p), ("D", ctypes.c_void_p), ("bD", ctypes.c_void_p),
+                ("decoders", ctypes.c_int32)]
 
 
 class Labels(ctypes.Structure):
@@ -268,12 +269,16 @@ def permute_rows(inp, index, out=None):
 # ------------------------------------------------------------------ experts + decoder
 
 def make_params(p: dict) -> MoeParams:
-    """p: W1 [K,h,d], b1 [K,h] or None, W2 [K,o,h], b2 [K,o] or None, D [V,o], bD [V] or None."""
+    """p: W1 [K,h,d], b1 [K,h] or None, W2 [K,o,h], b2 [K,o] or None, and the decoder: shared,
+    D [V,o] with bD [V] or None, or one per expert, D [K,V,o] with bD [K,V] or None."""
     K, h, d = p["W1"].shape
     o = p["W2"].shape[1]
-    V = p["D"].shape[0]
+    per_expert = p["D"].dim() == 3
+    if per_expert and p["D"].shape[0] != K:
+        raise HmoeError(f"per-expert decoders need D [K, V, o] with K = {K}, got {tuple(p['D'].shape)}")
+    V = p["D"].shape[-2]
     return MoeParams(K, d, h, o, V, _dt(p["W1"]), _ptr(p["W1"]), _ptr(p.get("b1")), _ptr(p["W2"]),
-                     _ptr(p.get("b2")), _ptr(p["D"]), _ptr(p.get("bD")))
+                     _ptr(p.get("b2")), _ptr(p["D"]), _ptr(p.get("bD")), K if per_expert else 1)
 
 
 def moe_workspace(params: MoeParams, n) -> int:
@@ -282,8 +287,9 @@ def moe_workspace(params: MoeParams, n) -> int:
 
 def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None,
                 save_logits=False):
-    """Expert MLPs + shared decoder + multilabel softmax loss (Eq. 3).  With save_logits the
-    [n, V] logits are returned too (for a backward that does not recompute them)."""
+    """Expert MLPs + decoder(s) + multilabel softmax loss (Eq. 3).  With save_logits the
+    [n, V] logits are returned too (for a backward that does not recompute them; in slot
+    order, row p = sample perm[p], when every expert has its own decoder, which needs them)."""
     prm = make_params(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
@@ -319,8 +325,8 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
          "db1": o.get("db1", torch.empty(K, h, dtype=f32, device=dev)),
          "dW2": o.get("dW2", torch.empty(K, o_, h, dtype=f32, device=dev)),
          "db2": o.get("db2", torch.empty(K, o_, dtype=f32, device=dev)),
-         "dD": o.get("dD", torch.empty(V, o_, dtype=f32, device=dev)),
-         "dbD": o.get("dbD", torch.empty(V, dtype=f32, device=dev)),
+         "dD": o.get("dD", torch.empty(p["D"].shape, dtype=f32, device=dev)),
+         "dbD": o.get("dbD", torch.empty(p["D"].shape[:-1], dtype=f32, device=dev)),
          "dX": (o.get("dX", torch.empty(n, d, dtype=X_sorted.dtype, device=dev))
                 if want_dX else None)}
     lab = Labels(_ptr(row_ptr), _ptr(tag))

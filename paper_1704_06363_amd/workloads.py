@@ -124,10 +124,12 @@ def zipf_labels(n: int, V: int, max_tags: int, seed: int, s: float = 1.1, min_ta
 # ---------------------------------------------------------------- experts and decoder
 
 def moe_params(K: int, d: int, h: int, o: int, V: int, seed: int, dtype: str = "bf16",
-               device="cpu", bias: bool = False, bias_scale: float = 0.1) -> dict:
-    """Expert MLPs (Linear d->h, ReLU, Linear h->o; [out][in] layout) and the shared decoder
-    (Linear o->V).  Weights ~ N(0, 1/fan_in).  Biases are zero unless `bias` is set, then
-    N(0, bias_scale^2) (used to exercise the bias paths)."""
+               device="cpu", bias: bool = False, bias_scale: float = 0.1,
+               per_expert_decoders: bool = False) -> dict:
+    """Expert MLPs (Linear d->h, ReLU, Linear h->o; [out][in] layout) and the decoder
+    (Linear o->V): one shared D [V, o], bD [V], or with per_expert_decoders one per expert,
+    D [K, V, o], bD [K, V].  Weights ~ N(0, 1/fan_in).  Biases are zero unless `bias` is set,
+    then N(0, bias_scale^2) (used to exercise the bias paths)."""
     g = _gen(device, seed)
     dt = _DT[dtype]
 
@@ -141,8 +143,9 @@ def moe_params(K: int, d: int, h: int, o: int, V: int, seed: int, dtype: str = "
                     * bias_scale).to(dt)
         return torch.zeros(*shape, device=device, dtype=dt)
 
+    dec = (K,) if per_expert_decoders else ()
     return {"W1": w((K, h, d), d), "b1": b((K, h)), "W2": w((K, o, h), h), "b2": b((K, o)),
-            "D": w((V, o), o), "bD": b((V,))}
+            "D": w(dec + (V, o), o), "bD": b(dec + (V,))}
 
 
 def zipf_bucket_ids(n: int, K: int, seed: int, s: float = 1.3,

@@ -1,0 +1,122 @@
+"""The independent-decoder variant (Section 2: every expert has its own decoder D_e, bD_e and a
+sample is decoded by its expert's) on the HIP path against the fp64 oracle, in fp32 and bf16,
+at ragged multi-tile sizes with an empty expert; and its reduction to the shared decoder when
+all the D_e are equal."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_1704_06363_amd import hmoe
+from paper_1704_06363_amd import workloads as W
+from tests.parity import RTOL, assert_close, assert_scalar_close, np64, npi
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(n, d, h, o, V, K, store, seed, empty=None, bias=True):
+    X = W.rectified_gaussian(n, d, seed=seed, dtype=store, device="cuda")
+    ids = np.random.default_rng(seed + 1).integers(0, K, n).astype(np.int32)
+    if empty is not None:
+        ids[ids == empty] = (empty + 1) % K
+    rp, tg = W.zipf_labels(n, V, 8, seed=seed + 2)
+    p = W.moe_params(K, d, h, o, V, seed=seed + 3, dtype=store, device="cuda", bias=bias,
+                     per_expert_decoders=True)
+    return X, ids, rp, tg, p
+
+
+def _check(X, ids, rp, tg, p, K, store):
+    rt = RTOL[store]
+    a = torch.as_tensor(ids, dtype=torch.int32).cuda()
+    dd = hmoe.moe_dispatch(a, K, rows=X)
+    row_ptr = torch.tensor(rp, device="cuda")
+    tag = torch.tensor(tg, device="cuda")
+    f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], row_ptr, tag, save_logits=True)
+    Xh = np64(X)
+    ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
+    ref = O.moe_forward(Xh, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
+                        store=store, want_logits=True)
+    perm = npi(dd["perm"])
+    assert_close(f["H1_sorted"], ref["H1"][perm], rt, "H1_sorted")
+    assert_close(f["H"], ref["H"], rt, "H")
+    assert_close(f["lse"], ref["lse"], rt, "lse")
+    assert_close(f["loss"], ref["loss"], rt, "loss")
+    assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
+    assert_close(f["logits"], ref["logits"][perm], rt, "logits (slot order)")
+    # backward from the oracle's saved activations and logits (slot order)
+    tdt = torch.bfloat16 if store == "bf16" else torch.float32
+    H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(tdt).cuda()
+    H = torch.tensor(ref["H"], dtype=torch.float32).to(tdt).cuda()
+    lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
+    Lg = torch.tensor(ref["logits"][perm], dtype=torch.float32).to(tdt).cuda()
+    g = hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], row_ptr, tag, H1s, H,
+                          lse, logits=Lg)
+    gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
+                        ref["lse"], store=store, logit_round=True)
+    for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
+        assert_close(g[k], gr[k], rt, k)
+    return g
+
+
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+def test_independent_decoders_ragged_with_empty_expert(store):
+    # 1100 rows over 5 experts (expert 2 empty), V = 1000 and o = 136: ragged in rows, columns
+    # and K; every decoder tile shape and an empty expert's decoder (exact zero gradients)
+    n, d, h, o, V, K = 1100, 256, 384, 136, 1000, 5
+    X, ids, rp, tg, p = _run(n, d, h, o, V, K, store, seed=100, empty=2)
+    g = _check(X, ids, rp, tg, p, K, store)
+    assert torch.count_nonzero(g["dD"][2]).item() == 0
+    assert torch.count_nonzero(g["dbD"][2]).item() == 0
+
+
+def test_independent_decoders_one_expert_and_single_sample():
+    X, ids, rp, tg, p = _run(300, 64, 64, 64, 264, 1, "bf16", seed=110)
+    _check(X, ids, rp, tg, p, 1, "bf16")
+    X, ids, rp, tg, p = _run(1, 64, 64, 32, 96, 4, "bf16", seed=111)
+    _check(X, ids, rp, tg, p, 4, "bf16")
+
+
+def test_equal_decoders_reduce_to_the_shared_one():
+    """Every expert given the same decoder: the HIP path's per-expert results agree with its
+    shared-decoder results (loss exactly per sample up to summation order; dD summed over the
+    experts is the shared dD)."""
+    n, d, h, o, V, K = 1500, 128, 256, 128, 704, 4
+    inp = W.balanced_inputs(device="cuda", seed=120, n=n, d=d, h=h, o=o, V=V, K=K, bias=True)
+    ps = inp["params"]
+    pe = dict(ps)
+    pe["D"] = ps["D"].unsqueeze(0).expand(K, V, o).contiguous()
+    pe["bD"] = ps["bD"].unsqueeze(0).expand(K, V).contiguous()
+    a, _ = hmoe.kmeans_assign(inp["X"], inp["C"])
+    dd = hmoe.moe_dispatch(a, K, rows=inp["X"])
+    rp = torch.as_tensor(inp["row_ptr"]).cuda()
+    tg = torch.as_tensor(inp["tag"]).cuda()
+    args = (dd["rows_sorted"], dd["offsets"], dd["perm"], rp, tg)
+    fs = hmoe.moe_forward(ps, *args, save_logits=True)
+    fe = hmoe.moe_forward(pe, *args, save_logits=True)
+    rt = RTOL["bf16"]
+    for k in ("H1_sorted", "H"):
+        assert torch.equal(fs[k], fe[k]), k
+    assert_close(fe["lse"], fs["lse"], 1e-5, "lse")
+    assert_close(fe["loss"], fs["loss"], 1e-5, "loss")
+    perm = dd["perm"].long()
+    assert_close(fe["logits"], fs["logits"][perm], 1e-2, "logits")
+    gs = hmoe.moe_backward(ps, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, fs["H1_sorted"],
+                           fs["H"], fs["lse"], logits=fs["logits"])
+    ge = hmoe.moe_backward(pe, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, fe["H1_sorted"],
+                           fe["H"], fe["lse"], logits=fe["logits"])
+    for k in ("dW1", "db1", "dW2", "db2", "dX"):
+        assert_close(ge[k], gs[k], rt, k)
+    assert_close(ge["dD"].sum(0), gs["dD"], rt, "sum_e dD_e")
+    assert_close(ge["dbD"].sum(0), gs["dbD"], rt, "sum_e dbD_e")
+
+
+def test_backward_needs_saved_logits():
+    X, ids, rp, tg, p = _run(64, 64, 64, 64, 96, 2, "bf16", seed=130)
+    a = torch.as_tensor(ids, dtype=torch.int32).cuda()
+    dd = hmoe.moe_dispatch(a, 2, rows=X)
+    row_ptr = torch.tensor(rp, device="cuda")
+    tag = torch.tensor(tg, device="cuda")
+    f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], row_ptr, tag, save_logits=True)
+    with pytest.raises(hmoe.HmoeError, match="saved logits"):
+        hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], row_ptr, tag,
+                          f["H1_sorted"], f["H"], f["lse"])
