@@ -10,8 +10,9 @@ tensors already resident in HBM.
 Printed: one JSON line with the step throughput (samples/s), the roofline of the dominant
 kernel (HIP events recorded around every launch in the timed region), the fp64 CPU oracle
 timed on a bounded sample of the same workload, and extra legs for the gater fit
-(2^20 fp32 rows, K = 64, 20 Lloyd iterations), the skewed routing step (K = 128, V = 100k)
-and the large streamed assignment (2^24 bf16 rows, K = 1024).
+(2^20 fp32 rows, K = 64, 20 Lloyd iterations), the skewed routing step (K = 128, V = 100k),
+the balanced step with one decoder per expert (the independent-decoder model) and the large
+streamed assignment (2^24 bf16 rows, K = 1024).
 """
 from __future__ import annotations
 
@@ -145,8 +146,8 @@ class RoutedStep:
                       "db1": torch.empty(K, h, dtype=f32, device=dev),
                       "dW2": torch.empty(K, o, h, dtype=f32, device=dev),
                       "db2": torch.empty(K, o, dtype=f32, device=dev),
-                      "dD": torch.empty(V, o, dtype=f32, device=dev),
-                      "dbD": torch.empty(V, dtype=f32, device=dev),
+                      "dD": torch.empty(inp["params"]["D"].shape, dtype=f32, device=dev),
+                      "dbD": torch.empty(inp["params"]["D"].shape[:-1], dtype=f32, device=dev),
                       "dX": torch.empty(n, d, dtype=bf, device=dev)}
         prm = hmoe.make_params(inp["params"])
         need = max(hmoe.moe_workspace(prm, n), hmoe.moe_dispatch_workspace(n, K),
@@ -301,6 +302,30 @@ def leg_skewed(steps, warmup):
     return out
 
 
+def leg_independent(steps, warmup):
+    """The balanced routed step with one decoder per expert (Section 2's independent-decoder
+    model): the same per-sample work, so the same FLOPs per step."""
+    import torch
+    from paper_1704_06363_amd import workloads as W
+    inp = W.balanced_inputs(device="cuda", seed=0)
+    s = inp["shape"]
+    inp["params"] = W.moe_params(s["K"], s["d"], s["h"], s["o"], s["V"], seed=20, dtype="bf16",
+                                 device="cuda", per_expert_decoders=True)
+    st = RoutedStep(inp, routed_by_gater=True)
+    ms, rep = time_steps(st.run, steps, warmup)
+    fl = gemm_flops(s)
+    tot = step_flops(s)
+    out = {"workload": "independent-decoder routed step: n=65536 bf16, d=2048, K=16 experts each with "
+                       "its own decoder (16 x 50000 x 1024), MLP 2048-4096-1024, fwd+bwd",
+           "samples_per_s": round(s["n"] / (ms * 1e-3), 1), "ms_per_step": round(ms, 3),
+           "tflops": round(tot / (ms * 1e-3) / 1e12, 1),
+           "frac_bf16_peak": round(tot / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "kernels": kernel_table(rep, fl, PEAK_BF16_TFLOPS, steps)}
+    del st, inp
+    torch.cuda.empty_cache()
+    return out
+
+
 def leg_large_assign(n_chunks):
     import torch
     from paper_1704_06363_amd import hmoe
@@ -357,7 +382,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-legs", action="store_true", help="skip the gater/skewed/large legs")
+    ap.add_argument("--no-legs", action="store_true", help="skip the gater/skewed/independent/large legs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
@@ -429,6 +454,8 @@ def main():
         legs["gater_fit"] = leg_gater_fit(steps=2)
         log("leg: skewed routing")
         legs["skewed"] = leg_skewed(steps=max(2, args.steps // 2), warmup=1)
+        log("leg: independent decoders")
+        legs["independent"] = leg_independent(steps=max(2, args.steps // 2), warmup=1)
         log("leg: large assign")
         legs["large_assign"] = leg_large_assign(args.large_chunks)
         res["legs"] = legs

@@ -120,3 +120,51 @@ def test_backward_needs_saved_logits():
     with pytest.raises(hmoe.HmoeError, match="saved logits"):
         hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], row_ptr, tag,
                           f["H1_sorted"], f["H"], f["lse"])
+
+
+def test_independent_step_full_size():
+    """The balanced workload's shapes (n = 65536, d = 2048, MLP 2048-4096-1024, V = 50,000,
+    K = 16) with one decoder per expert, in the bench's launch configuration: H, lse, loss and
+    dX on sampled rows of two experts against the oracle (the experts remapped to 0 and 1, so
+    the oracle widens two decoders instead of sixteen), and per-expert invariants of the
+    gradients: sum_v dbD_e = 0, sum_v dD_e = 0, db2_e = D_e^T dbD_e."""
+    inp = W.balanced_inputs(device="cuda", seed=0)
+    s = inp["shape"]
+    n, K, V, o = s["n"], s["K"], s["V"], s["o"]
+    p = W.moe_params(K, s["d"], s["h"], o, V, seed=20, dtype="bf16", device="cuda", bias=True,
+                     per_expert_decoders=True)
+    a, _ = hmoe.kmeans_assign(inp["X"], inp["C"])
+    dd = hmoe.moe_dispatch(a, K, rows=inp["X"])
+    rp = torch.as_tensor(inp["row_ptr"]).cuda()
+    tg = torch.as_tensor(inp["tag"]).cuda()
+    f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], rp, tg, save_logits=True)
+    g = hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, f["H1_sorted"],
+                          f["H"], f["lse"], logits=f["logits"])
+    torch.cuda.synchronize()
+    rt = RTOL["bf16"]
+    a_np = npi(a)
+    rs = np.random.default_rng(1)
+    pick = [3, 11]
+    rows = np.sort(np.concatenate([rs.choice(np.flatnonzero(a_np == e), 12, replace=False) for e in pick]))
+    ids = np.searchsorted(pick, a_np[rows]).astype(np.int32)
+    sel = torch.as_tensor(pick, dtype=torch.long, device="cuda")
+    ph = {k: np64(v[sel]) for k, v in p.items()}
+    Xs = np64(inp["X"][torch.as_tensor(rows, dtype=torch.long, device="cuda")])
+    cnt = inp["row_ptr"][1:] - inp["row_ptr"][:-1]
+    srp = np.concatenate([[0], np.cumsum(cnt[rows])]).astype(np.int32)
+    stg = np.concatenate([inp["tag"][inp["row_ptr"][i]:inp["row_ptr"][i + 1]] for i in rows]).astype(np.int32)
+    ref = O.moe_forward(Xs, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], srp, stg,
+                        store="bf16")
+    assert_close(np64(f["H"])[rows], ref["H"], rt, "H (sampled rows)")
+    assert_close(np64(f["lse"])[rows], ref["lse"], rt, "lse (sampled rows)")
+    assert_close(np64(f["loss"])[rows], ref["loss"], rt, "loss (sampled rows)")
+    gr = O.moe_backward(Xs, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], srp, stg, ref["H1"], ref["H"],
+                        ref["lse"], scale=1.0 / n, store="bf16", logit_round=True)
+    assert_close(np64(g["dX"])[rows], gr["dX"], rt, "dX (sampled rows)")
+    dbD = np64(g["dbD"])
+    assert np.all(np.abs(dbD.sum(axis=1)) <= 1e-3 * np.abs(dbD).sum(axis=1))
+    db2 = np64(g["db2"])
+    for e in range(K):
+        dDe = np64(g["dD"][e])
+        assert np.all(np.abs(dDe.sum(axis=0)) <= 1e-2 * np.abs(dDe).sum(axis=0) + 1e-12), e
+        assert_close(db2[e], np64(p["D"][e]).T @ dbD[e], rt, f"db2_{e} vs D_{e}^T dbD_{e}")
