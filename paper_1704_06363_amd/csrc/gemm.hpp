@@ -678,15 +678,29 @@ __device__ __forceinline__ TileCoord tile_plain(int64_t M, int N, int K) {
 // [seg[e], seg[e+1]) of A and C.  tile_start[e] = number of BM-row tiles of groups < e
 // (prefix, tile_start[G] = total).  Launched over an upper bound of m-tiles x n-tiles; the
 // excess workgroups find no tile and exit.
-template <class C>
+// XCD: workgroups go to the 8 XCDs round-robin (blockIdx.x % 8), each with its own L2; this
+// order gives each XCD a run of 8 consecutive m-tiles with all their n-tiles (of the
+// 64 nt workgroups b = 64 nt r + q: XCD x = q % 8 takes m-tile 64 r + 8 x + (q / 8) / nt,
+// n-tile (q / 8) % nt), so an XCD fetches each of its A row blocks once and the B tiles of
+// few groups.  The grid must then be a multiple of 64 nt (the m-tile bound rounded up to 64).
+template <class C, bool XCD = false>
 __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ seg,
                                                   const int32_t* __restrict__ tile_start, int G, int N,
                                                   int K) {
   TileCoord tc;
   const int nt = (int)cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
-  const int64_t mtile = b / nt;
-  const int ni = (int)(b - mtile * nt);
+  int64_t mtile;
+  int ni;
+  if constexpr (XCD) {
+    const int64_t r = b / (64 * nt), q = b - r * 64 * nt;
+    const int slot = (int)(q / 8);
+    mtile = r * 64 + (q % 8) * 8 + slot / nt;
+    ni = slot % nt;
+  } else {
+    mtile = b / nt;
+    ni = (int)(b - mtile * nt);
+  }
   tc.valid = false;
   const int total = tile_start[G];
   if (mtile >= total) return tc;

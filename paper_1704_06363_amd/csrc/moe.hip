@@ -741,7 +741,7 @@ struct ReluMask {
 // order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order (in slot order, row m, when
 // perm is NULL: the per-expert decoders' dH = g D_e).
 //   A: [rows][Kd] (ld Kd), W: [G][Kd][N] (the layer's [out][in] weights seen as [K][N]).
-template <class C, bool MASK>
+template <class C, bool MASK, bool XCD = false>
 __global__ void __launch_bounds__(C::THREADS)
     k_expert_dgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
                    const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
@@ -750,7 +750,7 @@ __global__ void __launch_bounds__(C::THREADS)
   using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
+  const TileCoord tc = tile_group_m<C, XCD>(seg, tile_start, G, N, Kd);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
@@ -906,9 +906,10 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
       HMOE_LAUNCH("decoder bias grad", k_piece_colsum, dim3((unsigned)cdiv(s.V, 256), (unsigned)s.K), dim3(256), 0,
                   st, pdb, gts, s.V, dbD);
     HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
-    HMOE_LAUNCH("decoder dH", (k_expert_dgrad<C, false>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
-                dim3(C::THREADS), C::LDS, st, (const T*)G, D, offsets, ts, s.K, s.o, s.V, (const T*)nullptr,
-                (const int32_t*)nullptr, dYs);
+    // XCD-grouped tile order: the o / BN tiles of an m-tile share one G row block (V wide)
+    HMOE_LAUNCH("decoder dH", (k_expert_dgrad<C, false, true>),
+                dim3((unsigned)(cdiv(mt_bound, 64) * 64 * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
+                (const T*)G, D, offsets, ts, s.K, s.o, s.V, (const T*)nullptr, (const int32_t*)nullptr, dYs);
     HMOE_LAUNCH("decoder dD", k_expert_wgrad<C>,
                 dim3((unsigned)((int64_t)s.K * cdiv(s.V, C::BM) * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
                 (const T*)G, (const T*)Hs, offsets, order, s.K, s.V, s.o, dD);
