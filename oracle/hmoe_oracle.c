@@ -519,3 +519,66 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
   free(dZ);
   return 0;
 }
+
+/* ------------------------------------------------ Section 4.4: t_m, p@m (Eq. 4), q@m (Eq. 5) */
+
+/* t_m: the indices of the m largest entries of each row of L [n x V], in decreasing order of
+ * value, equal values in increasing index order (the paper does not say how ties break).  Plain
+ * selection: m scans per row, each taking the largest entry not yet taken (strict ">" keeps
+ * the lowest index among equal values).  1 <= m <= V. */
+int hmoe_orc_topm(int64_t n, int32_t V, int32_t m, const double* L, int32_t* idx) {
+  if (n < 0 || V <= 0 || m <= 0 || m > V) return -1;
+  int bad = 0;
+#pragma omp parallel
+  {
+    char* taken = (char*)malloc((size_t)V);
+    if (!taken) {
+#pragma omp atomic write
+      bad = 1;
+    }
+#pragma omp for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+      if (!taken) continue;
+      const double* row = L + i * (int64_t)V;
+      memset(taken, 0, (size_t)V);
+      for (int32_t r = 0; r < m; ++r) {
+        int32_t best = -1;
+        for (int32_t v = 0; v < V; ++v)
+          if (!taken[v] && (best < 0 || row[v] > row[best])) best = v;
+        taken[best] = 1;
+        idx[i * (int64_t)m + r] = best;
+      }
+    }
+    free(taken);
+  }
+  return bad ? -2 : 0;
+}
+
+/* Counts behind Eq. 4 and Eq. 5 for every m' = 1..m, from the top-m lists idx [n x m]:
+ *   p_hits[m'-1] = sum_i |t_m'(i) ∩ P_i|, so p@m' = p_hits[m'-1] / sum_i |P_i|;
+ *   q_hits[m'-1] = number of the S given draws (q_sample[s], q_tag[s]) -- a tag drawn uniformly
+ *   from the dictionary, then an image carrying it -- whose tag is in t_m'(q_sample[s]),
+ *   so q@m' = q_hits[m'-1] / S. */
+int hmoe_orc_topm_hits(int64_t n, int32_t m, const int32_t* idx, const int32_t* row_ptr,
+                       const int32_t* tag, int64_t S, const int32_t* q_sample,
+                       const int32_t* q_tag, int64_t* p_hits, int64_t* q_hits) {
+  if (n < 0 || m <= 0 || S < 0) return -1;
+  for (int32_t r = 0; r < m; ++r) p_hits[r] = q_hits[r] = 0;
+  for (int64_t i = 0; i < n; ++i)
+    for (int32_t r = 0; r < m; ++r) {
+      const int32_t v = idx[i * (int64_t)m + r];
+      int in = 0;
+      for (int32_t q = row_ptr[i]; q < row_ptr[i + 1]; ++q)
+        if (tag[q] == v) in = 1;
+      if (in)
+        for (int32_t k = r; k < m; ++k) p_hits[k] += 1; /* in t_m' for every m' > r */
+    }
+  for (int64_t s = 0; s < S; ++s) {
+    const int64_t i = q_sample[s];
+    if (i < 0 || i >= n) return -3;
+    for (int32_t r = 0; r < m; ++r)
+      if (idx[i * (int64_t)m + r] == q_tag[s])
+        for (int32_t k = r; k < m; ++k) q_hits[k] += 1;
+  }
+  return 0;
+}

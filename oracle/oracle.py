@@ -237,3 +237,31 @@ def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
         _p(dW2), _p(db2), _p(dD), _p(dbD), _p(dX))
     _check(rc, "moe_backward")
     return {"dW1": dW1, "db1": db1, "dW2": dW2, "db2": db2, "dD": dD, "dbD": dbD, "dX": dX}
+
+
+def topm(L, m: int) -> np.ndarray:
+    """t_m (Section 4.4): indices of the m largest entries of each row, in decreasing order,
+    equal values by increasing index.  L is taken as given (pass the stored logits)."""
+    L = _f64(L)
+    n, V = L.shape
+    idx = np.empty((n, m), dtype=np.int32)
+    _check(_load().hmoe_orc_topm(ctypes.c_int64(n), ctypes.c_int32(V), ctypes.c_int32(m), _p(L),
+                                 _p(idx)), "topm")
+    return idx
+
+
+def topm_hits(idx, row_ptr, tag, q_sample, q_tag):
+    """Counts behind Eq. 4 (p@m) and Eq. 5 (q@m), Section 4.4, for every m' = 1..m of the
+    top-m lists idx [n, m]: p_hits[m'-1] = sum_i |t_m'(i) & P_i| and q_hits[m'-1] = number of
+    the given (sample, tag) draws whose tag is in the sample's t_m'.  p@m' = p_hits / nnz,
+    q@m' = q_hits / S."""
+    idx = _i32(idx)
+    n, m = idx.shape
+    row_ptr = _i32(row_ptr); tag = _i32(tag)
+    q_sample = _i32(q_sample); q_tag = _i32(q_tag)
+    S = q_sample.shape[0]
+    p_hits = np.zeros(m, dtype=np.int64); q_hits = np.zeros(m, dtype=np.int64)
+    _check(_load().hmoe_orc_topm_hits(ctypes.c_int64(n), ctypes.c_int32(m), _p(idx), _p(row_ptr),
+                                      _p(tag), ctypes.c_int64(S), _p(q_sample), _p(q_tag),
+                                      _p(p_hits), _p(q_hits)), "topm_hits")
+    return p_hits, q_hits

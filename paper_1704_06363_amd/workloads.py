@@ -148,6 +148,23 @@ def moe_params(K: int, d: int, h: int, o: int, V: int, seed: int, dtype: str = "
             "D": w(dec + (V, o), o), "bD": b(dec + (V,))}
 
 
+def q_draws(row_ptr, tag, S: int, seed: int):
+    """The S draws behind q@m (Section 4.4, Eq. 5): each picks a tag uniformly among the tags
+    that label at least one sample, then a sample uniformly among the samples it labels.
+    Returns (q_sample, q_tag) int32 arrays."""
+    row_ptr = np.asarray(row_ptr, dtype=np.int64)
+    tag = np.asarray(tag, dtype=np.int64)
+    n = row_ptr.shape[0] - 1
+    owner = np.repeat(np.arange(n), np.diff(row_ptr))
+    order = np.argsort(tag, kind="stable")
+    tags_sorted, owners = tag[order], owner[order]
+    present, first, count = np.unique(tags_sorted, return_index=True, return_counts=True)
+    rs = np.random.default_rng(seed)
+    pick = rs.integers(0, present.shape[0], S)
+    within = (rs.random(S) * count[pick]).astype(np.int64)
+    return (owners[first[pick] + within].astype(np.int32), present[pick].astype(np.int32))
+
+
 def zipf_bucket_ids(n: int, K: int, seed: int, s: float = 1.3,
                     forced_small=(0, 0, 1, 1, 2, 2, 3, 3)) -> np.ndarray:
     """Expert ids with bucket sizes following Zipf(s) over K ranks: size_r = round(n r^-s / H),
