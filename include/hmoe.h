@@ -180,6 +180,29 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                       float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* ------------------------------------------------------------------ inference tail */
+
+/* t_m (Section 4.4): for every row of logits [n x vocab] (dtype dt; e.g. as stored by
+ * hmoe_moe_forward -- the softmax keeps the order, so these are the m most probable tags), the
+ * indices of its m largest entries in decreasing order, equal values in increasing index
+ * order.  idx int32[n][m] out; val float[n][m] out or NULL (the entries at those indices).
+ * 1 <= m <= 16, m <= vocab; the entries are assumed finite.  One wave per row; the logits are
+ * read once.  Errors: HMOE_EINVAL (m out of range, NULL logits or idx), HMOE_ESHAPE (vocab
+ * not a multiple of 8). */
+int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m, int32_t* idx,
+              float* val, void* stream);
+
+/* The counts behind p@m (Eq. 4) and q@m (Eq. 5), Section 4.4, for every m' = 1..m, from the
+ * top-m lists idx int32[n][m] (hmoe_topm):
+ *   hits[m' - 1]     = sum_i |t_m'(i) ∩ P_i|, so p@m' = hits[m' - 1] / (number of positives);
+ *   hits[m + m' - 1] = number of the S draws (q_sample[s], q_tag[s]) whose tag is in
+ *                      t_m'(q_sample[s]), so q@m' = hits[m + m' - 1] / S.
+ * The draws (a tag uniformly from the dictionary, then a sample carrying it) are the caller's;
+ * a draw whose sample is outside [0, n) counts as a miss.  hits int64[2m] out (device);
+ * q_sample, q_tag int32[S] (device, NULL when S = 0).  1 <= m <= 16. */
+int hmoe_topm_hits(const int32_t* idx, int64_t n, int32_t m, const hmoe_labels_t* y, const int32_t* q_sample,
+                   const int32_t* q_tag, int64_t S, int64_t* hits, void* stream);
+
 /* ------------------------------------------------------------------ diagnostics */
 
 /* Launch timing for benchmarks, not part of the hot path.  While enabled, every kernel the

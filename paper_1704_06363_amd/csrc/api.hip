@@ -366,4 +366,38 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                              dD, dbD, dX, w, (hipStream_t)stream);
 }
 
+int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m, int32_t* idx, float* val,
+              void* stream) {
+  clear_error();
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_width("vocab", vocab));
+  if (m < 1 || m > 16 || m > vocab) return fail(HMOE_EINVAL, "m = %d outside [1, min(16, vocab)]", m);
+  if (n == 0) return HMOE_OK;
+  HMOE_TRY(check_ptr("logits", logits));
+  HMOE_TRY(check_ptr("idx", idx, false));
+  return launch_topm(logits, dt, n, vocab, m, idx, val, (hipStream_t)stream);
+}
+
+int hmoe_topm_hits(const int32_t* idx, int64_t n, int32_t m, const hmoe_labels_t* y, const int32_t* q_sample,
+                   const int32_t* q_tag, int64_t S, int64_t* hits, void* stream) {
+  clear_error();
+  HMOE_TRY(check_n(n));
+  if (m < 1 || m > 16) return fail(HMOE_EINVAL, "m = %d outside [1, 16]", m);
+  if (S < 0 || S >= (int64_t(1) << 31)) return fail(HMOE_EINVAL, "S = %lld outside [0, 2^31)", (long long)S);
+  HMOE_TRY(check_ptr("hits", hits, false));
+  if (n > 0) {
+    HMOE_TRY(check_ptr("idx", idx, false));
+    if (!y) return fail(HMOE_EINVAL, "labels are NULL");
+    HMOE_TRY(check_ptr("labels.row_ptr", y->row_ptr, false));
+    HMOE_TRY(check_ptr("labels.tag", y->tag, false));
+  }
+  if (S > 0) {
+    HMOE_TRY(check_ptr("q_sample", q_sample, false));
+    HMOE_TRY(check_ptr("q_tag", q_tag, false));
+  }
+  static const hmoe_labels_t none = {nullptr, nullptr};
+  return launch_topm_hits(idx, n, m, y ? y : &none, q_sample, q_tag, S, hits, (hipStream_t)stream);
+}
+
 }  // extern "C"

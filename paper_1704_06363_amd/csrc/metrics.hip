@@ -1,0 +1,159 @@
+// metrics.hip -- the inference tail of Section 4.4: t_m, the m largest logits of every row
+// (the softmax keeps their order, so these are the m most probable tags), and the counts
+// behind p@m (Eq. 4) and q@m (Eq. 5) for every m' <= m.
+//
+// k_topm: one wave per row.  Lane l reads the row's 16-byte vectors l, l + 64, ... (so it sees
+// its entries in increasing index order) and keeps its own M largest in a register list sorted
+// by decreasing value; an entry enters only when strictly greater than the list's last, which
+// with the index order keeps equal values in increasing index order.  The m results are then
+// taken in m rounds of a wave-wide (value desc, index asc) maximum over the lists' heads; the
+// lane holding the winner drops it.  The row is read once: the kernel is bound by HBM.
+//
+// k_topm_hits: one thread per row (p) and per draw (q); the rank of each matching tag in the
+// top-m list adds 1 to every m' above it.  Integer counts, summed through LDS and then with
+// one 64-bit atomic per block and m' -- integer sums, so the result does not depend on order.
+#include "launch.hpp"
+#include "primitives.hpp"
+
+namespace hmoe {
+
+template <typename T, int M>
+__global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n, int V, int m,
+                                              int32_t* __restrict__ idx, float* __restrict__ val) {
+  constexpr int EPV = 16 / sizeof(T);
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
+  if (row >= n) return;
+  float lv[M];
+  int li[M];
+#pragma unroll
+  for (int k = 0; k < M; ++k) {
+    lv[k] = -INFINITY;
+    li[k] = 0x7fffffff;
+  }
+  const T* r = L + row * (int64_t)V;
+  const int nvec = V / EPV;
+  for (int v = l; v < nvec; v += 64) {
+    const i32x4 raw = *reinterpret_cast<const i32x4*>(r + (int64_t)v * EPV);
+    const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+    for (int z = 0; z < EPV; ++z) {
+      float cv = to_f32(e[z]);
+      if (cv > lv[M - 1]) {
+        int ci = v * EPV + z;
+        // carry the entry down the list: it goes before the first strictly smaller one
+#pragma unroll
+        for (int k = 0; k < M; ++k) {
+          const bool gt = cv > lv[k];
+          const float tv = lv[k];
+          const int ti = li[k];
+          lv[k] = gt ? cv : tv;
+          li[k] = gt ? ci : ti;
+          cv = gt ? tv : cv;
+          ci = gt ? ti : ci;
+        }
+      }
+    }
+  }
+  for (int q = 0; q < m; ++q) {
+    float bv = lv[0];
+    int bi = li[0];
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+      const float ov = shfl_xor(bv, s);
+      const int oi = shfl_xor(bi, s);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    if (li[0] == bi) {  // this lane's head won: drop it
+#pragma unroll
+      for (int k = 0; k < M - 1; ++k) {
+        lv[k] = lv[k + 1];
+        li[k] = li[k + 1];
+      }
+      lv[M - 1] = -INFINITY;
+      li[M - 1] = 0x7fffffff;
+    }
+    if (l == 0) {
+      idx[row * (int64_t)m + q] = bi;
+      if (val) val[row * (int64_t)m + q] = bv;
+    }
+  }
+}
+
+// hits[0 .. m) for p, hits[m .. 2m) for q; must start at zero.
+__global__ void __launch_bounds__(256) k_topm_hits(const int32_t* __restrict__ idx, int64_t n, int m,
+                                                   const int32_t* __restrict__ row_ptr,
+                                                   const int32_t* __restrict__ tag,
+                                                   const int32_t* __restrict__ q_sample,
+                                                   const int32_t* __restrict__ q_tag, int64_t S,
+                                                   unsigned long long* __restrict__ hits) {
+  __shared__ unsigned int cnt[2 * 16];
+  if (threadIdx.x < 2 * 16) cnt[threadIdx.x] = 0u;
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t < n) {
+    const int32_t* top = idx + t * (int64_t)m;
+    for (int32_t q = row_ptr[t]; q < row_ptr[t + 1]; ++q) {
+      const int32_t tg = tag[q];
+      for (int k = 0; k < m; ++k)
+        if (top[k] == tg) {
+          atomicAdd(&cnt[k], 1u);  // counted for every m' > k below
+          break;
+        }
+    }
+  } else if (t - n < S) {
+    const int64_t s = t - n;
+    const int32_t i = q_sample[s];
+    if (i >= 0 && i < n) {  // a draw naming no sample counts as a miss
+      const int32_t* top = idx + (int64_t)i * m;
+      const int32_t tg = q_tag[s];
+      for (int k = 0; k < m; ++k)
+        if (top[k] == tg) {
+          atomicAdd(&cnt[16 + k], 1u);
+          break;
+        }
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < m) {
+    // the entry at rank k is in t_m' for every m' > k: prefix over the ranks
+    unsigned long long p = 0, qh = 0;
+    for (int k = 0; k <= (int)threadIdx.x; ++k) {
+      p += cnt[k];
+      qh += cnt[16 + k];
+    }
+    if (p) atomicAdd(&hits[threadIdx.x], p);
+    if (qh) atomicAdd(&hits[m + threadIdx.x], qh);
+  }
+}
+
+template <typename T>
+static int topm_t(const T* L, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
+  const dim3 grid((unsigned)cdiv(n, 4));
+  if (m <= 4)
+    HMOE_LAUNCH("top-m", (k_topm<T, 4>), grid, dim3(256), 0, st, L, n, V, m, idx, val);
+  else if (m <= 8)
+    HMOE_LAUNCH("top-m", (k_topm<T, 8>), grid, dim3(256), 0, st, L, n, V, m, idx, val);
+  else
+    HMOE_LAUNCH("top-m", (k_topm<T, 16>), grid, dim3(256), 0, st, L, n, V, m, idx, val);
+  return HMOE_OK;
+}
+
+int launch_topm(const void* L, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
+  if (dt == HMOE_BF16) return topm_t<bf16>((const bf16*)L, n, V, m, idx, val, st);
+  return topm_t<float>((const float*)L, n, V, m, idx, val, st);
+}
+
+int launch_topm_hits(const int32_t* idx, int64_t n, int m, const hmoe_labels_t* y, const int32_t* q_sample,
+                     const int32_t* q_tag, int64_t S, int64_t* hits, hipStream_t st) {
+  HMOE_TRY(launch_zero_f32((float*)hits, 4 * (int64_t)m, st));  // 2m int64 = 4m zero words
+  if (n + S == 0) return HMOE_OK;
+  HMOE_LAUNCH("top-m hits", k_topm_hits, dim3((unsigned)cdiv(n + S, 256)), dim3(256), 0, st, idx, n, m, y->row_ptr,
+              y->tag, q_sample, q_tag, S, (unsigned long long*)hits);
+  return HMOE_OK;
+}
+
+}  // namespace hmoe

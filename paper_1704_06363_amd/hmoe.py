@@ -26,6 +26,7 @@ SYMBOLS = (
     "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
     "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
     "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
+    "hmoe_topm", "hmoe_topm_hits",
     "hmoe_timer_enable", "hmoe_timer_report",
 )
 
@@ -83,13 +84,15 @@ def lib():
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                         _P, _P, _P, _SZ, _P]
+        L.hmoe_topm.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _P, _P, _P]
+        L.hmoe_topm_hits.argtypes = [_P, _I64, _I32, _c.POINTER(Labels), _P, _P, _I64, _P, _P]
         L.hmoe_timer_enable.argtypes = [_c.c_int]
         L.hmoe_timer_enable.restype = _c.c_int
         L.hmoe_timer_report.argtypes = [_c.c_char_p, _SZ]
         L.hmoe_timer_report.restype = _I64
         for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
                      "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
-                     "hmoe_moe_backward"):
+                     "hmoe_moe_backward", "hmoe_topm", "hmoe_topm_hits"):
             getattr(L, name).restype = _c.c_int
         _lib = L
     return _lib
@@ -338,3 +341,30 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
                                  _ptr(g["dD"]), _ptr(g["dbD"]), _ptr(g["dX"]), _ptr(w), wb,
                                  _stream()), "moe_backward")
     return g
+
+
+# ------------------------------------------------------------------ inference tail
+
+def topm(logits, m: int, out=None, want_values=False):
+    """t_m (Section 4.4): the indices [n, m] of each row's m largest logits, decreasing, equal
+    values by increasing index (and their values, fp32, with want_values)."""
+    n, V = logits.shape
+    dev = logits.device
+    o = out or {}
+    idx = o.get("idx", torch.empty(n, m, dtype=torch.int32, device=dev))
+    val = o.get("val", torch.empty(n, m, dtype=torch.float32, device=dev)) if want_values else None
+    _chk(lib().hmoe_topm(_ptr(logits), _dt(logits), n, V, m, _ptr(idx), _ptr(val), _stream()), "topm")
+    return (idx, val) if want_values else idx
+
+
+def topm_hits(idx, row_ptr, tag, q_sample=None, q_tag=None, out=None):
+    """Counts behind p@m' (Eq. 4) and q@m' (Eq. 5) for m' = 1..m: an int64 tensor [2, m] with
+    row 0 = sum_i |t_m'(i) & P_i| and row 1 = the draws (q_sample, q_tag) whose tag is in the
+    sample's t_m'."""
+    n, m = idx.shape
+    S = 0 if q_sample is None else q_sample.shape[0]
+    hits = out if out is not None else torch.empty(2, m, dtype=torch.int64, device=idx.device)
+    lab = Labels(_ptr(row_ptr), _ptr(tag))
+    _chk(lib().hmoe_topm_hits(_ptr(idx), n, m, ctypes.byref(lab), _ptr(q_sample), _ptr(q_tag), S, _ptr(hits),
+                              _stream()), "topm_hits")
+    return hits

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 16
+    assert len(names) == 18
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(hmoe.SYMBOLS)
@@ -78,6 +78,18 @@ def test_argument_errors_are_reported_before_launch(lib):
     # update with an unknown mode
     rc = lib.hmoe_kmeans_update(16, 0, 10, 16, 3, 16, 16, 16, 16, 16, 9, 0, None, 0, None)
     assert rc == -1 and "mode" in hmoe.last_error()
+    # a decoder count that is neither 1 nor K
+    p = hmoe.MoeParams(4, 64, 128, 64, 1000, 0, 16, None, 16, None, 16, None, 3)
+    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, 16,
+                              16, 16, None, 0, None)
+    assert rc == -1 and "decoders" in hmoe.last_error()
+    # top-m: m outside [1, 16], and a vocabulary that is not a multiple of 8
+    rc = lib.hmoe_topm(16, 1, 10, 64, 17, 16, None, None)
+    assert rc == -1 and "m = 17" in hmoe.last_error()
+    rc = lib.hmoe_topm(16, 1, 10, 60, 5, 16, None, None)
+    assert rc == -3 and "vocab" in hmoe.last_error()
+    rc = lib.hmoe_topm_hits(16, 10, 0, ctypes.byref(lab), None, None, 0, 16, None)
+    assert rc == -1 and "m = 0" in hmoe.last_error()
 
 
 def test_binding_refuses_host_tensors(lib):

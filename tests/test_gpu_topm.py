@@ -1,0 +1,97 @@
+"""The inference tail (Section 4.4) on the HIP path against the oracle: t_m per row, bit-exact
+indices on the same logits (including forced ties, fp32 and bf16, small and 50,000-wide
+vocabularies, m = 1 .. 16 and the full ranking), the counts behind p@m (Eq. 4) and q@m
+(Eq. 5), and the whole inference path (forward, then t_m and the counts) against the oracle's
+own forward, exempting rows whose m-th and (m+1)-th logits are closer than the two sides'
+rounding."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_1704_06363_amd import hmoe
+from paper_1704_06363_amd import workloads as W
+from tests.parity import np64, npi
+
+pytestmark = pytest.mark.gpu
+
+
+def _logits(n, V, dtype, seed, ties):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    if ties:  # small integers: many exact ties per row
+        L = torch.randint(-8, 9, (n, V), generator=g).float()
+    else:
+        L = torch.randn(n, V, generator=g) * 3.0
+    return L.to(torch.bfloat16 if dtype == "bf16" else torch.float32).cuda()
+
+
+@pytest.mark.parametrize("dtype,n,V,m,ties", [
+    ("bf16", 1000, 1000, 10, True), ("bf16", 999, 1000, 5, False), ("f32", 777, 520, 16, True),
+    ("f32", 300, 64, 1, False), ("bf16", 64, 8, 8, False), ("bf16", 50, 50000, 10, False),
+    ("bf16", 37, 50000, 16, True)])
+def test_topm_bit_exact(dtype, n, V, m, ties):
+    L = _logits(n, V, dtype, seed=n + V + m, ties=ties)
+    idx, val = hmoe.topm(L, m, want_values=True)
+    ref = O.topm(np64(L), m)
+    assert np.array_equal(npi(idx), ref)
+    np.testing.assert_array_equal(np64(val), np.take_along_axis(np64(L), ref.astype(np.int64), axis=1))
+
+
+def test_hits_exact():
+    n, V, m = 3000, 2000, 10
+    L = _logits(n, V, "bf16", seed=5, ties=False)
+    rp, tg = W.zipf_labels(n, V, 8, seed=6)
+    qs, qt = W.q_draws(rp, tg, 100000, seed=7)
+    idx = hmoe.topm(L, m)
+    dev = lambda a: torch.as_tensor(a).cuda()  # noqa: E731
+    hits = hmoe.topm_hits(idx, dev(rp), dev(tg), dev(qs), dev(qt))
+    p_ref, q_ref = O.topm_hits(O.topm(np64(L), m), rp, tg, qs, qt)
+    assert npi(hits[0]).tolist() == p_ref.tolist()
+    assert npi(hits[1]).tolist() == q_ref.tolist()
+    # no draws, and draws naming no sample
+    h0 = hmoe.topm_hits(idx, dev(rp), dev(tg))
+    assert npi(h0[0]).tolist() == p_ref.tolist() and int(npi(h0[1]).sum()) == 0
+    bad = hmoe.topm_hits(idx, dev(rp), dev(tg), dev(np.array([-1, n], np.int32)), dev(np.array([0, 0], np.int32)))
+    assert int(npi(bad[1]).sum()) == 0
+
+
+def test_inference_path_against_the_oracle():
+    """Forward, then t_10 and the counts.  fp32 (the tiny workload): the lists equal the
+    oracle's except on rows with two consecutive ranks closer than 1e-5 (relative).  bf16 (a
+    balanced-shape miniature): the stored bf16 logits of a row's top ranks are often equal or
+    one rounding apart, so instead every chosen tag must be within two bf16 roundings of the
+    oracle's 10th largest logit, and p@m, q@m must agree with the oracle's to 1%."""
+    m = 10
+    for store, inp in (("f32", W.tiny_inputs(device="cuda", seed=0)),
+                       ("bf16", W.balanced_inputs(device="cuda", seed=3, n=2000, d=256, h=512, o=128,
+                                                  V=1000, K=4))):
+        p = inp["params"]
+        n = inp["X"].shape[0]
+        K = p["W1"].shape[0]
+        ids = np.random.default_rng(1).integers(0, K, n).astype(np.int32)
+        dd = hmoe.moe_dispatch(torch.as_tensor(ids).cuda(), K, rows=inp["X"])
+        rp, tg = inp["row_ptr"], inp["tag"]
+        dev = lambda a: torch.as_tensor(a).cuda()  # noqa: E731
+        f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dev(rp), dev(tg), save_logits=True)
+        idx = npi(hmoe.topm(f["logits"], m))
+        ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
+        ref = O.moe_forward(np64(inp["X"]), ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
+                            store=store, want_logits=True)
+        Lr = ref["logits"]
+        top_ref = O.topm(Lr, m + 1)
+        srt = np.take_along_axis(Lr, top_ref.astype(np.int64), axis=1)
+        qs, qt = W.q_draws(rp, tg, 20000, seed=9)
+        hits = npi(hmoe.topm_hits(dev(idx), dev(rp), dev(tg), dev(qs), dev(qt)))
+        p_ref, q_ref = O.topm_hits(top_ref[:, :m], rp, tg, qs, qt)
+        if store == "f32":
+            gap = srt[:, :-1] - srt[:, 1:]
+            near = np.any(gap <= 1e-5 * np.maximum(np.abs(srt[:, :-1]), 1.0), axis=1)
+            assert near.mean() < 0.05
+            assert np.array_equal(idx[~near], top_ref[~near, :m])
+            assert np.all(np.abs(hits[0] - p_ref) <= near.sum() * m)
+        else:
+            chosen = np.take_along_axis(Lr, idx.astype(np.int64), axis=1)
+            tenth = srt[:, m - 1:m]
+            assert np.all(chosen >= tenth - 2 * 2.0 ** -7 * np.maximum(np.abs(tenth), 1.0))
+            assert np.all(np.abs(hits[0] - p_ref) <= 0.01 * rp[-1])
+            assert np.all(np.abs(hits[1] - q_ref) <= 0.01 * len(qs))
