@@ -11,8 +11,9 @@ Printed: one JSON line with the step throughput (samples/s), the roofline of the
 kernel (HIP events recorded around every launch in the timed region), the fp64 CPU oracle
 timed on a bounded sample of the same workload, and extra legs for the gater fit
 (2^20 fp32 rows, K = 64, 20 Lloyd iterations), the skewed routing step (K = 128, V = 100k),
-the balanced step with one decoder per expert (the independent-decoder model) and the large
-streamed assignment (2^24 bf16 rows, K = 1024).
+the balanced step with one decoder per expert (the independent-decoder model), inference on
+the balanced batch (forward, top-10 tags per row, p@m / q@m counts) and the large streamed
+assignment (2^24 bf16 rows, K = 1024).
 """
 from __future__ import annotations
 
@@ -154,7 +155,7 @@ class RoutedStep:
                    hmoe.kmeans_assign_workspace(n, d, K, bf))
         self.ws = torch.empty(need, dtype=torch.uint8, device=dev)
 
-    def run(self):
+    def run(self, backward=True):
         h, p = self.h, self.inp["params"]
         if self.routed_by_gater:
             h.kmeans_assign(self.X, self.C, assign=self.ids, min_dist=self.md, ws=self.ws)
@@ -162,6 +163,8 @@ class RoutedStep:
         dd = self.disp
         f = h.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], self.row_ptr, self.tag,
                           out=self.fwd, ws=self.ws)
+        if not backward:
+            return
         h.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], self.row_ptr,
                        self.tag, f["H1_sorted"], f["H"], f["lse"], out=self.grads, ws=self.ws,
                        logits=f["logits"])
@@ -326,6 +329,43 @@ def leg_independent(steps, warmup):
     return out
 
 
+def leg_inference(steps, warmup, m=10, draws=100000):
+    """Inference on the balanced batch (Section 4.4): gater assignment, dispatch, the forward
+    with the logits stored, then t_m of every row and the counts behind p@m and q@m."""
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    inp = W.balanced_inputs(device="cuda", seed=0)
+    s = inp["shape"]
+    st = RoutedStep(inp, routed_by_gater=True)
+    qs, qt = W.q_draws(inp["row_ptr"], inp["tag"], draws, seed=1)
+    qs, qt = torch.as_tensor(qs).cuda(), torch.as_tensor(qt).cuda()
+    idx = torch.empty(s["n"], m, dtype=torch.int32, device="cuda")
+    hits = torch.empty(2, m, dtype=torch.int64, device="cuda")
+
+    def run():
+        st.run(backward=False)
+        hmoe.topm(st.fwd["logits"], m, out={"idx": idx})
+        hmoe.topm_hits(idx, st.row_ptr, st.tag, qs, qt, out=hits)
+
+    ms, rp = time_steps(run, steps, warmup)
+    k = kernel_table(rp, gemm_flops(s), PEAK_BF16_TFLOPS, steps)
+    tk = k.get("top-m", {}).get("avg_ms", float("nan"))
+    nnz = int(inp["row_ptr"][-1])
+    h = hits.cpu().numpy()
+    out = {"workload": f"inference: balanced batch (n=65536, V=50000) forward with stored bf16 logits, "
+                       f"then top-{m} per row and p@m / q@m counts ({draws} q draws)",
+           "samples_per_s": round(s["n"] / (ms * 1e-3), 1), "ms_per_batch": round(ms, 3),
+           "topm_ms": round(tk, 4),
+           "topm_frac_hbm_peak": round(s["n"] * s["V"] * 2 / (tk * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "p_at_m": [round(float(x) / nnz, 6) for x in h[0]],
+           "q_at_m": [round(float(x) / draws, 6) for x in h[1]],
+           "kernels": k}
+    del st, inp
+    torch.cuda.empty_cache()
+    return out
+
+
 def leg_large_assign(n_chunks):
     import torch
     from paper_1704_06363_amd import hmoe
@@ -382,7 +422,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-legs", action="store_true", help="skip the gater/skewed/independent/large legs")
+    ap.add_argument("--no-legs", action="store_true", help="skip the extra legs (gater fit, skewed, independent decoders, inference, large assign)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
@@ -456,6 +496,8 @@ def main():
         legs["skewed"] = leg_skewed(steps=max(2, args.steps // 2), warmup=1)
         log("leg: independent decoders")
         legs["independent"] = leg_independent(steps=max(2, args.steps // 2), warmup=1)
+        log("leg: inference tail")
+        legs["inference"] = leg_inference(steps=max(2, args.steps // 2), warmup=1)
         log("leg: large assign")
         legs["large_assign"] = leg_large_assign(args.large_chunks)
         res["legs"] = legs

@@ -5,7 +5,9 @@
 // k_topm: one wave per row.  Lane l reads the row's 16-byte vectors l, l + 64, ... (so it sees
 // its entries in increasing index order) and keeps its own M largest in a register list sorted
 // by decreasing value; an entry enters only when strictly greater than the list's last, which
-// with the index order keeps equal values in increasing index order.  The m results are then
+// with the index order keeps equal values in increasing index order, and only when it is not
+// below a wave-wide bound on the row's m-th value (the m-th largest of the lanes' maxima).
+// The m results are then
 // taken in m rounds of a wave-wide (value desc, index asc) maximum over the lists' heads; the
 // lane holding the winner drops it.  The row is read once: the kernel is bound by HBM.
 //
@@ -33,27 +35,65 @@ __global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n
   }
   const T* r = L + row * (int64_t)V;
   const int nvec = V / EPV;
-  for (int v = l; v < nvec; v += 64) {
-    const i32x4 raw = *reinterpret_cast<const i32x4*>(r + (int64_t)v * EPV);
-    const T* e = reinterpret_cast<const T*>(&raw);
+  // Wave-wide lower bound on the row's m-th largest value (the m-th largest of the lanes'
+  // maxima: m entries are at least that large), so an entry below thr is not in t_m (entries
+  // equal to it may be, and stay).  It closes in on the m-th value within a few steps, which
+  // keeps the insertion branch -- taken by the wave when any lane takes it -- rare.
+  float thr = -INFINITY;
+  constexpr int U = 4;  // vectors in flight per lane
+  // the trip count is the same for every lane (the bound is a wave-wide shuffle reduction)
+  int step = 0;
+  for (int b0 = 0; b0 < nvec; b0 += 64 * U, ++step) {
+    i32x4 raw[U];
 #pragma unroll
-    for (int z = 0; z < EPV; ++z) {
-      float cv = to_f32(e[z]);
-      if (cv > lv[M - 1]) {
-        int ci = v * EPV + z;
-        // carry the entry down the list: it goes before the first strictly smaller one
+    for (int u = 0; u < U; ++u) {
+      const int v = b0 + 64 * u + l;
+      if (v < nvec) raw[u] = *reinterpret_cast<const i32x4*>(r + (int64_t)v * EPV);
+    }
 #pragma unroll
-        for (int k = 0; k < M; ++k) {
-          const bool gt = cv > lv[k];
-          const float tv = lv[k];
-          const int ti = li[k];
-          lv[k] = gt ? cv : tv;
-          li[k] = gt ? ci : ti;
-          cv = gt ? tv : cv;
-          ci = gt ? ti : ci;
+    for (int u = 0; u < U; ++u) {
+      const int v = b0 + 64 * u + l;
+      if (v >= nvec) break;
+      const T* e = reinterpret_cast<const T*>(&raw[u]);
+      float f[EPV];
+      float vmax = -INFINITY;
+#pragma unroll
+      for (int z = 0; z < EPV; ++z) {
+        f[z] = to_f32(e[z]);
+        vmax = fmaxf(vmax, f[z]);
+      }
+      if (!(vmax >= thr && vmax > lv[M - 1])) continue;  // the common case: nothing here enters
+#pragma unroll
+      for (int z = 0; z < EPV; ++z) {
+        float cv = f[z];
+        if (cv >= thr && cv > lv[M - 1]) {
+          int ci = v * EPV + z;
+          // carry the entry down the list: it goes before the first strictly smaller one
+#pragma unroll
+          for (int k = 0; k < M; ++k) {
+            const bool gt = cv > lv[k];
+            const float tv = lv[k];
+            const int ti = li[k];
+            lv[k] = gt ? cv : tv;
+            li[k] = gt ? ci : ti;
+            cv = gt ? tv : cv;
+            ci = gt ? ti : ci;
+          }
         }
       }
     }
+    // the m-th largest of the lanes' maxima: m lanes each hold an entry at least that large
+    // (refreshed on the first steps, then every 4th: it settles quickly, and any value it
+    // took is a valid bound)
+    if (step >= 4 && (step & 3) != 0) continue;
+    float x = lv[0];
+    float t = -INFINITY;
+    for (int q = 0; q < m; ++q) {
+      t = wave_max(x);
+      const uint64_t hit = __ballot(x == t);
+      if (l == __ffsll((unsigned long long)hit) - 1) x = -INFINITY;  // drop one holder
+    }
+    thr = t;
   }
   for (int q = 0; q < m; ++q) {
     float bv = lv[0];
