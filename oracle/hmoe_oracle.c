@@ -582,3 +582,23 @@ int hmoe_orc_topm_hits(int64_t n, int32_t m, const int32_t* idx, const int32_t* 
   }
   return 0;
 }
+
+/* ----------------------------------------------------------- Section 4.2: SGD update */
+
+/* One SGD step on count parameters (Section 4.2: weight decay; momentum for the trunk, none
+ * for the experts): g' = g + weight_decay * w; with momentum > 0, v = momentum * v + g' and
+ * w = w - lr * v; otherwise w = w - lr * g'.  v may be NULL when momentum = 0. */
+int hmoe_orc_sgd_step(int64_t count, double* w, const double* g, double* v, double lr,
+                      double weight_decay, double momentum) {
+  if (count < 0 || (momentum > 0.0 && !v)) return -1;
+  for (int64_t i = 0; i < count; ++i) {
+    const double gd = g[i] + weight_decay * w[i];
+    if (momentum > 0.0) {
+      v[i] = momentum * v[i] + gd;
+      w[i] = w[i] - lr * v[i];
+    } else {
+      w[i] = w[i] - lr * gd;
+    }
+  }
+  return 0;
+}

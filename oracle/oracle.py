@@ -265,3 +265,19 @@ def topm_hits(idx, row_ptr, tag, q_sample, q_tag):
                                       _p(tag), ctypes.c_int64(S), _p(q_sample), _p(q_tag),
                                       _p(p_hits), _p(q_hits)), "topm_hits")
     return p_hits, q_hits
+
+
+def sgd_step(w, g, lr: float, weight_decay: float = 0.0, momentum: float = 0.0, v=None):
+    """One SGD step (Section 4.2: weight decay; momentum for the trunk, none for the experts).
+    Returns the new weights (and the new momentum buffer when momentum > 0); inputs untouched."""
+    w = _f64(w).copy()
+    shape = w.shape
+    w = w.reshape(-1)
+    g = _f64(g).reshape(-1)
+    vv = None
+    if momentum > 0.0:
+        vv = (np.zeros_like(w) if v is None else _f64(v).reshape(-1).copy())
+    _check(_load().hmoe_orc_sgd_step(ctypes.c_int64(w.shape[0]), _p(w), _p(g), _p(vv),
+                                     ctypes.c_double(lr), ctypes.c_double(weight_decay),
+                                     ctypes.c_double(momentum)), "sgd_step")
+    return (w.reshape(shape), vv.reshape(shape)) if momentum > 0.0 else w.reshape(shape)
