@@ -12,8 +12,8 @@ kernel (HIP events recorded around every launch in the timed region), the fp64 C
 timed on a bounded sample of the same workload, and extra legs for the gater fit
 (2^20 fp32 rows, K = 64, 20 Lloyd iterations), the skewed routing step (K = 128, V = 100k),
 the balanced step with one decoder per expert (the independent-decoder model), inference on
-the balanced batch (forward, top-10 tags per row, p@m / q@m counts) and the large streamed
-assignment (2^24 bf16 rows, K = 1024).
+the balanced batch (forward, top-10 tags per row, p@m / q@m counts), the SGD update of the
+balanced model's parameters and the large streamed assignment (2^24 bf16 rows, K = 1024).
 """
 from __future__ import annotations
 
@@ -366,6 +366,34 @@ def leg_inference(steps, warmup, m=10, draws=100000):
     return out
 
 
+def leg_sgd_update(steps, warmup):
+    """One SGD step (Section 4.2: weight decay 1e-4, no momentum for the experts and the
+    decoder) over every parameter of the balanced model, fp32 master weights, writing the bf16
+    copies the next forward reads."""
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    c = W.CONFIGS["balanced"]
+    p = W.moe_params(c.K, c.d, c.h, c.o, c.V, seed=20, dtype="bf16", device="cuda", bias=True)
+    master = {k: v.float() for k, v in p.items()}
+    grads = {k: torch.randn_like(v) * 1e-3 for k, v in master.items()}
+
+    def run():
+        for k in p:
+            hmoe.sgd_step(master[k], grads[k], lr=0.1, weight_decay=1e-4, w_lo=p[k])
+
+    ms, rep = time_steps(run, steps, warmup)
+    count = sum(v.numel() for v in master.values())
+    out = {"workload": f"SGD step (weight decay, no momentum) over the balanced model's {count} expert and "
+                       "decoder parameters, fp32 master weights plus bf16 copies",
+           "ms_per_update": round(ms, 3),
+           "frac_hbm_peak": round(count * 14 / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "kernels": kernel_table(rep, {}, PEAK_BF16_TFLOPS, steps)}
+    del p, master, grads
+    torch.cuda.empty_cache()
+    return out
+
+
 def leg_large_assign(n_chunks):
     import torch
     from paper_1704_06363_amd import hmoe
@@ -422,7 +450,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-legs", action="store_true", help="skip the extra legs (gater fit, skewed, independent decoders, inference, large assign)")
+    ap.add_argument("--no-legs", action="store_true", help="skip the extra legs (gater fit, skewed, independent decoders, inference, SGD update, large assign)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
@@ -498,6 +526,8 @@ def main():
         legs["independent"] = leg_independent(steps=max(2, args.steps // 2), warmup=1)
         log("leg: inference tail")
         legs["inference"] = leg_inference(steps=max(2, args.steps // 2), warmup=1)
+        log("leg: sgd update")
+        legs["sgd_update"] = leg_sgd_update(steps=max(2, args.steps // 2), warmup=1)
         log("leg: large assign")
         legs["large_assign"] = leg_large_assign(args.large_chunks)
         res["legs"] = legs

@@ -180,6 +180,21 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                       float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* ------------------------------------------------------------------ parameter update */
+
+/* One SGD step (Section 4.2: weight decay; the experts -- and the decoder trained with them --
+ * without momentum, the trunk with momentum).  For each of count elements:
+ *   g' = g + weight_decay * w;  momentum > 0: v = momentum * v + g', w = w - lr * v;
+ *   otherwise w = w - lr * g'   (fp32 arithmetic).
+ * w float[count] in/out: the fp32 master weights; g float[count]: the gradient (as written by
+ * hmoe_moe_backward); v float[count] in/out, the momentum buffer, or NULL when momentum == 0;
+ * w_lo [count] out in dtype dt (the updated weights rounded to nearest even, for the next
+ * forward) or NULL.  Device pointers, 16-byte aligned; w_lo must not overlap w.  One fused
+ * pass, bound by HBM.  Errors: HMOE_EINVAL (NULL w or g, negative count or hyperparameter,
+ * momentum > 0 without v), HMOE_ESHAPE (misaligned pointer), HMOE_EDTYPE. */
+int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t dt, int64_t count, float lr,
+                  float weight_decay, float momentum, void* stream);
+
 /* ------------------------------------------------------------------ inference tail */
 
 /* t_m (Section 4.4): for every row of logits [n x vocab] (dtype dt; e.g. as stored by

@@ -366,6 +366,22 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                              dD, dbD, dX, w, (hipStream_t)stream);
 }
 
+int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t dt, int64_t count, float lr,
+                  float weight_decay, float momentum, void* stream) {
+  clear_error();
+  HMOE_TRY(check_dtype(dt));
+  if (count < 0) return fail(HMOE_EINVAL, "count = %lld is negative", (long long)count);
+  if (!(lr >= 0.f) || !(weight_decay >= 0.f) || !(momentum >= 0.f))
+    return fail(HMOE_EINVAL, "lr, weight_decay and momentum must be >= 0");
+  if (count == 0) return HMOE_OK;
+  HMOE_TRY(check_ptr("w", w));
+  HMOE_TRY(check_ptr("g", g));
+  if (momentum > 0.f) HMOE_TRY(check_ptr("v (momentum buffer)", v));
+  if (w_lo) HMOE_TRY(check_ptr("w_lo", w_lo));
+  return launch_sgd(w, g, momentum > 0.f ? v : nullptr, w_lo, dt, count, lr, weight_decay, momentum,
+                    (hipStream_t)stream);
+}
+
 int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m, int32_t* idx, float* val,
               void* stream) {
   clear_error();

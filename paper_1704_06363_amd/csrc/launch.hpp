@@ -15,6 +15,8 @@ int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, i
                    hmoe_dtype_t dt, hipStream_t st);
 int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st);
 int launch_seg_order(const int32_t* seg, int G, int32_t* order, hipStream_t st);
+int launch_sgd(float* w, const float* g, float* v, void* wlo, hmoe_dtype_t dt, int64_t count, float lr, float wd,
+               float mu, hipStream_t st);
 int launch_topm(const void* L, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st);
 int launch_topm_hits(const int32_t* idx, int64_t n, int m, const hmoe_labels_t* y, const int32_t* q_sample,
                      const int32_t* q_tag, int64_t S, int64_t* hits, hipStream_t st);

@@ -26,7 +26,7 @@ SYMBOLS = (
     "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
     "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
     "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
-    "hmoe_topm", "hmoe_topm_hits",
+    "hmoe_sgd_step", "hmoe_topm", "hmoe_topm_hits",
     "hmoe_timer_enable", "hmoe_timer_report",
 )
 
@@ -84,6 +84,7 @@ def lib():
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                         _P, _P, _P, _SZ, _P]
+        L.hmoe_sgd_step.argtypes = [_P, _P, _P, _P, _c.c_int, _I64, _c.c_float, _c.c_float, _c.c_float, _P]
         L.hmoe_topm.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _P, _P, _P]
         L.hmoe_topm_hits.argtypes = [_P, _I64, _I32, _c.POINTER(Labels), _P, _P, _I64, _P, _P]
         L.hmoe_timer_enable.argtypes = [_c.c_int]
@@ -92,7 +93,7 @@ def lib():
         L.hmoe_timer_report.restype = _I64
         for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
                      "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
-                     "hmoe_moe_backward", "hmoe_topm", "hmoe_topm_hits"):
+                     "hmoe_moe_backward", "hmoe_sgd_step", "hmoe_topm", "hmoe_topm_hits"):
             getattr(L, name).restype = _c.c_int
         _lib = L
     return _lib
@@ -368,3 +369,17 @@ def topm_hits(idx, row_ptr, tag, q_sample=None, q_tag=None, out=None):
     _chk(lib().hmoe_topm_hits(_ptr(idx), n, m, ctypes.byref(lab), _ptr(q_sample), _ptr(q_tag), S, _ptr(hits),
                               _stream()), "topm_hits")
     return hits
+
+
+# ------------------------------------------------------------------ parameter update
+
+def sgd_step(w, g, lr: float, weight_decay: float = 0.0, momentum: float = 0.0, v=None, w_lo=None):
+    """One SGD step in place on the fp32 master weights w (Section 4.2); v is the momentum
+    buffer (required when momentum > 0); w_lo, if given, receives the updated weights in its
+    dtype (bf16 or fp32)."""
+    if w.dtype != torch.float32 or g.dtype != torch.float32 or g.numel() != w.numel():
+        raise HmoeError("sgd_step needs fp32 w and g of the same size")
+    dt = _dt(w_lo) if w_lo is not None else 1
+    _chk(lib().hmoe_sgd_step(_ptr(w), _ptr(g), _ptr(v), _ptr(w_lo), dt, w.numel(), lr, weight_decay, momentum,
+                             _stream()), "sgd_step")
+    return w
