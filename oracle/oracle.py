@@ -9,7 +9,8 @@ device.  ``store`` names the precision in which the device stores a tensor that 
 reads back: "f64" (no rounding), "f32" or "bf16" (round to nearest even).
 
 Each function names the part of the paper (Gross, Ranzato & Szlam, arXiv 1704.06363) it
-follows; the C file holds the arithmetic.
+follows; the C file holds the arithmetic, except for the PCA, whose eigensolve is LAPACK's
+(numpy.linalg.eigh) applied to the covariance written out in numpy.
 """
 from __future__ import annotations
 
@@ -281,3 +282,29 @@ def sgd_step(w, g, lr: float, weight_decay: float = 0.0, momentum: float = 0.0, 
                                      ctypes.c_double(lr), ctypes.c_double(weight_decay),
                                      ctypes.c_double(momentum)), "sgd_step")
     return (w.reshape(shape), vv.reshape(shape)) if momentum > 0.0 else w.reshape(shape)
+
+
+def pca(X, r: int):
+    """Section 4.2's projection before the K-means: the sample mean and the r leading
+    eigenpairs of the sample covariance C = (1/(n-1)) sum_i (x_i - mean)(x_i - mean)^T, by
+    LAPACK's symmetric eigensolver.  Components [r, d] in decreasing eigenvalue order, each
+    row's sign fixed so that its largest-magnitude entry is positive (lowest index on ties).
+    Returns (mean [d], components [r, d], eigenvalues [r])."""
+    X = _f64(X)
+    n = X.shape[0]
+    mean = X.sum(axis=0) / n
+    Xc = X - mean
+    C = (Xc.T @ Xc) / (n - 1)
+    w, U = np.linalg.eigh(C)
+    order = np.argsort(-w, kind="stable")[:r]
+    comps = U[:, order].T.copy()
+    for j in range(r):
+        k = int(np.argmax(np.abs(comps[j])))
+        if comps[j, k] < 0:
+            comps[j] = -comps[j]
+    return mean, comps, w[order]
+
+
+def pca_project(X, mean, comps):
+    """The projected features (x_i - mean) U^T that the K-means runs on (Section 4.2)."""
+    return (_f64(X) - _f64(mean)) @ _f64(comps).T
