@@ -180,6 +180,27 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                       float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* ------------------------------------------------------------------ PCA before the K-means */
+
+/* Section 4.2: the trunk's features are projected to their first 256 principal directions
+ * before the K-means.
+ * hmoe_pca_fit: mean float[d] out; components float[r][d] out -- the r leading eigenvectors of
+ *   the sample covariance (1/(n-1)) sum_i (x_i - mean)(x_i - mean)^T as orthonormal rows in
+ *   decreasing eigenvalue order, each row's largest-magnitude entry positive; eigvals float[r]
+ *   out.  Subspace iteration: n_iter steps Q <- orth(C Q) from a start drawn from `seed`, then
+ *   Rayleigh-Ritz; a component's accuracy depends on the gap between its eigenvalue and the
+ *   (r+1)-th.  X [n x d] in dtype dt; n >= 2, 8 <= r <= d, r and d multiples of 8.  The
+ *   d x d x r work runs on the GPU and the r x r factorisations on the host (fp64), so the call
+ *   synchronises `stream` (a preprocessing step; not for graph capture).  Device pointers
+ *   throughout (eigvals too).
+ * hmoe_pca_project: Z [n x r] (dtype dt) = (X - mean) components^T.
+ * Both take the workspace hmoe_pca_workspace asks for. */
+size_t hmoe_pca_workspace(int64_t n, int32_t d, int32_t r, hmoe_dtype_t dt);
+int hmoe_pca_fit(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t r, int32_t n_iter, uint64_t seed,
+                 float* mean, float* components, float* eigvals, void* ws, size_t ws_bytes, void* stream);
+int hmoe_pca_project(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const float* mean,
+                     const float* components, int32_t r, void* Z, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------ parameter update */
 
 /* One SGD step (Section 4.2: weight decay; the experts -- and the decoder trained with them --

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhmoe.so")
-SOURCES = ["api.hip", "dispatch.hip", "kmeans.hip", "metrics.hip", "moe.hip", "optim.hip"]
+SOURCES = ["api.hip", "dispatch.hip", "kmeans.hip", "metrics.hip", "moe.hip", "optim.hip", "pca.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 instructions are kept out of the generated code (hipcc's host pass warns that it

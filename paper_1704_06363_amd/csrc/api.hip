@@ -366,6 +366,50 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
                              dD, dbD, dX, w, (hipStream_t)stream);
 }
 
+static int check_pca(hmoe_dtype_t dt, int64_t n, int32_t d, int32_t r) {
+  HMOE_TRY(check_dtype(dt));
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_width("d", d));
+  HMOE_TRY(check_width("r", r));
+  if (r > d) return fail(HMOE_EINVAL, "r = %d exceeds d = %d", r, d);
+  return HMOE_OK;
+}
+
+size_t hmoe_pca_workspace(int64_t n, int32_t d, int32_t r, hmoe_dtype_t dt) {
+  if (n < 0 || d <= 0 || r <= 0) return 0;
+  const size_t a = pca_fit_ws(n, d, r), b = pca_project_ws(d, r, dt);
+  return a > b ? a : b;
+}
+
+int hmoe_pca_fit(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t r, int32_t n_iter, uint64_t seed,
+                 float* mean, float* components, float* eigvals, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_pca(dt, n, d, r));
+  if (n < 2) return fail(HMOE_EINVAL, "n = %lld: the sample covariance needs n >= 2", (long long)n);
+  if (n_iter < 0) return fail(HMOE_EINVAL, "n_iter = %d is negative", n_iter);
+  HMOE_TRY(check_ptr("X", X));
+  HMOE_TRY(check_ptr("mean", mean, false));
+  HMOE_TRY(check_ptr("components", components));
+  HMOE_TRY(check_ptr("eigvals", eigvals, false));
+  HMOE_TRY(check_ws(hmoe_pca_workspace(n, d, r, dt), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_pca_fit(X, dt, n, d, r, n_iter, seed, mean, components, eigvals, w, (hipStream_t)stream);
+}
+
+int hmoe_pca_project(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const float* mean,
+                     const float* components, int32_t r, void* Z, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  HMOE_TRY(check_pca(dt, n, d, r));
+  if (n == 0) return HMOE_OK;
+  HMOE_TRY(check_ptr("X", X));
+  HMOE_TRY(check_ptr("mean", mean, false));
+  HMOE_TRY(check_ptr("components", components, false));
+  HMOE_TRY(check_ptr("Z", Z));
+  HMOE_TRY(check_ws(hmoe_pca_workspace(n, d, r, dt), ws_bytes, ws));
+  Workspace w(ws, ws_bytes);
+  return launch_pca_project(X, dt, n, d, mean, components, r, Z, w, (hipStream_t)stream);
+}
+
 int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t dt, int64_t count, float lr,
                   float weight_decay, float momentum, void* stream) {
   clear_error();

@@ -902,6 +902,23 @@ __device__ __forceinline__ void store_direct(const TileCoord& tc, const floatx4 
   }
 }
 
+// Destination row of a tile row for the plain case: m0 + r.
+struct RowId {
+  int64_t m0;
+  __device__ __forceinline__ int64_t operator()(int r) const { return m0 + r; }
+};
+
+// Tile configuration per data type: bf16 runs the 256 x 256 direct-to-LDS engine, fp32 the
+// register-staged 128 x 128 one.
+template <typename T>
+struct Pick {
+  using C = CfgSmall<float>;
+};
+template <>
+struct Pick<bf16> {
+  using C = CfgDma;
+};
+
 // The epilogue store for the configuration's orientation.
 template <class C, typename O, class Elem, class RowMap, class Vec>
 __device__ __forceinline__ void store_out(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ], lds<char>* smem,

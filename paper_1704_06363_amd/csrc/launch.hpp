@@ -15,6 +15,16 @@ int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, i
                    hmoe_dtype_t dt, hipStream_t st);
 int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st);
 int launch_seg_order(const int32_t* seg, int G, int32_t* order, hipStream_t st);
+template <typename T>
+int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st);
+template <typename T>
+int launch_gemm_nn(const T* A, const T* W, int64_t rows, int Kd, int N, T* out, Workspace& ws, hipStream_t st);
+size_t pca_fit_ws(int64_t n, int d, int r);
+size_t pca_project_ws(int d, int r, hmoe_dtype_t dt);
+int launch_pca_fit(const void* X, hmoe_dtype_t dt, int64_t n, int d, int r, int n_iter, uint64_t seed, float* mean,
+                   float* comps, float* eigvals, Workspace& ws, hipStream_t st);
+int launch_pca_project(const void* X, hmoe_dtype_t dt, int64_t n, int d, const float* mean, const float* comps,
+                       int r, void* Z, Workspace& ws, hipStream_t st);
 int launch_sgd(float* w, const float* g, float* v, void* wlo, hmoe_dtype_t dt, int64_t count, float lr, float wd,
                float mu, hipStream_t st);
 int launch_topm(const void* L, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st);

@@ -24,23 +24,8 @@
 
 namespace hmoe {
 
-// Tile configuration per data type: bf16 runs the 256 x 256 direct-to-LDS engine, fp32 the
-// register-staged 128 x 128 one.
-template <typename T>
-struct Pick {
-  using C = CfgSmall<float>;
-};
-template <>
-struct Pick<bf16> {
-  using C = CfgDma;
-};
-
 // ------------------------------------------------------------------ expert forward
 
-struct RowId {
-  int64_t m0;
-  __device__ __forceinline__ int64_t operator()(int r) const { return m0 + r; }
-};
 struct RowVia {  // destination row = map[m0 + r]
   const int32_t* __restrict__ map;
   int64_t m0;
@@ -964,6 +949,50 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
                 dX);
   return HMOE_OK;
 }
+
+// ------------------------------------------------------------------ plain products (the PCA)
+
+// seg = {0, rows}: one group for the grouped kernels below.
+static __global__ void k_seg_one(int32_t* __restrict__ seg, int64_t rows) {
+  if (threadIdx.x == 0) {
+    seg[0] = 0;
+    seg[1] = (int32_t)rows;
+  }
+}
+
+// out [M][N] fp32 = A^T B over `rows` rows (A [rows][M], B [rows][N]): the reduction-grouped
+// kernel with a single group.
+template <typename T>
+int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st) {
+  using C = typename Pick<T>::C;
+  int32_t* seg = ws.take<int32_t>(2);
+  int32_t* order = ws.take<int32_t>(1);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  HMOE_LAUNCH("one segment", k_seg_one, dim3(1), dim3(64), 0, st, seg, rows);
+  HMOE_TRY(launch_seg_order(seg, 1, order, st));
+  HMOE_LAUNCH("gemm tn", k_expert_wgrad<C>, dim3((unsigned)(cdiv(M, C::BM) * cdiv(N, C::BN))), dim3(C::THREADS),
+              C::LDS, st, A, B, seg, order, 1, M, N, out);
+  return HMOE_OK;
+}
+
+// out [rows][N] = A W (A [rows][Kd], W [Kd][N]), in the data dtype: the row-grouped kernel with
+// a single group.
+template <typename T>
+int launch_gemm_nn(const T* A, const T* W, int64_t rows, int Kd, int N, T* out, Workspace& ws, hipStream_t st) {
+  using C = typename Pick<T>::C;
+  int32_t* seg = ws.take<int32_t>(2);
+  int32_t* ts = ws.take<int32_t>(2);
+  if (!ws.fits()) return HMOE_EWORKSPACE;
+  HMOE_LAUNCH("one segment", k_seg_one, dim3(1), dim3(64), 0, st, seg, rows);
+  HMOE_TRY(launch_seg_tiles(seg, 1, C::BM, ts, st));
+  HMOE_LAUNCH("gemm nn", (k_expert_dgrad<C, false>), dim3((unsigned)((cdiv(rows, C::BM) + 1) * cdiv(N, C::BN))),
+              dim3(C::THREADS), C::LDS, st, A, W, seg, ts, 1, N, Kd, (const T*)nullptr, (const int32_t*)nullptr, out);
+  return HMOE_OK;
+}
+
+template int launch_gemm_tn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t);
+template int launch_gemm_tn<bf16>(const bf16*, const bf16*, int64_t, int, int, float*, Workspace&, hipStream_t);
+template int launch_gemm_nn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t);
 
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                        const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits, float* lse,

@@ -26,6 +26,7 @@ SYMBOLS = (
     "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
     "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
     "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
+    "hmoe_pca_workspace", "hmoe_pca_fit", "hmoe_pca_project",
     "hmoe_sgd_step", "hmoe_topm", "hmoe_topm_hits",
     "hmoe_timer_enable", "hmoe_timer_report",
 )
@@ -84,6 +85,10 @@ def lib():
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                         _P, _P, _P, _SZ, _P]
+        L.hmoe_pca_workspace.restype = _SZ
+        L.hmoe_pca_workspace.argtypes = [_I64, _I32, _I32, _c.c_int]
+        L.hmoe_pca_fit.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _I32, _c.c_uint64, _P, _P, _P, _P, _SZ, _P]
+        L.hmoe_pca_project.argtypes = [_P, _c.c_int, _I64, _I32, _P, _P, _I32, _P, _P, _SZ, _P]
         L.hmoe_sgd_step.argtypes = [_P, _P, _P, _P, _c.c_int, _I64, _c.c_float, _c.c_float, _c.c_float, _P]
         L.hmoe_topm.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _P, _P, _P]
         L.hmoe_topm_hits.argtypes = [_P, _I64, _I32, _c.POINTER(Labels), _P, _P, _I64, _P, _P]
@@ -93,7 +98,8 @@ def lib():
         L.hmoe_timer_report.restype = _I64
         for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
                      "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
-                     "hmoe_moe_backward", "hmoe_sgd_step", "hmoe_topm", "hmoe_topm_hits"):
+                     "hmoe_moe_backward", "hmoe_pca_fit", "hmoe_pca_project", "hmoe_sgd_step",
+                     "hmoe_topm", "hmoe_topm_hits"):
             getattr(L, name).restype = _c.c_int
         _lib = L
     return _lib
@@ -383,3 +389,34 @@ def sgd_step(w, g, lr: float, weight_decay: float = 0.0, momentum: float = 0.0, 
     _chk(lib().hmoe_sgd_step(_ptr(w), _ptr(g), _ptr(v), _ptr(w_lo), dt, w.numel(), lr, weight_decay, momentum,
                              _stream()), "sgd_step")
     return w
+
+
+# ------------------------------------------------------------------ PCA before the K-means
+
+def pca_workspace(n, d, r, dtype) -> int:
+    return lib().hmoe_pca_workspace(n, d, r, 1 if dtype == torch.bfloat16 else 0)
+
+
+def pca_fit(X, r: int, n_iter: int = 20, seed: int = 0, ws=None):
+    """Section 4.2: mean [d], components [r, d] (the r leading principal directions, decreasing
+    eigenvalue, largest-magnitude entry of each positive) and eigenvalues [r], fp32."""
+    n, d = X.shape
+    dev = X.device
+    mean = torch.empty(d, dtype=torch.float32, device=dev)
+    comps = torch.empty(r, d, dtype=torch.float32, device=dev)
+    ev = torch.empty(r, dtype=torch.float32, device=dev)
+    w, wb = _workspace(pca_workspace(n, d, r, X.dtype), ws, dev)
+    _chk(lib().hmoe_pca_fit(_ptr(X), _dt(X), n, d, r, n_iter, seed, _ptr(mean), _ptr(comps), _ptr(ev), _ptr(w), wb,
+                            _stream()), "pca_fit")
+    return mean, comps, ev
+
+
+def pca_project(X, mean, comps, out=None, ws=None):
+    """(X - mean) comps^T in X's dtype: the features the K-means runs on."""
+    n, d = X.shape
+    r = comps.shape[0]
+    Z = out if out is not None else torch.empty(n, r, dtype=X.dtype, device=X.device)
+    w, wb = _workspace(pca_workspace(n, d, r, X.dtype), ws, X.device)
+    _chk(lib().hmoe_pca_project(_ptr(X), _dt(X), n, d, _ptr(mean), _ptr(comps), r, _ptr(Z), _ptr(w), wb, _stream()),
+         "pca_project")
+    return Z

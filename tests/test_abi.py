@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 19
+    assert len(names) == 22
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(hmoe.SYMBOLS)
@@ -90,6 +90,11 @@ def test_argument_errors_are_reported_before_launch(lib):
     assert rc == -3 and "vocab" in hmoe.last_error()
     rc = lib.hmoe_topm_hits(16, 10, 0, ctypes.byref(lab), None, None, 0, 16, None)
     assert rc == -1 and "m = 0" in hmoe.last_error()
+    # PCA: more components than dimensions, one sample
+    rc = lib.hmoe_pca_fit(16, 0, 100, 64, 72, 5, 0, 16, 16, 16, None, 0, None)
+    assert rc == -1 and "exceeds" in hmoe.last_error()
+    rc = lib.hmoe_pca_fit(16, 0, 1, 64, 8, 5, 0, 16, 16, 16, None, 0, None)
+    assert rc == -1 and "n >= 2" in hmoe.last_error()
     # SGD: momentum without a buffer, a negative learning rate
     rc = lib.hmoe_sgd_step(16, 16, None, None, 1, 100, ctypes.c_float(0.1), ctypes.c_float(0.0),
                            ctypes.c_float(0.9), None)

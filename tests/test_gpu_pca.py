@@ -1,0 +1,67 @@
+"""The PCA before the K-means (Section 4.2) on the HIP path against the oracle: the mean, the
+leading eigenvalues and the components (same sign convention, so compared entry by entry) on
+spiked-covariance data whose leading r directions are well separated, in fp32 and bf16; the
+projection from the oracle's fit and from the path's own; and the fit at the gater-fit
+workload's width (d = 512 to r = 256 on a 256-component mixture, where only the leading
+directions above the noise floor are determined)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_1704_06363_amd import hmoe
+from paper_1704_06363_amd import workloads as W
+from tests.parity import assert_close, np64
+
+pytestmark = pytest.mark.gpu
+
+
+def _spiked(n, d, r, seed, dtype):
+    """Rows mu + G diag(s) Q^T + 0.05 noise: r planted directions with standard deviations
+    from 6 down to 2 (relative eigenvalue gaps of at least 7%), then a noise floor."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    Q, _ = torch.linalg.qr(torch.randn(d, d, generator=g, dtype=torch.float64))
+    s = torch.linspace(6.0, 2.0, r, dtype=torch.float64)
+    X = (torch.randn(n, r, generator=g, dtype=torch.float64) * s) @ Q[:, :r].T
+    X += 0.05 * torch.randn(n, d, generator=g, dtype=torch.float64) + torch.randn(d, generator=g, dtype=torch.float64)
+    return X.to(torch.bfloat16 if dtype == "bf16" else torch.float32).cuda()
+
+
+@pytest.mark.parametrize("dtype,n,d,r", [("f32", 20000, 128, 32), ("bf16", 30000, 256, 64), ("f32", 5000, 64, 64)])
+def test_fit_and_project(dtype, n, d, r):
+    X = _spiked(n, d, min(r, d), seed=d + r, dtype=dtype)
+    mean, comps, ev = hmoe.pca_fit(X, r, n_iter=30, seed=1)
+    m_ref, c_ref, e_ref = O.pca(np64(X), r)
+    assert_close(mean, m_ref, 1e-5, "mean")
+    assert_close(ev, e_ref, 1e-3, "eigenvalues")
+    assert_close(comps, c_ref, 1e-2, "components")
+    # the projection, from the oracle's fit and from the path's own
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+    Zr = O.pca_project(np64(X), m_ref, c_ref)
+    Z = hmoe.pca_project(X, torch.tensor(m_ref, dtype=torch.float32).cuda(),
+                         torch.tensor(c_ref, dtype=torch.float32).cuda())
+    assert_close(Z, Zr, tol, "projection (oracle's fit)")
+    assert_close(hmoe.pca_project(X, mean, comps), Zr, max(tol, 1e-2), "projection (own fit)")
+
+
+def test_gater_width_mixture():
+    # d = 512 features of a 256-component mixture projected to r = 256: the 255 directions the
+    # component means span stand far above the unit noise, the last one is noise
+    n, d, r = 1 << 16, 512, 256
+    X = W.gmm_features(n, d, 256, seed=3, dtype="f32", device="cuda")
+    mean, comps, ev = hmoe.pca_fit(X, r, n_iter=20, seed=2)
+    m_ref, c_ref, e_ref = O.pca(np64(X), r)
+    assert_close(mean, m_ref, 1e-5, "mean")
+    assert_close(ev[:200], e_ref[:200], 1e-3, "leading eigenvalues")
+    # the leading 200 directions one by one (|cos| close to 1), the rest as a subspace
+    cos = np.abs(np.sum(np64(comps)[:200] * c_ref[:200], axis=1))
+    assert cos.min() > 0.999, cos.min()
+    P = np64(comps)[:255]
+    s = np.linalg.svd(P @ c_ref[:255].T, compute_uv=False)
+    assert s.min() > 0.99, s.min()
+
+
+def test_argument_errors():
+    X = torch.zeros(10, 64, device="cuda")
+    with pytest.raises(hmoe.HmoeError, match="exceeds"):
+        hmoe.pca_fit(X, 72)
