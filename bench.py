@@ -34,6 +34,7 @@ METRIC = "k-means assign samples/s; routed MoE fwd+bwd samples/s and % MFMA/HBM 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+LEG_NAMES = ("gater_fit", "gater_pca", "skewed", "independent", "inference", "sgd_update", "large_assign")
 
 
 def log(*a):
@@ -285,6 +286,67 @@ def leg_gater_fit(steps):
     return out
 
 
+def leg_gater_pca(steps):
+    """Section 4.2's gater features: the 512-wide features of the gater-fit workload reduced to
+    their 256 leading principal directions (covariance, 20 subspace iterations, Rayleigh-Ritz),
+    projected, and clustered on the projection (k-means++ and the same Lloyd iterations)."""
+    import torch
+    from paper_1704_06363_amd import hmoe
+    from paper_1704_06363_amd import workloads as W
+    c = W.CONFIGS["gater_fit"]
+    r, n_iter = 256, 20
+    X = W.gmm_features(c.n, c.d, c.extra["n_comp"], seed=0, dtype="f32", device="cuda",
+                       dirichlet_alpha=c.extra["alpha"])
+    ws = torch.empty(hmoe.pca_workspace(c.n, c.d, r, torch.float32), dtype=torch.uint8, device="cuda")
+    Z = torch.empty(c.n, r, dtype=torch.float32, device="cuda")
+    u = torch.tensor(W.uniforms(c.K, 1), dtype=torch.float64, device="cuda")
+    kws = torch.empty(hmoe.kmeans_fit_workspace(c.n, r, c.K, torch.float32), dtype=torch.uint8, device="cuda")
+    fitted = {}
+
+    def fit():
+        fitted["m"], fitted["u"], fitted["ev"] = hmoe.pca_fit(X, r, n_iter, seed=0, ws=ws)
+
+    def proj():
+        hmoe.pca_project(X, fitted["m"], fitted["u"], out=Z, ws=ws)
+
+    def km():
+        hmoe.kmeans_fit(Z, c.K, c.n_iter, init_uniforms=u, ws=kws)
+
+    fit_ms, frep = time_steps(fit, steps, 1)
+    gpu_ms = sum(v[1] for v in frep.values()) / steps
+    cov_cnt, cov_ms = frep["pca X^T X"]
+    cov_avg = cov_ms / cov_cnt
+    cov_tf = 2.0 * c.n * c.d * c.d / (cov_avg * 1e-3) / 1e12
+    proj_ms, prep = time_steps(proj, steps, 1)
+    p_cnt, p_ms = prep["pca project"]
+    p_avg = p_ms / p_cnt
+    proj_tf = 2.0 * c.n * c.d * r / (p_avg * 1e-3) / 1e12
+    km_ms, krep = time_steps(km, steps, 1)
+    a_cnt, a_ms = krep["assign"]
+    a_avg = a_ms / a_cnt
+    ev = fitted["ev"].double()
+    out = {"workload": f"gater features with PCA: n={c.n} fp32, d={c.d} -> r={r} ({n_iter} subspace "
+                       f"iterations), projection, K-means K={c.K} with {c.n_iter} Lloyd iterations on the "
+                       "projection",
+           "pca_fit_ms": round(fit_ms, 3),
+           "pca_fit_gpu_kernels_ms": round(gpu_ms, 3),
+           "pca_fit_host_ms": round(fit_ms - gpu_ms, 3),
+           "covariance_avg_ms": round(cov_avg, 4),
+           "covariance_tflops": round(cov_tf, 2),
+           "covariance_frac_fp32_peak": round(cov_tf / PEAK_F32_TFLOPS, 4),
+           "project_avg_ms": round(p_avg, 4),
+           "project_tflops": round(proj_tf, 2),
+           "project_frac_fp32_peak": round(proj_tf / PEAK_F32_TFLOPS, 4),
+           "kmeans_fit_ms": round(km_ms, 3),
+           "kmeans_assign_avg_ms": round(a_avg, 4),
+           "kmeans_assign_tflops": round(2.0 * c.n * c.K * r / (a_avg * 1e-3) / 1e12, 2),
+           "leading_eigenvalues": [round(float(x), 3) for x in ev[:4].tolist()],
+           "kernels_fit": kernel_table(frep, {"pca X^T X": 2.0 * c.n * c.d * c.d}, PEAK_F32_TFLOPS, steps)}
+    del X, Z, ws, kws
+    torch.cuda.empty_cache()
+    return out
+
+
 def leg_skewed(steps, warmup):
     import torch
     from paper_1704_06363_amd import workloads as W
@@ -450,13 +512,17 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-legs", action="store_true", help="skip the extra legs (gater fit, skewed, independent decoders, inference, SGD update, large assign)")
+    ap.add_argument("--no-legs", action="store_true", help="skip the extra legs (gater fit, gater PCA, skewed, independent decoders, inference, SGD update, large assign)")
+    ap.add_argument("--legs", default="", help="comma-separated subset of the legs to run (default: all)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
+    unknown = set(x for x in args.legs.split(",") if x) - set(LEG_NAMES)
+    if unknown:
+        raise SystemExit(f"unknown legs: {sorted(unknown)}")
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is "
               f"a design note, not a measured configuration.", file=sys.stderr)
@@ -518,18 +584,20 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_legs:
         legs = {}
-        log("leg: gater fit")
-        legs["gater_fit"] = leg_gater_fit(steps=2)
-        log("leg: skewed routing")
-        legs["skewed"] = leg_skewed(steps=max(2, args.steps // 2), warmup=1)
-        log("leg: independent decoders")
-        legs["independent"] = leg_independent(steps=max(2, args.steps // 2), warmup=1)
-        log("leg: inference tail")
-        legs["inference"] = leg_inference(steps=max(2, args.steps // 2), warmup=1)
-        log("leg: sgd update")
-        legs["sgd_update"] = leg_sgd_update(steps=max(2, args.steps // 2), warmup=1)
-        log("leg: large assign")
-        legs["large_assign"] = leg_large_assign(args.large_chunks)
+        table = [("gater_fit", "gater fit", lambda: leg_gater_fit(steps=2)),
+                 ("gater_pca", "gater features with PCA", lambda: leg_gater_pca(steps=2)),
+                 ("skewed", "skewed routing", lambda: leg_skewed(steps=max(2, args.steps // 2), warmup=1)),
+                 ("independent", "independent decoders",
+                  lambda: leg_independent(steps=max(2, args.steps // 2), warmup=1)),
+                 ("inference", "inference tail", lambda: leg_inference(steps=max(2, args.steps // 2), warmup=1)),
+                 ("sgd_update", "sgd update", lambda: leg_sgd_update(steps=max(2, args.steps // 2), warmup=1)),
+                 ("large_assign", "large assign", lambda: leg_large_assign(args.large_chunks))]
+        chosen = set(x for x in args.legs.split(",") if x)
+        for key, what, run in table:
+            if chosen and key not in chosen:
+                continue
+            log(f"leg: {what}")
+            legs[key] = run()
         res["legs"] = legs
     print(json.dumps(res), flush=True)
 

@@ -377,7 +377,7 @@ static int check_pca(hmoe_dtype_t dt, int64_t n, int32_t d, int32_t r) {
 
 size_t hmoe_pca_workspace(int64_t n, int32_t d, int32_t r, hmoe_dtype_t dt) {
   if (n < 0 || d <= 0 || r <= 0) return 0;
-  const size_t a = pca_fit_ws(n, d, r), b = pca_project_ws(d, r, dt);
+  const size_t a = pca_fit_ws(n, d, r, dt), b = pca_project_ws(d, r, dt);
   return a > b ? a : b;
 }
 

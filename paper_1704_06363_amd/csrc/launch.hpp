@@ -16,10 +16,13 @@ int launch_permute(const void* in, void* out, const int32_t* index, int64_t n, i
 int launch_seg_tiles(const int32_t* seg, int G, int tile, int32_t* tile_start, hipStream_t st);
 int launch_seg_order(const int32_t* seg, int G, int32_t* order, hipStream_t st);
 template <typename T>
-int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st);
+size_t gemm_tn_ws();
+template <typename T>
+int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st,
+                   const char* label = "gemm tn");
 template <typename T>
 int launch_gemm_nn(const T* A, const T* W, int64_t rows, int Kd, int N, T* out, Workspace& ws, hipStream_t st);
-size_t pca_fit_ws(int64_t n, int d, int r);
+size_t pca_fit_ws(int64_t n, int d, int r, hmoe_dtype_t dt);
 size_t pca_project_ws(int d, int r, hmoe_dtype_t dt);
 int launch_pca_fit(const void* X, hmoe_dtype_t dt, int64_t n, int d, int r, int n_iter, uint64_t seed, float* mean,
                    float* comps, float* eigvals, Workspace& ws, hipStream_t st);

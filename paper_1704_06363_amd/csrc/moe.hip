@@ -628,40 +628,39 @@ __global__ void __launch_bounds__(C::THREADS)
   store_out<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
 }
 
-// dD = G^T H (fp32), reduction over the n samples.  The tiles are run in rounds of one per
-// resident workgroup; when the last round is only partly filled, its tiles are split over K
-// instead: tiles b < t_full run whole, tile t_full + r (r < R) is computed as `split` K-chunks
-// (work items t_full + r * split + c) whose fp32 partials go to part[r * split + c] and are
-// added in chunk order by k_split_reduce.
+// out [M][N] (fp32) = A^T B, reduction over `rows` rows (A [rows][M], B [rows][N], both
+// row-major): the decoder's dD = G^T H and the PCA's covariance and Gram products.  The tiles are
+// run in rounds of one per resident workgroup; when the last round is only partly filled, its
+// tiles are split over K instead: tiles b < t_full run whole, tile t_full + r (r < R) is computed
+// as `split` K-chunks of `chunk` rows (work items t_full + r * split + c, every chunk non-empty)
+// whose fp32 partials go to part[r * split + c] and are added in chunk order by k_split_reduce.
 constexpr int kMaxSplitItems = 512;
 
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
-    k_dec_dD(const typename C::type* __restrict__ G, const typename C::type* __restrict__ H, int64_t n, int V, int o,
-             float* __restrict__ dD, int64_t t_full, int split, float* __restrict__ part) {
+    k_gemm_tn_split(const typename C::type* __restrict__ A, const typename C::type* __restrict__ B, int64_t rows,
+                    int M, int N, float* __restrict__ out, int64_t t_full, int split, int64_t chunk,
+                    float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
-  const int64_t T = cdiv(V, C::BM) * cdiv(o, C::BN);
+  const int64_t T = cdiv(M, C::BM) * cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
   floatx4 acc[C::MI][C::NJ];
   if (b < t_full) {
-    const TileCoord tc = tile_plain_at<C>(V, o, (int)n, b);
+    const TileCoord tc = tile_plain_at<C>(M, N, (int)rows, b);
     if (!tc.valid) return;
-    gemm_tile<C, false, false>(G + tc.m0, V, tc.m_rows, H + tc.n0, o, tc.n_cols, (int)n, smem, acc);
-    store_out<C, float>(tc, acc, smem, dD, o, Ident{}, RowId{tc.m0}, NoVec{});
+    gemm_tile<C, false, false>(A + tc.m0, M, tc.m_rows, B + tc.n0, N, tc.n_cols, (int)rows, smem, acc);
+    store_out<C, float>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, NoVec{});
     return;
   }
   const int64_t q = b - t_full;
   const int64_t t = t_full + q / split;
   if (t >= T) return;
   const int c = (int)(q % split);
-  const TileCoord tc = tile_plain_at<C>(V, o, (int)n, t);
-  const int64_t chunk = cdiv(cdiv(n, split), 32) * 32;
+  const TileCoord tc = tile_plain_at<C>(M, N, (int)rows, t);
   const int64_t k0 = c * chunk;
-  const int64_t kl = n - k0 < chunk ? n - k0 : chunk;
-  const int klen = kl > 0 ? (int)kl : 0;
-  gemm_tile<C, false, false>(G + tc.m0 + (k0 < n ? k0 : 0) * V, V, tc.m_rows, H + tc.n0 + (k0 < n ? k0 : 0) * o, o,
-                             tc.n_cols, klen, smem, acc);
+  const int klen = (int)(rows - k0 < chunk ? rows - k0 : chunk);
+  gemm_tile<C, false, false>(A + tc.m0 + k0 * M, M, tc.m_rows, B + tc.n0 + k0 * N, N, tc.n_cols, klen, smem, acc);
   TileCoord lt = tc;
   lt.m0 = 0;
   lt.n0 = 0;
@@ -669,18 +668,43 @@ __global__ void __launch_bounds__(C::THREADS)
 }
 
 template <class C>
-__global__ void __launch_bounds__(256) k_split_reduce(const float* __restrict__ part, int64_t n, int V, int o,
-                                                      int64_t t_full, int split, int R, float* __restrict__ dD) {
+__global__ void __launch_bounds__(256) k_split_reduce(const float* __restrict__ part, int64_t rows, int M, int N,
+                                                      int64_t t_full, int split, int R, float* __restrict__ out) {
   constexpr int TE = C::BM * C::BN;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)R * TE) return;
   const int r = (int)(idx / TE), e = (int)(idx % TE);
   const int i = e / C::BN, j = e % C::BN;
-  const TileCoord tc = tile_plain_at<C>(V, o, (int)n, t_full + r);
+  const TileCoord tc = tile_plain_at<C>(M, N, (int)rows, t_full + r);
   if (i >= tc.m_rows || j >= tc.n_cols) return;
   float s = 0.f;
   for (int c = 0; c < split; ++c) s += part[((int64_t)r * split + c) * TE + e];
-  dD[(tc.m0 + i) * (int64_t)o + tc.n0 + j] = s;
+  out[(tc.m0 + i) * (int64_t)N + tc.n0 + j] = s;
+}
+
+// Launches k_gemm_tn_split (and its reduction) for out = A^T B; `part` holds kMaxSplitItems
+// tiles of fp32 partials.  rows > 0.
+template <class C>
+static int launch_tn_split(const char* label, const typename C::type* A, const typename C::type* B, int64_t rows,
+                           int M, int N, float* out, float* part, hipStream_t st) {
+  // rounds of `slots` concurrent tiles (one workgroup per 160 KB of LDS per CU)
+  const int64_t tiles = cdiv(M, C::BM) * cdiv(N, C::BN);
+  int64_t slots = (int64_t)device_cus() * ((160 * 1024) / C::LDS);
+  if (slots > kMaxSplitItems) slots = kMaxSplitItems;
+  const int64_t R = tiles % slots;
+  const int64_t t_full = tiles - R;
+  int split = R > 0 ? (int)(slots / R) : 1;
+  // chunks of a multiple of 32 rows and at least 256 (fewer chunks when rows are few); split is
+  // then recounted so that no chunk is empty
+  int64_t chunk = cdiv(cdiv(rows, split), 32) * 32;
+  if (chunk < 256) chunk = 256;
+  split = (int)cdiv(rows, chunk);
+  HMOE_LAUNCH(label, k_gemm_tn_split<C>, dim3((unsigned)(t_full + R * split)), dim3(C::THREADS), C::LDS, st, A, B,
+              rows, M, N, out, t_full, split, chunk, part);
+  if (R > 0)
+    HMOE_LAUNCH("split-K reduce", k_split_reduce<C>, dim3((unsigned)cdiv(R * C::BM * C::BN, 256)), dim3(256), 0, st,
+                (const float*)part, rows, M, N, t_full, split, (int)R, out);
+  return HMOE_OK;
 }
 
 // ------------------------------------------------------------------ expert backward
@@ -915,21 +939,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
                 s.V, dbD);
   HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
               (const T*)G, D, n, s.V, s.o, inv, dYs);
-  {
-    // rounds of `slots` concurrent tiles (one workgroup per 160 KB of LDS per CU); the tiles of
-    // a partial last round are split over K to fill it
-    const int64_t tiles = cdiv(s.V, C::BM) * cdiv(s.o, C::BN);
-    int64_t slots = (int64_t)device_cus() * ((160 * 1024) / C::LDS);
-    if (slots > kMaxSplitItems) slots = kMaxSplitItems;
-    const int64_t R = tiles % slots;
-    const int64_t t_full = tiles - R;
-    const int split = R > 0 ? (int)(slots / R) : 1;
-    HMOE_LAUNCH("decoder dD", k_dec_dD<C>, dim3((unsigned)(t_full + R * split)), dim3(C::THREADS), C::LDS, st,
-                (const T*)G, H, n, s.V, s.o, dD, t_full, split, split_part);
-    if (R > 0)
-      HMOE_LAUNCH("decoder dD reduce", k_split_reduce<C>, dim3((unsigned)cdiv(R * C::BM * C::BN, 256)), dim3(256), 0,
-                  st, split_part, n, s.V, s.o, t_full, split, (int)R, dD);
-  }
+  HMOE_TRY(launch_tn_split<C>("decoder dD", (const T*)G, H, n, s.V, s.o, dD, split_part, st));
   }
   // experts
   const size_t mark = ws.off;
@@ -960,19 +970,22 @@ static __global__ void k_seg_one(int32_t* __restrict__ seg, int64_t rows) {
   }
 }
 
-// out [M][N] fp32 = A^T B over `rows` rows (A [rows][M], B [rows][N]): the reduction-grouped
-// kernel with a single group.
+// out [M][N] fp32 = A^T B over `rows` rows (A [rows][M], B [rows][N]), split over K when the
+// tiles alone would leave most of the chip idle.
 template <typename T>
-int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st) {
+size_t gemm_tn_ws() {
   using C = typename Pick<T>::C;
-  int32_t* seg = ws.take<int32_t>(2);
-  int32_t* order = ws.take<int32_t>(1);
+  return ((size_t)kMaxSplitItems * C::BM * C::BN) * sizeof(float) + 256;
+}
+
+template <typename T>
+int launch_gemm_tn(const T* A, const T* B, int64_t rows, int M, int N, float* out, Workspace& ws, hipStream_t st,
+                   const char* label) {
+  using C = typename Pick<T>::C;
+  float* part = ws.take<float>((size_t)kMaxSplitItems * C::BM * C::BN);
   if (!ws.fits()) return HMOE_EWORKSPACE;
-  HMOE_LAUNCH("one segment", k_seg_one, dim3(1), dim3(64), 0, st, seg, rows);
-  HMOE_TRY(launch_seg_order(seg, 1, order, st));
-  HMOE_LAUNCH("gemm tn", k_expert_wgrad<C>, dim3((unsigned)(cdiv(M, C::BM) * cdiv(N, C::BN))), dim3(C::THREADS),
-              C::LDS, st, A, B, seg, order, 1, M, N, out);
-  return HMOE_OK;
+  if (rows <= 0) return launch_zero_f32(out, (int64_t)M * N, st);
+  return launch_tn_split<C>(label, A, B, rows, M, N, out, part, st);
 }
 
 // out [rows][N] = A W (A [rows][Kd], W [Kd][N]), in the data dtype: the row-grouped kernel with
@@ -990,8 +1003,12 @@ int launch_gemm_nn(const T* A, const T* W, int64_t rows, int Kd, int N, T* out, 
   return HMOE_OK;
 }
 
-template int launch_gemm_tn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t);
-template int launch_gemm_tn<bf16>(const bf16*, const bf16*, int64_t, int, int, float*, Workspace&, hipStream_t);
+template size_t gemm_tn_ws<float>();
+template size_t gemm_tn_ws<bf16>();
+template int launch_gemm_tn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t,
+                                   const char*);
+template int launch_gemm_tn<bf16>(const bf16*, const bf16*, int64_t, int, int, float*, Workspace&, hipStream_t,
+                                  const char*);
 template int launch_gemm_nn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t);
 
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,

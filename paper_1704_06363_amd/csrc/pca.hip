@@ -6,8 +6,8 @@
 // eigenpairs of C by subspace iteration: Q <- orth(C Q), n_iter times from a seeded start, then
 // Rayleigh-Ritz (the eigenpairs of Q^T C Q, rotated back by Q).  The d x d x r and d x r x r
 // products run on the GPU; the r x r steps -- the Cholesky factor behind each orthonormalisation
-// (CholeskyQR, applied twice) and the final symmetric eigensolve (cyclic Jacobi) -- run on the
-// host in fp64, so a fit synchronises its stream.
+// (CholeskyQR) and the final symmetric eigensolve (Householder tridiagonalisation and implicit
+// QR steps) -- run on the host in fp64, so a fit synchronises its stream.
 // Projection: Z = (X - m) U^T on the tile engine, the mean folded into an fp32 column bias.
 #include <math.h>
 
@@ -129,76 +129,136 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // ------------------------------------------------------------------ host: r x r steps in fp64
 
-// S = R^T R with R upper triangular; returns R^{-1} (upper triangular) in Ri, or false when S is
-// not positive definite even after a tiny diagonal shift.
-static bool chol_inverse(std::vector<double> S, int r, std::vector<double>& Ri) {
+static inline double dot_f64(const double* a, const double* b, int n) {
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  int k = 0;
+  for (; k + 4 <= n; k += 4) {
+    s0 += a[k] * b[k];
+    s1 += a[k + 1] * b[k + 1];
+    s2 += a[k + 2] * b[k + 2];
+    s3 += a[k + 3] * b[k + 3];
+  }
+  for (; k < n; ++k) s0 += a[k] * b[k];
+  return (s0 + s1) + (s2 + s3);
+}
+
+// S = L L^T (L lower triangular, row-major, built row by row from contiguous dot products);
+// returns R^{-1} for R = L^T in Ri (upper triangular, row-major): row j of R^{-1} is column j of
+// L^{-1}, the forward solve of L x = e_j.  False when S is not positive definite even after a
+// tiny diagonal shift.
+static bool chol_inverse(const std::vector<double>& S, int r, std::vector<double>& Ri) {
   double tr = 0.0;
   for (int i = 0; i < r; ++i) tr += S[(size_t)i * r + i];
-  for (int i = 0; i < r; ++i) S[(size_t)i * r + i] += 1e-12 * tr / r;
-  std::vector<double> R((size_t)r * r, 0.0);
-  for (int j = 0; j < r; ++j) {
-    double dj = S[(size_t)j * r + j];
-    for (int k = 0; k < j; ++k) dj -= R[(size_t)k * r + j] * R[(size_t)k * r + j];
-    if (!(dj > 0.0)) return false;
-    const double rjj = sqrt(dj);
-    R[(size_t)j * r + j] = rjj;
-    for (int i = j + 1; i < r; ++i) {
-      double v = S[(size_t)j * r + i];
-      for (int k = 0; k < j; ++k) v -= R[(size_t)k * r + j] * R[(size_t)k * r + i];
-      R[(size_t)j * r + i] = v / rjj;
+  const double shift = 1e-12 * tr / r;
+  std::vector<double> L((size_t)r * r, 0.0);
+  for (int i = 0; i < r; ++i) {
+    double* Li = &L[(size_t)i * r];
+    for (int j = 0; j <= i; ++j) {
+      const double* Lj = &L[(size_t)j * r];
+      const double v = S[(size_t)i * r + j] + (i == j ? shift : 0.0) - dot_f64(Li, Lj, j);
+      if (i == j) {
+        if (!(v > 0.0)) return false;
+        Li[i] = sqrt(v);
+      } else {
+        Li[j] = v / Lj[j];
+      }
     }
   }
-  // inverse of the upper-triangular R, column by column (back substitution)
   Ri.assign((size_t)r * r, 0.0);
-  for (int c = 0; c < r; ++c) {
-    for (int i = c; i >= 0; --i) {
-      double v = (i == c) ? 1.0 : 0.0;
-      for (int k = i + 1; k <= c; ++k) v -= R[(size_t)i * r + k] * Ri[(size_t)k * r + c];
-      Ri[(size_t)i * r + c] = v / R[(size_t)i * r + i];
-    }
+  std::vector<double> x(r);
+  for (int j = 0; j < r; ++j) {
+    x[j] = 1.0 / L[(size_t)j * r + j];
+    for (int i = j + 1; i < r; ++i) x[i] = -dot_f64(&L[(size_t)i * r + j], &x[j], i - j) / L[(size_t)i * r + i];
+    for (int i = j; i < r; ++i) Ri[(size_t)j * r + i] = x[i];
   }
   return true;
 }
 
-// Eigenpairs of the symmetric A (r x r) by cyclic Jacobi rotations: on return w holds the
-// eigenvalues and the columns of V the eigenvectors (unsorted).
-static void jacobi_eigen(std::vector<double> A, int r, std::vector<double>& w, std::vector<double>& V) {
-  V.assign((size_t)r * r, 0.0);
-  for (int i = 0; i < r; ++i) V[(size_t)i * r + i] = 1.0;
-  auto a = [&](int i, int j) -> double& { return A[(size_t)i * r + j]; };
-  double norm = 0.0;
-  for (double x : A) norm += x * x;
-  for (int sweep = 0; sweep < 100; ++sweep) {
-    double off = 0.0;
-    for (int p = 0; p < r; ++p)
-      for (int q = p + 1; q < r; ++q) off += a(p, q) * a(p, q);
-    if (off <= 1e-30 * norm) break;
-    for (int p = 0; p < r; ++p)
-      for (int q = p + 1; q < r; ++q) {
-        const double apq = a(p, q);
-        if (apq == 0.0) continue;
-        const double theta = (a(q, q) - a(p, p)) / (2.0 * apq);
-        const double t = (theta >= 0.0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(theta * theta + 1.0));
-        const double c = 1.0 / sqrt(t * t + 1.0), s = t * c;
-        for (int k = 0; k < r; ++k) {  // columns p, q
-          const double akp = a(k, p), akq = a(k, q);
-          a(k, p) = c * akp - s * akq;
-          a(k, q) = s * akp + c * akq;
-        }
-        for (int k = 0; k < r; ++k) {  // rows p, q
-          const double apk = a(p, k), aqk = a(q, k);
-          a(p, k) = c * apk - s * aqk;
-          a(q, k) = s * apk + c * aqk;
-        }
-        for (int k = 0; k < r; ++k) {
-          const double vkp = V[(size_t)k * r + p], vkq = V[(size_t)k * r + q];
-          V[(size_t)k * r + p] = c * vkp - s * vkq;
-          V[(size_t)k * r + q] = s * vkp + c * vkq;
-        }
-      }
+// Eigenpairs of the symmetric A (n x n, row-major; destroyed): Householder reflections reduce A
+// to tridiagonal form T = Q^T A Q, then implicit symmetric QR steps with the Wilkinson shift
+// (bulge chasing with Givens rotations, deflating negligible off-diagonal entries) diagonalise
+// T.  Both transformations are accumulated into the rows of VT, so on return row j of VT is the
+// unit eigenvector of eigenvalue w[j] (unsorted).  All updates run along contiguous rows.
+static void sym_eigen(std::vector<double>& A, int n, std::vector<double>& w, std::vector<double>& VT) {
+  VT.assign((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) VT[(size_t)i * n + i] = 1.0;
+  std::vector<double> d(n), e(n, 0.0), u(n), p(n), acc(n);
+  for (int k = 0; k + 2 < n; ++k) {
+    const int m = n - k - 1;
+    const double* x = &A[(size_t)k * n + k + 1];  // the column below the diagonal, read as row k
+    const double xn = sqrt(dot_f64(x, x, m));
+    if (xn == 0.0) continue;  // already reduced: e[k] stays 0
+    const double alpha = x[0] > 0.0 ? -xn : xn;
+    for (int i = 0; i < m; ++i) u[i] = x[i];
+    u[0] -= alpha;
+    e[k] = alpha;
+    const double sc = sqrt(2.0 / dot_f64(u.data(), u.data(), m));
+    for (int i = 0; i < m; ++i) u[i] *= sc;  // the reflection is I - u u^T
+    // trailing block B <- H B H = B - u q^T - q u^T with p = B u, q = p - (u^T p / 2) u
+    for (int i = 0; i < m; ++i) p[i] = dot_f64(&A[(size_t)(k + 1 + i) * n + k + 1], u.data(), m);
+    const double half = 0.5 * dot_f64(u.data(), p.data(), m);
+    for (int i = 0; i < m; ++i) p[i] -= half * u[i];
+    for (int i = 0; i < m; ++i) {
+      double* row = &A[(size_t)(k + 1 + i) * n + k + 1];
+      const double ui = u[i], qi = p[i];
+      for (int j = 0; j < m; ++j) row[j] -= ui * p[j] + qi * u[j];
+    }
+    // VT <- H VT on rows k+1 ..
+    for (int j = 0; j < n; ++j) acc[j] = 0.0;
+    for (int i = 0; i < m; ++i) {
+      const double* row = &VT[(size_t)(k + 1 + i) * n];
+      const double ui = u[i];
+      for (int j = 0; j < n; ++j) acc[j] += ui * row[j];
+    }
+    for (int i = 0; i < m; ++i) {
+      double* row = &VT[(size_t)(k + 1 + i) * n];
+      const double ui = u[i];
+      for (int j = 0; j < n; ++j) row[j] -= ui * acc[j];
+    }
   }
-  w.resize(r);
-  for (int i = 0; i < r; ++i) w[i] = a(i, i);
+  for (int i = 0; i < n; ++i) d[i] = A[(size_t)i * n + i];
+  if (n >= 2) e[n - 2] = A[(size_t)(n - 2) * n + n - 1];
+  const double eps = 2.220446049250313e-16;
+  int hi = n - 1;
+  for (int guard = 0; hi > 0 && guard < 60 * n;) {
+    if (fabs(e[hi - 1]) <= eps * (fabs(d[hi - 1]) + fabs(d[hi]))) {  // d[hi] has converged
+      e[hi - 1] = 0.0;
+      --hi;
+      continue;
+    }
+    int lo = hi - 1;  // the unreduced block [lo, hi]
+    while (lo > 0 && fabs(e[lo - 1]) > eps * (fabs(d[lo - 1]) + fabs(d[lo]))) --lo;
+    ++guard;
+    // Wilkinson shift: the eigenvalue of the trailing 2 x 2 block nearer to its last diagonal
+    const double half = 0.5 * (d[hi - 1] - d[hi]);
+    const double eb = e[hi - 1];
+    const double mu = d[hi] - eb * eb / (half + (half >= 0.0 ? 1.0 : -1.0) * hypot(half, eb));
+    double x = d[lo] - mu, z = e[lo];
+    for (int k = lo; k < hi; ++k) {
+      // rotation of coordinates (k, k+1) that zeroes z against x (the bulge from step k-1)
+      const double r = hypot(x, z);
+      const double c = r == 0.0 ? 1.0 : x / r, s = r == 0.0 ? 0.0 : -z / r;
+      if (k > lo) e[k - 1] = r;
+      const double ak = d[k], bk = d[k + 1], f = e[k];
+      d[k] = c * c * ak - 2.0 * c * s * f + s * s * bk;
+      d[k + 1] = s * s * ak + 2.0 * c * s * f + c * c * bk;
+      e[k] = c * s * (ak - bk) + (c * c - s * s) * f;
+      if (k + 1 < hi) {
+        const double g = e[k + 1];
+        z = -s * g;  // the new bulge at (k, k + 2)
+        e[k + 1] = c * g;
+      }
+      x = e[k];
+      double* r0 = &VT[(size_t)k * n];
+      double* r1 = &VT[(size_t)(k + 1) * n];
+      for (int j = 0; j < n; ++j) {
+        const double v0 = r0[j], v1 = r1[j];
+        r0[j] = c * v0 - s * v1;
+        r1[j] = s * v0 + c * v1;
+      }
+    }
+  }
+  w = d;
 }
 
 static int d2h(void* dst, const void* src, size_t bytes, hipStream_t st) {
@@ -210,11 +270,13 @@ static int h2d(void* dst, const void* src, size_t bytes, hipStream_t st) {
   return hip_check(hipStreamSynchronize(st), "pca: synchronise");
 }
 
-// Q <- Q R^{-1} with Q^T Q = R^T R (CholeskyQR), twice; Z is scratch of Q's size.
-static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* Rinv, Workspace& ws, hipStream_t st) {
+// Q <- Q R^{-1} with Q^T Q = R^T R (CholeskyQR), `passes` times (the second pass restores the
+// orthonormality the fp32 Gram matrix loses on an ill-conditioned Q); Z is scratch of Q's size.
+static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* Rinv, int passes, Workspace& ws,
+                          hipStream_t st) {
   std::vector<float> hs((size_t)r * r);
   std::vector<double> Sd((size_t)r * r), Ri;
-  for (int pass = 0; pass < 2; ++pass) {
+  for (int pass = 0; pass < passes; ++pass) {
     const size_t mark = ws.off;
     HMOE_TRY(launch_gemm_tn<float>(Q, Q, d, r, r, S, ws, st));
     HMOE_TRY(d2h(hs.data(), S, hs.size() * sizeof(float), st));
@@ -232,7 +294,7 @@ static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* R
   return HMOE_OK;
 }
 
-size_t pca_fit_ws(int64_t n, int d, int r) {
+size_t pca_fit_ws(int64_t n, int d, int r, hmoe_dtype_t dt) {
   Workspace ws(nullptr, 0);
   ws.take<double>(d);
   ws.take<int32_t>(2);
@@ -241,7 +303,9 @@ size_t pca_fit_ws(int64_t n, int d, int r) {
   ws.take<float>((size_t)d * r);
   ws.take<float>((size_t)r * r);
   ws.take<float>((size_t)r * r);
-  return ws.off + segsum_ws(n, 1, d) + 4096;
+  const size_t g = dt == HMOE_BF16 ? gemm_tn_ws<bf16>() : gemm_tn_ws<float>();
+  const size_t sg = segsum_ws(n, 1, d);
+  return ws.off + (g > sg ? g : sg) + 4096;
 }
 
 template <typename T>
@@ -259,18 +323,20 @@ static int pca_fit_t(const T* X, int64_t n, int d, int r, int n_iter, uint64_t s
   HMOE_LAUNCH("pca segment", k_pca_seg, dim3(1), dim3(64), 0, st, seg, n);
   HMOE_TRY(launch_segsum<T, double>(X, d, nullptr, seg, 1, d, n, msum, 0, ws, st));
   ws.off = mark;
-  HMOE_TRY(launch_gemm_tn<T>(X, X, n, d, d, Cv, ws, st));
+  HMOE_TRY(launch_gemm_tn<T>(X, X, n, d, d, Cv, ws, st, "pca X^T X"));
   ws.off = mark;
   HMOE_LAUNCH("pca covariance", k_cov_finalize, dim3((unsigned)cdiv((int64_t)d * d, 256)), dim3(256), 0, st, Cv, msum,
               n, d, mean);
   HMOE_LAUNCH("pca start", k_pca_start, dim3((unsigned)cdiv((int64_t)d * r, 256)), dim3(256), 0, st, Q,
               (int64_t)d * r, seed);
-  HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, ws, st));
+  // one CholeskyQR pass per iteration keeps the subspace; the basis that enters Rayleigh-Ritz
+  // gets two
+  HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, n_iter == 0 ? 2 : 1, ws, st));
   for (int it = 0; it < n_iter; ++it) {
     HMOE_TRY(launch_gemm_nn<float>(Cv, Q, d, d, r, Z, ws, st));
     ws.off = mark;
     std::swap(Q, Z);
-    HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, ws, st));
+    HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, it == n_iter - 1 ? 2 : 1, ws, st));
   }
   // Rayleigh-Ritz: the eigenpairs of Q^T C Q, sorted by decreasing eigenvalue
   HMOE_TRY(launch_gemm_nn<float>(Cv, Q, d, d, r, Z, ws, st));
@@ -279,16 +345,16 @@ static int pca_fit_t(const T* X, int64_t n, int d, int r, int n_iter, uint64_t s
   ws.off = mark;
   std::vector<float> hs((size_t)r * r);
   HMOE_TRY(d2h(hs.data(), S, hs.size() * sizeof(float), st));
-  std::vector<double> Tm((size_t)r * r), w, V;
+  std::vector<double> Tm((size_t)r * r), w, VT;
   for (int i = 0; i < r; ++i)
     for (int j = 0; j < r; ++j) Tm[(size_t)i * r + j] = 0.5 * ((double)hs[(size_t)i * r + j] + hs[(size_t)j * r + i]);
-  jacobi_eigen(Tm, r, w, V);
+  sym_eigen(Tm, r, w, VT);
   std::vector<int> ord(r);
   for (int i = 0; i < r; ++i) ord[i] = i;
   std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return w[a] > w[b]; });
   std::vector<float> hw(r);
   for (int i = 0; i < r; ++i)
-    for (int j = 0; j < r; ++j) hs[(size_t)i * r + j] = (float)V[(size_t)i * r + ord[j]];
+    for (int j = 0; j < r; ++j) hs[(size_t)i * r + j] = (float)VT[(size_t)ord[j] * r + i];
   for (int j = 0; j < r; ++j) hw[j] = (float)w[ord[j]];
   HMOE_TRY(h2d(Rinv, hs.data(), hs.size() * sizeof(float), st));
   HMOE_TRY(h2d(eigvals, hw.data(), hw.size() * sizeof(float), st));
