@@ -288,11 +288,19 @@ __global__ void __launch_bounds__(C::THREADS)
   }
 }
 
-// lse = merge of the tile partials; loss = lse - mean positive logit.  One wave per row (row
-// widths are multiples of 8, so o / (16 / sizeof(T)) vectors cover a row exactly).
+// lse = merge of the tile partials; loss = lse - mean positive logit.  A block takes 64 rows.
+// The merge reads the partials [tile][row] coalesced: lane l of wave w takes row r0 + l and the
+// tiles t = w, w + 4, ... with an online (max, sum) merge, and the four waves' pairs are merged
+// in wave order.  The positive logits are (row, tag) tasks, numbered row by row in tag order:
+// 8 lanes per task each take every 8th 16-byte vector of the H row and the D row (row widths
+// are multiples of 8, so o / (16 / sizeof(T)) vectors cover a row exactly), the 8 partial sums
+// are combined by lane shuffles, and each row adds its tasks' dots in task order.
 // With per-expert decoders the rows (partials and H) are in slot order: row r is sample
 // perm[r], decoded by D_e, bD_e of the expert e whose segment of `seg` holds r; lse and loss
 // are written in sample order.  Shared decoder: perm = seg = NULL.
+constexpr int kLossRows = 64;
+constexpr int kLossTasks = 512;  // tasks staged in LDS at a time
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, const float* __restrict__ ps,
                                                   int nt, const T* __restrict__ H, const T* __restrict__ D,
@@ -301,48 +309,135 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
                                                   int G, const int32_t* __restrict__ row_ptr,
                                                   const int32_t* __restrict__ tag, float* __restrict__ lse,
                                                   float* __restrict__ loss) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int l = threadIdx.x & 63;
-  if (row >= n) return;
-  const int64_t smp = perm ? perm[row] : row;
-  if (seg) {
-    const int e = find_segment(seg, G, row);
-    D += (int64_t)e * V * o;
-    if (bD) bD += (int64_t)e * V;
-  }
-  float M = -FLT_MAX;
-  for (int t = l; t < nt; t += 64) M = fmaxf(M, pm[(int64_t)t * n + row]);
-  M = wave_max(M);
-  float S = 0.f;
-  for (int t = l; t < nt; t += 64) S += ps[(int64_t)t * n + row] * __expf(pm[(int64_t)t * n + row] - M);
-  S = wave_sum(S);
-  const float Lv = M + __logf(S);
-  // positive logits: lane group g (8 lanes) takes tags g, g + 8, ...; each lane covers every
-  // 8th 16-byte chunk of the rows; the partial sums are combined over the wave in a fixed order
   constexpr int EPV = 16 / sizeof(T);
-  const int32_t p0 = row_ptr[smp], p1 = row_ptr[smp + 1];
-  const int g = l >> 3, gl = l & 7;
-  const T* h = H + row * o;
-  const int vpr = o / EPV;
-  float pos = 0.f;
-  for (int32_t q = p0 + g; q < p1; q += 8) {
-    const int32_t tg = tag[q];
-    const T* dv = D + (int64_t)tg * o;
-    float s = 0.f;
-    for (int v = gl; v < vpr; v += 8) {
-      const i32x4 hr = *reinterpret_cast<const i32x4*>(h + v * EPV);
-      const i32x4 dr = *reinterpret_cast<const i32x4*>(dv + v * EPV);
-      const T* he = reinterpret_cast<const T*>(&hr);
-      const T* de = reinterpret_cast<const T*>(&dr);
-#pragma unroll
-      for (int z = 0; z < EPV; ++z) s += to_f32(he[z]) * to_f32(de[z]);
-    }
-    pos += s + ((bD && gl == 0) ? to_f32(bD[tg]) : 0.f);
+  __shared__ float s_m[4][kLossRows], s_s[4][kLossRows], s_pos[kLossRows];
+  __shared__ int32_t s_first[kLossRows + 1];  // first task of each row (exclusive prefix)
+  __shared__ int32_t s_p0[kLossRows], s_exp[kLossRows];
+  __shared__ int32_t s_trow[kLossTasks], s_ttag[kLossTasks];
+  __shared__ float s_dot[kLossTasks];
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int64_t r0 = (int64_t)blockIdx.x * kLossRows;
+  const int rows = (int)(n - r0 < kLossRows ? n - r0 : kLossRows);
+  {
+    float M = -FLT_MAX, S = 0.f;
+    if (l < rows)
+      for (int t = w; t < nt; t += 4) {
+        const float m = pm[(int64_t)t * n + r0 + l], sv = ps[(int64_t)t * n + r0 + l];
+        if (m > M) {
+          S = S * __expf(M - m) + sv;
+          M = m;
+        } else {
+          S += sv * __expf(m - M);
+        }
+      }
+    s_m[w][l] = M;
+    s_s[w][l] = S;
   }
-  pos = wave_sum(pos);
-  if (l == 0) {
+  if (threadIdx.x < kLossRows) {
+    const int t = threadIdx.x;
+    int32_t cnt = 0;
+    if (t < rows) {
+      const int64_t row = r0 + t;
+      const int64_t smp = perm ? perm[row] : row;
+      const int32_t p0 = row_ptr[smp];
+      cnt = row_ptr[smp + 1] - p0;
+      s_p0[t] = p0;
+      s_exp[t] = seg ? find_segment(seg, G, row) : 0;
+    }
+    s_first[t + 1] = cnt;  // turned into the prefix below
+    s_pos[t] = 0.f;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    s_first[0] = 0;
+    for (int t = 0; t < kLossRows; ++t) s_first[t + 1] += s_first[t];
+  }
+  __syncthreads();
+  const int total = s_first[kLossRows];
+  const int g = l >> 3, gl = l & 7;
+  const int vpr = o / EPV;
+  for (int c0 = 0; c0 < total; c0 += kLossTasks) {
+    const int cn = total - c0 < kLossTasks ? total - c0 : kLossTasks;
+    if (threadIdx.x < rows) {  // stage this row's tasks of the chunk
+      const int t = threadIdx.x;
+      const int a = s_first[t] > c0 ? s_first[t] : c0;
+      const int b = s_first[t + 1] < c0 + cn ? s_first[t + 1] : c0 + cn;
+      for (int j = a; j < b; ++j) {
+        s_trow[j - c0] = t;
+        s_ttag[j - c0] = tag[s_p0[t] + (j - s_first[t])];
+      }
+    }
+    __syncthreads();
+    // 32 tasks per step over the block; the trip count is the same for every lane of a wave
+    for (int j0 = w * 8; j0 < cn; j0 += 32) {
+      const int j = j0 + g;
+      float sdot = 0.f;
+      if (j < cn) {
+        const int t = s_trow[j];
+        const int32_t tg = s_ttag[j];
+        const T* h = H + (r0 + t) * o;
+        const T* dv = D + ((int64_t)s_exp[t] * V + tg) * o;
+        int v = gl;
+        for (; v + 24 < vpr; v += 32) {  // four vector pairs in flight
+          i32x4 hr[4], dr[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            hr[u] = *reinterpret_cast<const i32x4*>(h + (v + 8 * u) * EPV);
+            dr[u] = *reinterpret_cast<const i32x4*>(dv + (v + 8 * u) * EPV);
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const T* he = reinterpret_cast<const T*>(&hr[u]);
+            const T* de = reinterpret_cast<const T*>(&dr[u]);
+#pragma unroll
+            for (int z = 0; z < EPV; ++z) sdot += to_f32(he[z]) * to_f32(de[z]);
+          }
+        }
+        for (; v < vpr; v += 8) {
+          const i32x4 hr = *reinterpret_cast<const i32x4*>(h + v * EPV);
+          const i32x4 dr = *reinterpret_cast<const i32x4*>(dv + v * EPV);
+          const T* he = reinterpret_cast<const T*>(&hr);
+          const T* de = reinterpret_cast<const T*>(&dr);
+#pragma unroll
+          for (int z = 0; z < EPV; ++z) sdot += to_f32(he[z]) * to_f32(de[z]);
+        }
+      }
+      sdot += shfl_xor(sdot, 4);
+      sdot += shfl_xor(sdot, 2);
+      sdot += shfl_xor(sdot, 1);
+      if (j < cn && gl == 0) {
+        const int t = s_trow[j];
+        s_dot[j] = sdot + (bD ? to_f32(bD[(int64_t)s_exp[t] * V + s_ttag[j]]) : 0.f);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < rows) {  // this row's tasks of the chunk, in task order
+      const int t = threadIdx.x;
+      const int a = s_first[t] > c0 ? s_first[t] : c0;
+      const int b = s_first[t + 1] < c0 + cn ? s_first[t + 1] : c0 + cn;
+      float acc = s_pos[t];
+      for (int j = a; j < b; ++j) acc += s_dot[j - c0];
+      s_pos[t] = acc;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x < rows) {
+    const int t = threadIdx.x;
+    float M = s_m[0][t], S = s_s[0][t];
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+      const float m = s_m[q][t], sv = s_s[q][t];
+      if (m > M) {
+        S = S * __expf(M - m) + sv;
+        M = m;
+      } else {
+        S += sv * __expf(m - M);
+      }
+    }
+    const float Lv = M + __logf(S);
+    const int64_t smp = perm ? perm[r0 + t] : r0 + t;
     lse[smp] = Lv;
-    loss[smp] = Lv - pos / (float)(p1 - p0);
+    loss[smp] = Lv - s_pos[t] / (float)(s_first[t + 1] - s_first[t]);
   }
 }
 
@@ -850,7 +945,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
     HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
     HMOE_LAUNCH("decoder forward", k_dec_fwd_grouped<C>, dim3((unsigned)(mt_bound * ntv)), dim3(C::THREADS), C::LDS,
                 st, (const T*)Hs, D, (const T*)p->bD, offsets, ts, s.K, n, s.V, s.o, pm, ps, Lg);
-    HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv,
+    HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, kLossRows)), dim3(256), 0, st, pm, ps, ntv,
                 (const T*)Hs, D, (const T*)p->bD, n, s.o, s.V, perm, offsets, s.K, y->row_ptr, y->tag, lse, loss);
     return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
   }
@@ -866,7 +961,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
     HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS,
                 st, (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
   }
-  HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
+  HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, kLossRows)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
               (const T*)p->bD, n, s.o, s.V, (const int32_t*)nullptr, (const int32_t*)nullptr, 0, y->row_ptr,
               y->tag, lse, loss);
   return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);

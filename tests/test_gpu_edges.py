@@ -1,5 +1,5 @@
 """Edge cases of the HIP path against the fp64 oracle: rows with more tags than the gradient
-kernels stage in LDS, the narrowest widths the ABI allows, a single sample, a decoder with more
+and loss kernels stage in LDS, the narrowest widths the ABI allows, a single sample, a decoder with more
 tiles than the chip holds workgroups at once, the largest K, and exactly duplicated centres
 (ties must go to the lower index)."""
 import numpy as np
@@ -50,7 +50,8 @@ def _step_vs_oracle(X, ids, K, p, rp, tg, store, saved):
 
 @pytest.mark.parametrize("saved", [False, True])
 def test_rows_with_many_tags(saved):
-    # 17..24 tags on every other row: past the 16 tags per row the gradient kernels stage in LDS
+    # 17..24 tags on every other row: past the 16 tags per row the gradient kernels stage in LDS,
+    # and past the 512 (row, tag) pairs per 64 rows the loss kernel stages at a time
     n, d, h, o, V, K = 300, 64, 128, 64, 264, 3
     rp_few, tg_few = W.zipf_labels(n, V, 3, seed=40)
     rp_many, tg_many = W.zipf_labels(n, V, 24, seed=41, min_tags=17)
@@ -61,6 +62,7 @@ def test_rows_with_many_tags(saved):
     rp = np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32)
     tg = np.concatenate(rows).astype(np.int32)
     assert (rp[1:] - rp[:-1]).max() > 16
+    assert min(rp[min(i + 64, n)] - rp[i] for i in range(0, n, 64) if i + 64 <= n) > 512
     X = W.rectified_gaussian(n, d, seed=42, dtype="bf16", device="cuda")
     ids = np.random.default_rng(43).integers(0, K, n).astype(np.int32)
     p = W.moe_params(K, d, h, o, V, seed=44, dtype="bf16", device="cuda", bias=True)
