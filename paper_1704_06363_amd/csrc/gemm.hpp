@@ -428,7 +428,8 @@ __device__ __forceinline__ void dma_read_frags(const lds<char>* bA, const lds<ch
 // sub-tile, so each lane ends up with four consecutive output columns of one row (see TRANS).
 // ROWNORM: xs[i] += squares of this lane's 8 elements of A fragment i, for the fragments
 // i = wn (mod WAVES_N) that this wave is responsible for (the work is spread over the waves
-// that share the rows; each row's sum stays within one wave).
+// that share the rows; each row's sum stays within one wave), as four packed bf16 dot products
+// (the squares of bf16 values are exact in fp32).
 template <class C, bool ROWNORM>
 __device__ __forceinline__ void dma_mfmas(const bf16x8 (&a)[C::MI], const bf16x8 (&b)[C::NJ],
                                           floatx4 (&acc)[C::MI][C::NJ], float* xs) {
@@ -443,9 +444,9 @@ __device__ __forceinline__ void dma_mfmas(const bf16x8 (&a)[C::MI], const bf16x8
     for (int i = 0; i < C::MI; ++i)
       if ((i % C::WAVES_N) == wn) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float v = (float)a[i][e];
-          xs[i] += v * v;
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 v = {a[i][2 * e], a[i][2 * e + 1]};
+          xs[i] = __builtin_amdgcn_fdot2_f32_bf16(v, v, xs[i], false);
         }
       }
   }

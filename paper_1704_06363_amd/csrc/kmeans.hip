@@ -116,8 +116,13 @@ __global__ void __launch_bounds__(C::THREADS)
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   float xs[C::MI];
-  gemm_tile<C, true, true, true>(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem, acc,
-                                 xs);
+  // only the first centre tile of a row block needs the row norms (min_dist = min + |x|^2)
+  DmaTile<C, true, true> pipe;
+  pipe.prime(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem);
+  if (tc.n0 == 0)
+    pipe.template run<true>(smem, acc, xs);
+  else
+    pipe.template run<false>(smem, acc);
   using F = Frag<C>;
   const F f;
   lds<float>* xn = reinterpret_cast<lds<float>*>(smem);  // [BM]
@@ -125,7 +130,7 @@ __global__ void __launch_bounds__(C::THREADS)
   lds<int32_t>* ri = reinterpret_cast<lds<int32_t>*>(rv + C::WAVES_N * C::BM);
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
-    if ((i % C::WAVES_N) == f.wn) {
+    if (tc.n0 == 0 && (i % C::WAVES_N) == f.wn) {
       float s = xs[i];
       s += shfl_xor(s, 16);
       s += shfl_xor(s, 32);
