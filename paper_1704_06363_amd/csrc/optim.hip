@@ -62,9 +62,9 @@ __global__ void __launch_bounds__(256) k_sgd(float* __restrict__ w, const float*
 template <typename O>
 static int sgd_t(float* w, const float* g, float* v, O* wlo, int64_t count, float lr, float wd, float mu,
                  hipStream_t st) {
+  // one 16-byte vector per thread (a grid capped at 16 workgroups per CU looping over the
+  // tensor measured 20% slower: fewer loads in flight)
   int64_t grid = cdiv(cdiv(count, 4), 256);
-  const int64_t cap = (int64_t)device_cus() * 16;
-  if (grid > cap) grid = cap;
   if (grid < 1) grid = 1;
   if (mu > 0.f)
     HMOE_LAUNCH("sgd step", (k_sgd<O, true>), dim3((unsigned)grid), dim3(256), 0, st, w, g, v, wlo, count, lr, wd, mu);
