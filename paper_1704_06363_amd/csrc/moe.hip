@@ -71,16 +71,28 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // ------------------------------------------------------------------ decoder forward
 
-// Softmax statistics of one logits tile (logit = accumulator + bias): per row, m = max over the
-// tile's valid columns and s = sum exp(logit - m), merged over the WAVES_N waves that share the
-// row through rm / rs (LDS, [WAVES_N][BM] floats each) and written as the tile's partials
-// pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
+// acc += bias, in place: the accumulators become the tile's logits (the statistics and the
+// stored logits both read them).
 template <class C>
-__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
-                                               const float (&bias)[Frag<C>::NCOL], lds<float>* rm, lds<float>* rs,
-                                               int64_t n, float* __restrict__ pm, float* __restrict__ ps) {
+__device__ __forceinline__ void add_bias(floatx4 (&acc)[C::MI][C::NJ], const float (&bias)[Frag<C>::NCOL]) {
+  using F = Frag<C>;
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[i][j][r] += bias[F::qidx(j, r)];
+}
+
+// Per-wave row statistics of a logits tile: m = max over the wave's valid columns of the row,
+// s = sum exp(logit - m) (as exp2 of logit log2(e) - m log2(e)), into rm / rs [WAVES_N][BM].
+// FULL: every column of the tile is valid (no column guards).
+template <class C, bool FULL>
+__device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                              lds<float>* rm, lds<float>* rs) {
   using F = Frag<C>;
   const F f;
+  constexpr float kLog2e = 1.4426950408889634f;
   if constexpr (F::T) {
     // one row per i; its WN columns of this wave sit in lanes lr, lr + 16, lr + 32, lr + 48
 #pragma unroll
@@ -90,15 +102,16 @@ __device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx
       for (int j = 0; j < C::NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[F::qidx(j, r)]);
+          if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
       mx = fmaxf(mx, shfl_xor(mx, 16));
       mx = fmaxf(mx, shfl_xor(mx, 32));
+      const float mb = mx * kLog2e;
       float s = 0.f;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (f.col(j, r) < tc.n_cols) s += __expf(acc[i][j][r] + bias[F::qidx(j, r)] - mx);
+          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
       s += shfl_xor(s, 16);
       s += shfl_xor(s, 32);
       if (f.lg == 0) {
@@ -115,13 +128,14 @@ __device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx
         float mx = -FLT_MAX;
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j)
-          if (f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r] + bias[j]);
+          if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
+        const float mb = mx * kLog2e;
         float s = 0.f;
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j)
-          if (f.col(j, r) < tc.n_cols) s += __expf(acc[i][j][r] + bias[j] - mx);
+          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
         if (f.lr == 0) {
@@ -130,6 +144,20 @@ __device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx
         }
       }
   }
+}
+
+// Softmax statistics of one logits tile (acc already holds accumulator + bias): per row,
+// m = max over the tile's valid columns and s = sum exp(logit - m), merged over the WAVES_N
+// waves that share the row through rm / rs (LDS, [WAVES_N][BM] floats each) and written as the
+// tile's partials pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
+template <class C>
+__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                               lds<float>* rm, lds<float>* rs, int64_t n, float* __restrict__ pm,
+                                               float* __restrict__ ps) {
+  if (tc.n_cols == C::BN)
+    dec_row_stats<C, true>(tc, acc, rm, rs);
+  else
+    dec_row_stats<C, false>(tc, acc, rm, rs);
   wg_barrier_lds();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     float M = rm[t];
@@ -174,12 +202,12 @@ __global__ void __launch_bounds__(C::THREADS)
   using F = Frag<C>;
   float bias[F::NCOL];
   dec_tile_bias<C>(tc, bD, bias);
+  add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, bias, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
-    store_out<C, T>(tc, acc, smem, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
-                    RowId{tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
   }
 }
 
@@ -203,12 +231,12 @@ __global__ void __launch_bounds__(C::THREADS)
   using F = Frag<C>;
   float bias[F::NCOL];
   dec_tile_bias<C>(tc, bD ? bD + (int64_t)tc.group * V : nullptr, bias);
+  add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, bias, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
-    store_out<C, T>(tc, acc, smem, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
-                    RowId{tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
   }
 }
 
@@ -265,7 +293,8 @@ __global__ void __launch_bounds__(C::THREADS)
       bias[4 * j + 2] = __uint_as_float(bp[j].y << 16);
       bias[4 * j + 3] = __uint_as_float(bp[j].y & 0xffff0000u);
     }
-    dec_tile_stats<C>(tc, acc, bias, rm, rs, n, pm, ps);
+    add_bias<C>(acc, bias);
+    dec_tile_stats<C>(tc, acc, rm, rs, n, pm, ps);
     const int64_t tn = t + gridDim.x;
     const bool more = tn < tiles;
     TileCoord nc = tc;
@@ -278,8 +307,7 @@ __global__ void __launch_bounds__(C::THREADS)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
     if (L)
-      store_direct<C, bf16>(tc, acc, L, V, [&](int, int j, int r, float v) { return v + bias[F::qidx(j, r)]; },
-                            RowId{tc.m0}, NoVec{});
+      store_direct<C, bf16>(tc, acc, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
     __builtin_amdgcn_sched_barrier(0);
     if (!more) break;
     stores_pending = L != nullptr && tc.m_rows == C::BM && tc.n_cols == C::BN;
