@@ -293,8 +293,10 @@ __global__ void __launch_bounds__(C::THREADS)
       bias[4 * j + 2] = __uint_as_float(bp[j].y << 16);
       bias[4 * j + 3] = __uint_as_float(bp[j].y & 0xffff0000u);
     }
-    add_bias<C>(acc, bias);
-    dec_tile_stats<C>(tc, acc, rm, rs, n, pm, ps);
+    // the next tile's first stages go out before the statistics, so their loads land while
+    // the epilogue runs (run() ends with every wave past its last read of the ring; the
+    // statistics' partials stores are then younger than the primed loads, which can only make
+    // the next tile's waits stricter)
     const int64_t tn = t + gridDim.x;
     const bool more = tn < tiles;
     TileCoord nc = tc;
@@ -303,6 +305,8 @@ __global__ void __launch_bounds__(C::THREADS)
       dec_bias_packed<C>(nc, bD, bp);
       pipe.prime(H + nc.m0 * o, o, nc.m_rows, D + (int64_t)nc.n0 * o, o, nc.n_cols, o, smem);
     }
+    add_bias<C>(acc, bias);
+    dec_tile_stats<C>(tc, acc, rm, rs, n, pm, ps);
     // nothing may move between the primed loads and the stores: the next waits count them
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
