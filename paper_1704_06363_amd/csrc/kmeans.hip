@@ -413,15 +413,73 @@ __global__ void __launch_bounds__(256) k_gather_centres(const T* __restrict__ X,
 
 // ------------------------------------------------------------------ Lloyd update
 
+// The farthest-row search of the first reseed, spread over the grid: block b takes rows
+// [b chunk, (b + 1) chunk) and writes its largest min_dist among rows whose cluster has more
+// than one member (lowest index on ties; -1 / INT64_MAX when it has none) to pv[b], pi[b].
+// Every block returns at once when no cluster is empty.
+constexpr int kReseedBlocks = 512;
+
+__global__ void __launch_bounds__(1024) k_reseed_scan(const int32_t* __restrict__ assign,
+                                                      const float* __restrict__ d1, int64_t n, int K,
+                                                      const int32_t* __restrict__ counts32, float* __restrict__ pv,
+                                                      int64_t* __restrict__ pi) {
+  __shared__ int any_empty;
+  __shared__ float bv[16];
+  __shared__ int64_t bix[16];
+  if (threadIdx.x == 0) any_empty = 0;
+  __syncthreads();
+  for (int k = threadIdx.x; k < K; k += 1024)
+    if (counts32[k] == 0) any_empty = 1;
+  __syncthreads();
+  if (!any_empty) return;
+  const int64_t chunk = cdiv(n, (int64_t)gridDim.x);
+  const int64_t i0 = (int64_t)blockIdx.x * chunk;
+  const int64_t i1 = i0 + chunk < n ? i0 + chunk : n;
+  float best = -1.f;
+  int64_t bi = INT64_MAX;
+  for (int64_t i = i0 + threadIdx.x; i < i1; i += 1024) {
+    if (counts32[assign[i]] <= 1) continue;
+    const float v = d1[i];
+    if (v > best || (v == best && i < bi)) {
+      best = v;
+      bi = i;
+    }
+  }
+  for (int m = 1; m < 64; m <<= 1) {
+    const float v2 = __shfl_xor(best, m, 64);
+    const int64_t i2 = __shfl_xor(bi, m, 64);
+    if (v2 > best || (v2 == best && i2 < bi)) {
+      best = v2;
+      bi = i2;
+    }
+  }
+  if ((threadIdx.x & 63) == 0) {
+    bv[threadIdx.x >> 6] = best;
+    bix[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 16; ++w)
+      if (bv[w] > best || (bv[w] == best && bix[w] < bi)) {
+        best = bv[w];
+        bi = bix[w];
+      }
+    pv[blockIdx.x] = best;
+    pi[blockIdx.x] = bi;
+  }
+}
+
 // Loads counts into shared memory, reseeds empty clusters (ascending ids; each takes the
 // farthest row -- largest min_dist, lowest index on ties -- whose cluster has more than one
-// member, moves it and its vector between the fp64 sums), then writes counts back.
-// One block of 1024 threads; K <= 4096.
+// member, moves it and its vector between the fp64 sums), then writes counts back.  The first
+// reseed takes its row from the np partials of k_reseed_scan (the same counts and assignment,
+// so the same row); later ones scan the rows here.  One block of 1024 threads; K <= 4096.
 template <typename T>
 __global__ void __launch_bounds__(1024) k_reseed(const T* __restrict__ X, int64_t n, int d, int K,
                                                  int32_t* __restrict__ assign, const float* __restrict__ d1,
                                                  int32_t* __restrict__ counts32, int64_t* __restrict__ counts64,
-                                                 double* __restrict__ sums, int reseed) {
+                                                 double* __restrict__ sums, int reseed, const float* __restrict__ pv,
+                                                 const int64_t* __restrict__ pi, int np) {
   __shared__ int32_t cnt[4096];
   __shared__ float bv[16];
   __shared__ int64_t bix[16];
@@ -429,19 +487,32 @@ __global__ void __launch_bounds__(1024) k_reseed(const T* __restrict__ X, int64_
   for (int k = threadIdx.x; k < K; k += 1024) cnt[k] = counts32[k];
   __syncthreads();
   if (reseed && n > 0) {
+    bool first = true;
     for (int k = 0; k < K; ++k) {
       if (cnt[k] != 0) continue;
       float best = -1.f;
       int64_t bi = INT64_MAX;
-      for (int64_t i = threadIdx.x; i < n; i += 1024) {
-        const int32_t a = __hip_atomic_load(assign + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (cnt[a] <= 1) continue;
-        const float v = d1[i];
-        if (v > best || (v == best && i < bi)) {
-          best = v;
-          bi = i;
+      if (first && np > 0) {
+        for (int q = threadIdx.x; q < np; q += 1024) {
+          const float v = pv[q];
+          const int64_t i = pi[q];
+          if (v > best || (v == best && i < bi)) {
+            best = v;
+            bi = i;
+          }
+        }
+      } else {
+        for (int64_t i = threadIdx.x; i < n; i += 1024) {
+          const int32_t a = __hip_atomic_load(assign + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (cnt[a] <= 1) continue;
+          const float v = d1[i];
+          if (v > best || (v == best && i < bi)) {
+            best = v;
+            bi = i;
+          }
         }
       }
+      first = false;
       for (int m = 1; m < 64; m <<= 1) {
         const float v2 = __shfl_xor(best, m, 64);
         const int64_t i2 = __shfl_xor(bi, m, 64);
@@ -531,8 +602,19 @@ static int update_core(const T* X, int64_t n, int32_t d, int32_t K, int32_t* ass
     HMOE_LAUNCH("add counts", k_add_counts, dim3((unsigned)cdiv(K, 256)), dim3(256), 0, st, b.counts32, K, counts64);
     return HMOE_OK;
   }
+  float* pv = nullptr;
+  int64_t* pi = nullptr;
+  int np = 0;
+  if (reseed && n > 0) {
+    np = (int)(cdiv(n, (int64_t)4096) < kReseedBlocks ? cdiv(n, (int64_t)4096) : kReseedBlocks);
+    pv = ws.take<float>(np);
+    pi = ws.take<int64_t>(np);
+    if (!ws.fits()) return HMOE_EWORKSPACE;
+    HMOE_LAUNCH("reseed scan", k_reseed_scan, dim3((unsigned)np), dim3(1024), 0, st, (const int32_t*)assign, d1, n, K,
+                (const int32_t*)b.counts32, pv, pi);
+  }
   HMOE_LAUNCH("reseed", k_reseed<T>, dim3(1), dim3(1024), 0, st, X, n, d, K, assign, d1, b.counts32, counts64, sums,
-                     reseed);
+                     reseed, (const float*)pv, (const int64_t*)pi, np);
   return HMOE_OK;
 }
 
@@ -542,7 +624,8 @@ static size_t update_scratch(int64_t n, int32_t d, int32_t K) {
   ws.take<int32_t>(K + 1);
   ws.take<int32_t>(n);
   ws.take<int32_t>(n);
-  size_t s = ws.off + dispatch_ws(n, K) + segsum_ws(n, K, d) + 4096;
+  size_t s = ws.off + dispatch_ws(n, K) + segsum_ws(n, K, d) +
+             (size_t)kReseedBlocks * (sizeof(float) + sizeof(int64_t)) + 4096;
   return s;
 }
 

@@ -135,3 +135,29 @@ def test_duplicated_centres_break_ties_low(dtype, K):
     a_ref, d1, d2 = O.assign(np64(X), np64(base))
     assert_assign(a // 2, a_ref, d1, d2)
     assert_close(md, d1, 1e-4, "min_dist")
+
+
+def test_reseed_search_across_blocks():
+    # 300,000 rows: the first reseed's farthest-row search runs over 74 blocks of the grid and
+    # the later ones inside the reseeding block.  Rows 10 and 250,000 (different blocks) are the
+    # same far outlier, so their min distances tie: the first empty cluster must take row 10
+    # (lowest index), the second then takes row 250,000.
+    n, d, K = 300_000, 32, 8
+    X = W.gmm_features(n, d, 4, seed=51, dtype="f32", device="cuda")
+    X[10] = 40.0
+    X[250_000] = 40.0
+    Xh = np64(X)
+    C0 = Xh[[0, 1, 2, 3, 4, 5, 6, 7]].copy()
+    C0[K - 2:] = 1e3  # two far-away centres: their clusters start empty
+    a_ref, d1, _ = O.assign(Xh, C0)
+    a = torch.tensor(a_ref, dtype=torch.int32, device="cuda")
+    md = torch.tensor(d1, dtype=torch.float32, device="cuda")
+    C = torch.tensor(C0, dtype=torch.float32, device="cuda")
+    sums = torch.zeros(K, d, dtype=torch.float64, device="cuda")
+    cnt = torch.zeros(K, dtype=torch.int64, device="cuda")
+    hmoe.kmeans_update(X, K, a, md, sums, cnt, C, mode=hmoe.UPDATE_FULL, reseed=True)
+    C_ref, counts_ref, a2_ref = O.update(Xh, a_ref, np64(md), C0, reseed=True)
+    assert a2_ref[10] == K - 2 and a2_ref[250_000] == K - 1
+    assert npi(cnt).tolist() == counts_ref.tolist()
+    assert np.array_equal(npi(a), a2_ref)
+    assert_close(C, O.round_store(C_ref, "f32"), 1e-6, "centres")
