@@ -727,7 +727,9 @@ __device__ __forceinline__ TileCoord tile_group_m(const int32_t* __restrict__ se
 // Reduction-grouped problem (experts' weight gradients): group e reduces over the rows
 // [seg[e], seg[e+1]) of both operands; output tile (m, n) of group e.  Groups are taken in the
 // order `order` gives (longest reduction first), so the deepest tiles start in the first round
-// instead of forming the tail of the launch.
+// instead of forming the tail of the launch.  Within a group the tiles run in bands of 16
+// m-tiles, m fastest (as tile_plain_at): the tiles that share an A panel are 16 workgroups
+// apart, which the round-robin placement of workgroups puts on one XCD (one L2).
 template <class C>
 __device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ seg,
                                                   const int32_t* __restrict__ order, int G, int M, int N) {
@@ -737,7 +739,12 @@ __device__ __forceinline__ TileCoord tile_group_k(const int32_t* __restrict__ se
   const int per = mt * nt;
   const int slot = (int)(b / per);
   const int in = (int)(b - (int64_t)slot * per);
-  const int mi = in / nt, ni = in % nt;
+  constexpr int band = 16;
+  const int g = in / (band * nt);
+  const int inb = in - g * band * nt;
+  const int m_first = g * band;
+  const int bm = (mt - m_first < band) ? (mt - m_first) : band;
+  const int mi = m_first + inb % bm, ni = inb / bm;
   tc.valid = slot < G;
   const int e = tc.valid ? order[slot] : 0;
   tc.group = e;
