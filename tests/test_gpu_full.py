@@ -241,3 +241,38 @@ def test_large_assign_full_size():
         assert int(cnt[k]) == int(ref_cnt[q])
         if int(ref_cnt[q]) > 0:
             assert_close(Cn[k], (ref_sum[q] / ref_cnt[q]).float(), 1e-5, f"centre {k}")
+
+
+def test_gater_pca_full_size():
+    # the bench's PCA: 2^20 fp32 rows of width 512 (a 256-component Dirichlet(0.5) mixture) to
+    # 256 components with 20 subspace iterations, against the oracle's fp64 covariance of the
+    # same rows and LAPACK's eigenpairs.  Its spectrum has near-equal neighbours (relative gaps
+    # down to 0.2% among the leading 128) and reaches the noise floor well before 256, so
+    # single directions are compared only where both neighbouring gaps exceed 2%; every one of
+    # the leading 128 computed pairs must be an eigenpair of the fp64 covariance (residual),
+    # and the span of the leading k is compared at the largest gap.
+    c = W.CONFIGS["gater_fit"]
+    r, lead = 256, 128
+    X = W.gmm_features(c.n, c.d, c.extra["n_comp"], seed=0, dtype="f32", device="cuda",
+                       dirichlet_alpha=c.extra["alpha"])
+    mean, comps, ev = hmoe.pca_fit(X, r, 20, seed=0)
+    Z = hmoe.pca_project(X, mean, comps)
+    Xh = np64(X)
+    m_ref, c_ref, e_ref = O.pca(Xh, r)
+    assert_close(mean, m_ref, 1e-5, "mean")
+    assert_close(ev[:lead], e_ref[:lead], 1e-3, "leading eigenvalues")
+    U = np64(comps)[:lead]
+    Cov = np.cov(Xh, rowvar=False)
+    res = np.linalg.norm(Cov @ U.T - U.T * np64(ev)[:lead], axis=0)
+    assert res.max() < 1e-3 * e_ref[0], res.max() / e_ref[0]
+    gap = (e_ref[:-1] - e_ref[1:]) / e_ref[:-1]
+    single = [j for j in range(1, lead) if gap[j - 1] > 0.02 and gap[j] > 0.02]
+    assert len(single) >= 8
+    cos = np.abs(np.sum(U[single] * c_ref[single], axis=1))
+    assert cos.min() > 0.999, cos.min()
+    k = 16 + int(np.argmax(gap[16:lead]))  # span of the leading k + 1 at the largest gap
+    sv = np.linalg.svd(U[:k + 1] @ c_ref[:k + 1].T, compute_uv=False)
+    assert sv.min() > 0.999, (k, sv.min())
+    idx = np.random.default_rng(7).choice(c.n, 4096, replace=False)
+    Zr = O.pca_project(Xh[idx], np64(mean), np64(comps))
+    assert_close(_rows(Z, idx), Zr, 1e-4, "projection (sampled rows)")
