@@ -288,9 +288,14 @@ __device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict
 // registers with zero fill.  Needs every row width (ld) and valid row count in the row
 // direction of a K-strided operand to be a multiple of 8 elements.
 
+// fp32 operands (F32) take the same path for contractions with both operands K-contiguous: the
+// engine stages 16-bit units (a float is two, every ld and K doubled), so a 64-byte row still
+// holds one stage, and each 16-byte fragment -- four consecutive K of one row -- feeds four
+// v_mfma_f32_16x16x4_f32, the lane group g supplying K = 4 g + q to the q-th of them.
 template <typename T, int BM_, int BN_, int WM_, int WN_, int NS_>
 struct CfgD {
   using type = T;
+  static constexpr bool F32 = sizeof(T) == 4;
   static constexpr bool DMA = true;
   static constexpr bool TRANS = true;  // accumulator element (i, j, r) at row 16 i + l % 16, col 16 j + 4 (l / 16) + r
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
@@ -298,11 +303,11 @@ struct CfgD {
   static constexpr int WAVES = WAVES_M * WAVES_N;
   static constexpr int THREADS = 64 * WAVES;
   static constexpr int MI = WM / 16, NJ = WN / 16;
-  static constexpr int BK = 32, NS = NS_;
+  static constexpr int BK = 32, NS = NS_;  // BK in 16-bit units (64-byte rows)
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int LDS = NS * STAGE;
-  static_assert(sizeof(T) == 2, "direct-to-LDS engine is bf16 only");
+  static_assert(sizeof(T) == 2 || sizeof(T) == 4, "bf16 or fp32 operands");
 };
 
 #ifndef HMOE_PINGPONG
@@ -314,6 +319,11 @@ struct CfgD {
 #endif
 
 typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
+typedef CfgD<float, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDmaF32;        // fp32, K-contiguous operands
+// fp32 with at most 64 columns (the gater's assignment, K <= 64): 128 x 64 tiles of four waves
+// and a 3-stage ring (36 KB), four workgroups per CU -- measured against 256 x 64 (4 stages:
+// 11% slower; 3 stages: 15%), 128 x 64 with 2 or 4 stages (10%, 8%) and 64 x 64 (17%)
+typedef CfgD<float, 128, 64, 32, 64, 3> CfgDmaF32Narrow;
 
 // 16-byte chunk swizzle of the 64-byte K-contiguous rows (used by the DMA slot mapping and the
 // operand reads alike).  Measured with the LDS bank-conflict counter on gfx950 for the MFMA
@@ -433,6 +443,27 @@ __device__ __forceinline__ void dma_read_frags(const lds<char>* bA, const lds<ch
 template <class C, bool ROWNORM>
 __device__ __forceinline__ void dma_mfmas(const bf16x8 (&a)[C::MI], const bf16x8 (&b)[C::NJ],
                                           floatx4 (&acc)[C::MI][C::NJ], float* xs) {
+  if constexpr (C::F32) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+        for (int j = 0; j < C::NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(floatx4, b[j])[q],
+                                                           __builtin_bit_cast(floatx4, a[i])[q], acc[i][j], 0, 0, 0);
+    if constexpr (ROWNORM) {
+      const int wn = (threadIdx.x >> 6) % C::WAVES_N;
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i)
+        if ((i % C::WAVES_N) == wn) {
+          const floatx4 v = __builtin_bit_cast(floatx4, a[i]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) xs[i] = fmaf(v[e], v[e], xs[i]);
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
 #pragma unroll
@@ -618,13 +649,26 @@ __device__ __forceinline__ void gemm_tile_dma(const bf16* __restrict__ A, int64_
   t.template run<ROWNORM>(smem, acc, xs);
 }
 
+// Whether C is a direct-to-LDS configuration with fp32 operands.
+template <class C>
+__device__ __host__ constexpr bool dma_f32() {
+  if constexpr (C::DMA)
+    return C::F32;
+  else
+    return false;
+}
+
 // Full K loop for one tile on whichever engine the configuration names.
 template <class C, bool A_KC, bool B_KC, bool ROWNORM = false>
 __device__ __forceinline__ void gemm_tile(const typename C::type* __restrict__ A, int64_t lda, int a_rows,
                                           const typename C::type* __restrict__ B, int64_t ldb, int b_rows,
                                           int k_len, lds<char>* smem, floatx4 (&acc)[C::MI][C::NJ],
                                           float* xs = nullptr) {
-  if constexpr (C::DMA) {
+  if constexpr (dma_f32<C>()) {
+    static_assert(A_KC && B_KC, "fp32 on the direct-to-LDS engine: K-contiguous operands only");
+    gemm_tile_dma<C, A_KC, B_KC, ROWNORM>(reinterpret_cast<const bf16*>(A), 2 * lda, a_rows,
+                                          reinterpret_cast<const bf16*>(B), 2 * ldb, b_rows, 2 * k_len, smem, acc, xs);
+  } else if constexpr (C::DMA) {
     gemm_tile_dma<C, A_KC, B_KC, ROWNORM>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc, xs);
   } else {
     gemm_tile_reg<C, A_KC, B_KC, ROWNORM>(A, lda, a_rows, B, ldb, b_rows, k_len, smem, acc, xs);

@@ -101,12 +101,14 @@ __global__ void __launch_bounds__(C::THREADS)
   }
 }
 
-// The same tile on the direct-to-LDS engine (bf16, many centres).  Each lane holds four
-// consecutive centres of one row per fragment; the row norms come from the A fragments the
-// engine already reads (fragment i summed by wave i mod WAVES_N).
+// The same tile on the direct-to-LDS engine (bf16 with many centres, and fp32).  Each lane
+// holds four consecutive centres of one row per fragment; the row norms come from the A
+// fragments the engine already reads (fragment i summed by wave i mod WAVES_N).  fp32 rows are
+// staged as 16-bit units (U per element).
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
-    k_assign_dma(const bf16* __restrict__ X, int64_t n, int d, const bf16* __restrict__ Cn, int K,
+    k_assign_dma(const typename C::type* __restrict__ X, int64_t n, int d, const typename C::type* __restrict__ Cn,
+                 int K,
                  const float* __restrict__ cn, int32_t* __restrict__ assign, float* __restrict__ min_dist,
                  float* __restrict__ part_v, int32_t* __restrict__ part_i, float* __restrict__ xnorm) {
   static_assert(C::DMA && C::TRANS, "direct-to-LDS configuration expected");
@@ -117,8 +119,12 @@ __global__ void __launch_bounds__(C::THREADS)
   floatx4 acc[C::MI][C::NJ];
   float xs[C::MI];
   // only the first centre tile of a row block needs the row norms (min_dist = min + |x|^2)
+  constexpr int U = C::F32 ? 2 : 1;
+  const bf16* Xu = reinterpret_cast<const bf16*>(X);
+  const bf16* Cu = reinterpret_cast<const bf16*>(Cn);
   DmaTile<C, true, true> pipe;
-  pipe.prime(X + tc.m0 * d, d, tc.m_rows, Cn + (int64_t)tc.n0 * d, d, tc.n_cols, d, smem);
+  pipe.prime(Xu + tc.m0 * d * U, (int64_t)d * U, tc.m_rows, Cu + (int64_t)tc.n0 * d * U, (int64_t)d * U, tc.n_cols,
+             d * U, smem);
   if (tc.n0 == 0)
     pipe.template run<true>(smem, acc, xs);
   else
@@ -201,7 +207,8 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
 // with many centres the 256 x 256 direct-to-LDS engine, the rest 128 x 128.
 static int assign_bn(hmoe_dtype_t dt, int32_t K) {
   if (K <= 64) return 64;
-  return (dt == HMOE_BF16 && K > 128) ? CfgDma::BN : 128;
+  if (dt != HMOE_BF16) return CfgDmaF32::BN;
+  return K > 128 ? CfgDma::BN : 128;
 }
 
 static size_t assign_ws_bytes(int64_t n, int32_t K, hmoe_dtype_t dt) {
@@ -254,8 +261,9 @@ int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const vo
       return assign_t<CfgDma>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
   }
-  if (bn == 64) return assign_t<CfgNarrow<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
-  return assign_t<CfgSmall<float>>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
+  if (bn == 64)
+    return assign_t<CfgDmaF32Narrow>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
+  return assign_t<CfgDmaF32>((const float*)X, n, d, (const float*)C, K, assign, min_dist, ws, st);
 }
 
 // ------------------------------------------------------------------ k-means++ seeding

@@ -380,7 +380,8 @@ size_t pca_project_ws(int d, int r, hmoe_dtype_t dt) {
 template <typename T>
 static int pca_project_t(const T* X, int64_t n, int d, const float* mean, const float* comps, int r, T* Zo,
                          Workspace& ws, hipStream_t st) {
-  using C = typename Pick<T>::C;
+  // both operands K-contiguous: the direct-to-LDS engine in either dtype
+  using C = typename std::conditional<sizeof(T) == 2, CfgDma, CfgDmaF32>::type;
   float* b = ws.take<float>(r);
   T* W = ws.take<T>((size_t)r * d);
   if (!ws.fits()) return HMOE_EWORKSPACE;
