@@ -324,6 +324,7 @@ typedef CfgD<float, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDmaF32;        // fp3
 // and a 3-stage ring (36 KB), four workgroups per CU -- measured against 256 x 64 (4 stages:
 // 11% slower; 3 stages: 15%), 128 x 64 with 2 or 4 stages (10%, 8%) and 64 x 64 (17%)
 typedef CfgD<float, 128, 64, 32, 64, 3> CfgDmaF32Narrow;
+typedef CfgD<bf16, 128, 64, 32, 64, 3> CfgDmaNarrow;
 
 // 16-byte chunk swizzle of the 64-byte K-contiguous rows (used by the DMA slot mapping and the
 // operand reads alike).  Measured with the LDS bank-conflict counter on gfx950 for the MFMA

@@ -203,8 +203,9 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
   if (min_dist) min_dist[row] = fmaxf(v + xnorm[row], 0.f);
 }
 
-// Centre-tile width of the assignment: up to 64 centres run the narrow 256 x 64 tiles, bf16
-// with many centres the 256 x 256 direct-to-LDS engine, the rest 128 x 128.
+// Centre-tile width of the assignment: up to 64 centres run the narrow 128 x 64 tiles of the
+// direct-to-LDS engine, fp32 above that and bf16 above 128 centres its 256 x 256 tiles, bf16
+// with 65 .. 128 centres the register-staged 128 x 128 tiles.
 static int assign_bn(hmoe_dtype_t dt, int32_t K) {
   if (K <= 64) return 64;
   if (dt != HMOE_BF16) return CfgDmaF32::BN;
@@ -256,7 +257,7 @@ int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const vo
                   float* min_dist, Workspace& ws, hipStream_t st) {
   const int bn = assign_bn(dt, K);
   if (dt == HMOE_BF16) {
-    if (bn == 64) return assign_t<CfgNarrow<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+    if (bn == 64) return assign_t<CfgDmaNarrow>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     if (bn == CfgDma::BN)
       return assign_t<CfgDma>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
