@@ -206,10 +206,13 @@ __global__ void __launch_bounds__(256) k_assign_merge(const float* __restrict__ 
 // Centre-tile width of the assignment: up to 64 centres run the narrow 128 x 64 tiles of the
 // direct-to-LDS engine, fp32 above that and bf16 above 128 centres its 256 x 256 tiles, bf16
 // with 65 .. 128 centres the register-staged 128 x 128 tiles.
+// bf16 with more than 128 centres
+typedef CfgDma CfgAssignWide;
+
 static int assign_bn(hmoe_dtype_t dt, int32_t K) {
   if (K <= 64) return 64;
   if (dt != HMOE_BF16) return CfgDmaF32::BN;
-  return K > 128 ? CfgDma::BN : 128;
+  return K > 128 ? CfgAssignWide::BN : 128;
 }
 
 static size_t assign_ws_bytes(int64_t n, int32_t K, hmoe_dtype_t dt) {
@@ -258,8 +261,8 @@ int launch_assign(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, const vo
   const int bn = assign_bn(dt, K);
   if (dt == HMOE_BF16) {
     if (bn == 64) return assign_t<CfgDmaNarrow>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
-    if (bn == CfgDma::BN)
-      return assign_t<CfgDma>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
+    if (K > 128)
+      return assign_t<CfgAssignWide>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
     return assign_t<CfgSmall<bf16>>((const bf16*)X, n, d, (const bf16*)C, K, assign, min_dist, ws, st);
   }
   if (bn == 64)
