@@ -132,6 +132,11 @@ def timer_report() -> dict:
     return out
 
 
+def _out(o, key, make):
+    """o[key] when the caller passed it, else a new tensor from make() (only then allocated)."""
+    return o[key] if key in o else make()
+
+
 def _chk(rc: int, what: str):
     if rc != 0:
         raise HmoeError(f"{what} failed ({rc}): {last_error()}")
@@ -247,15 +252,15 @@ def moe_dispatch(expert, K, rows=None, out=None, ws=None):
     n = expert.shape[0]
     dev = expert.device
     o = out or {}
-    counts = o.get("counts", torch.empty(K, dtype=torch.int32, device=dev))
-    offsets = o.get("offsets", torch.empty(K + 1, dtype=torch.int32, device=dev))
-    perm = o.get("perm", torch.empty(n, dtype=torch.int32, device=dev))
-    inv = o.get("inv", torch.empty(n, dtype=torch.int32, device=dev))
+    counts = _out(o, "counts", lambda: torch.empty(K, dtype=torch.int32, device=dev))
+    offsets = _out(o, "offsets", lambda: torch.empty(K + 1, dtype=torch.int32, device=dev))
+    perm = _out(o, "perm", lambda: torch.empty(n, dtype=torch.int32, device=dev))
+    inv = _out(o, "inv", lambda: torch.empty(n, dtype=torch.int32, device=dev))
     rows_sorted = None
     w = 0
     dt = F32
     if rows is not None:
-        rows_sorted = o.get("rows_sorted", torch.empty_like(rows))
+        rows_sorted = _out(o, "rows_sorted", lambda: torch.empty_like(rows))
         w = rows.shape[1]
         dt = _dt(rows)
     wsb, wb = _workspace(moe_dispatch_workspace(n, K), ws, dev)
@@ -305,11 +310,11 @@ def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=Non
     dev = X_sorted.device
     dt = X_sorted.dtype
     o = out or {}
-    H1s = o.get("H1_sorted", torch.empty(n, prm.d_hid, dtype=dt, device=dev))
-    H = o.get("H", torch.empty(n, prm.d_out, dtype=dt, device=dev))
-    lse = o.get("lse", torch.empty(n, dtype=torch.float32, device=dev))
-    loss = o.get("loss", torch.empty(n, dtype=torch.float32, device=dev))
-    lm = o.get("loss_mean", torch.empty(1, dtype=torch.float32, device=dev))
+    H1s = _out(o, "H1_sorted", lambda: torch.empty(n, prm.d_hid, dtype=dt, device=dev))
+    H = _out(o, "H", lambda: torch.empty(n, prm.d_out, dtype=dt, device=dev))
+    lse = _out(o, "lse", lambda: torch.empty(n, dtype=torch.float32, device=dev))
+    loss = _out(o, "loss", lambda: torch.empty(n, dtype=torch.float32, device=dev))
+    lm = _out(o, "loss_mean", lambda: torch.empty(1, dtype=torch.float32, device=dev))
     lg = o.get("logits")
     if lg is None and save_logits:
         lg = torch.empty(n, prm.vocab, dtype=dt, device=dev)
@@ -331,13 +336,13 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
     K, d, h, o_, V = prm.K, prm.d_in, prm.d_hid, prm.d_out, prm.vocab
     f32 = torch.float32
     o = out or {}
-    g = {"dW1": o.get("dW1", torch.empty(K, h, d, dtype=f32, device=dev)),
-         "db1": o.get("db1", torch.empty(K, h, dtype=f32, device=dev)),
-         "dW2": o.get("dW2", torch.empty(K, o_, h, dtype=f32, device=dev)),
-         "db2": o.get("db2", torch.empty(K, o_, dtype=f32, device=dev)),
-         "dD": o.get("dD", torch.empty(p["D"].shape, dtype=f32, device=dev)),
-         "dbD": o.get("dbD", torch.empty(p["D"].shape[:-1], dtype=f32, device=dev)),
-         "dX": (o.get("dX", torch.empty(n, d, dtype=X_sorted.dtype, device=dev))
+    g = {"dW1": _out(o, "dW1", lambda: torch.empty(K, h, d, dtype=f32, device=dev)),
+         "db1": _out(o, "db1", lambda: torch.empty(K, h, dtype=f32, device=dev)),
+         "dW2": _out(o, "dW2", lambda: torch.empty(K, o_, h, dtype=f32, device=dev)),
+         "db2": _out(o, "db2", lambda: torch.empty(K, o_, dtype=f32, device=dev)),
+         "dD": _out(o, "dD", lambda: torch.empty(p["D"].shape, dtype=f32, device=dev)),
+         "dbD": _out(o, "dbD", lambda: torch.empty(p["D"].shape[:-1], dtype=f32, device=dev)),
+         "dX": (_out(o, "dX", lambda: torch.empty(n, d, dtype=X_sorted.dtype, device=dev))
                 if want_dX else None)}
     lab = Labels(_ptr(row_ptr), _ptr(tag))
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
@@ -358,8 +363,10 @@ def topm(logits, m: int, out=None, want_values=False):
     n, V = logits.shape
     dev = logits.device
     o = out or {}
-    idx = o.get("idx", torch.empty(n, m, dtype=torch.int32, device=dev))
-    val = o.get("val", torch.empty(n, m, dtype=torch.float32, device=dev)) if want_values else None
+    idx = o["idx"] if "idx" in o else torch.empty(n, m, dtype=torch.int32, device=dev)
+    val = None
+    if want_values:
+        val = o["val"] if "val" in o else torch.empty(n, m, dtype=torch.float32, device=dev)
     _chk(lib().hmoe_topm(_ptr(logits), _dt(logits), n, V, m, _ptr(idx), _ptr(val), _stream()), "topm")
     return (idx, val) if want_values else idx
 

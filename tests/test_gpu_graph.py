@@ -77,3 +77,54 @@ def test_captured_step_replays_bit_identical():
         for k, v in eager.items():
             assert torch.equal(got[k], v), (rep, k)
         del junk
+
+
+def test_captured_inference_tail_and_update_replay_bit_identical():
+    # t_m with values, the p@m / q@m counts and an SGD step with momentum and a bf16 copy, all
+    # captured in one graph; SGD works in place, so every replay starts from restored weights
+    g = torch.Generator(device="cpu").manual_seed(11)
+    n, V, m, S = 700, 3000, 10, 5000
+    L = (torch.randn(n, V, generator=g) * 3).to(torch.bfloat16).cuda()
+    rp, tg = W.zipf_labels(n, V, 8, seed=12)
+    rp_t, tg_t = torch.as_tensor(rp).cuda(), torch.as_tensor(tg).cuda()
+    qs, qt = W.q_draws(rp, tg, S, seed=13)
+    qs_t, qt_t = torch.as_tensor(qs).cuda(), torch.as_tensor(qt).cuda()
+    w0 = torch.randn(100_003, generator=g).cuda()
+    gr = torch.randn(100_003, generator=g).cuda()
+    v0 = torch.randn(100_003, generator=g).cuda()
+    bufs = {"idx": torch.empty(n, m, dtype=torch.int32, device="cuda"),
+            "val": torch.empty(n, m, dtype=torch.float32, device="cuda"),
+            "hits": torch.empty(2, m, dtype=torch.int64, device="cuda"),
+            "w": w0.clone(), "v": v0.clone(), "wlo": torch.empty(100_003, dtype=torch.bfloat16, device="cuda")}
+
+    def run():
+        hmoe.topm(L, m, out=bufs, want_values=True)
+        hmoe.topm_hits(bufs["idx"], rp_t, tg_t, qs_t, qt_t, out=bufs["hits"])
+        hmoe.sgd_step(bufs["w"], gr, lr=0.05, weight_decay=1e-4, momentum=0.9, v=bufs["v"], w_lo=bufs["wlo"])
+
+    run()
+    torch.cuda.synchronize()
+    eager = {k: t.clone() for k, t in bufs.items()}
+    bufs["w"].copy_(w0)
+    bufs["v"].copy_(v0)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    for rep in range(3):
+        bufs["w"].copy_(w0)
+        bufs["v"].copy_(v0)
+        for k in ("idx", "hits"):
+            bufs[k].fill_(-1)
+        bufs["val"].fill_(float("nan"))
+        bufs["wlo"].fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in eager.items():
+            assert torch.equal(bufs[k], v), (rep, k)
