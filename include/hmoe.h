@@ -101,8 +101,10 @@ int hmoe_kmeans_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int
 
 /* Hard partition of a batch by expert (Section 2: each expert sees its own share of the
  * data, no balancing): a stable counting sort.
- *   expert: int32[n], 0 <= e < K (out-of-range ids are an error caught on the device:
- *     counts then do not sum to n).
+ *   expert: int32[n], 0 <= e < K.  The ids live in device memory, which the library does not
+ *     read back: out-of-range ids are the caller's error, and their rows are placed after
+ *     every expert's (offsets[K] stops before them, counts exclude them, so the counts do not
+ *     sum to n), perm and inv remaining permutations of all n rows.
  *   counts int32[K], offsets int32[K+1] (exclusive scan), perm int32[n] (slot -> sample),
  *   inv int32[n] (sample -> slot).
  *   rows [n x w] (dtype dt) and rows_sorted [n x w]: optional; when rows is non-NULL,
@@ -142,7 +144,11 @@ typedef struct {
  * (Section 4.1, Eq. 3, with the indicator spread uniformly over the positives). */
 typedef struct {
   const int32_t* row_ptr; /* int32[n+1] */
-  const int32_t* tag;     /* int32[nnz], 0 <= tag < vocab */
+  const int32_t* tag;     /* int32[nnz], 0 <= tag < vocab.  The labels live in device memory,
+                           * which the library does not read back to validate: a tag outside
+                           * [0, vocab) is never dereferenced, contributes a logit of 0 to the
+                           * loss and matches no column of the gradient (the result is then
+                           * not Eq. 3's). */
 } hmoe_labels_t;
 
 /* Forward pass of the hard mixture with the loss of Eq. 3.

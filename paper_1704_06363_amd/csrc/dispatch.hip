@@ -11,6 +11,10 @@
 //   scatter recomputes the peer masks and writes each id's slot = offsets[k] + earlier blocks
 //           + earlier waves + earlier chunks + rank among earlier peer lanes: the order of
 //           equal ids is the sample order, so the permutation is unique.
+// Ids outside [0, K) (an error of the caller's, which the device cannot report synchronously)
+// go to one more bucket, K, after every expert: counts exclude them, offsets[K] stops before
+// them, and perm / inv stay permutations of all n rows, so nothing downstream indexes outside
+// its buffers.
 #include "launch.hpp"
 #include "primitives.hpp"
 
@@ -41,10 +45,10 @@ __device__ __forceinline__ void wave_hist(const int32_t* __restrict__ e, int64_t
   for (int c = 0; c < 4; ++c) {
     const int64_t i = (int64_t)blockIdx.x * kIdsPerBlock + w * 256 + c * 64 + l;
     int id = i < n ? e[i] : -1;
-    bool valid = i < n;
+    const bool valid = i < n;
     if (valid && (id < 0 || id >= K)) {
       if (err) atomicOr(err, 1);
-      valid = false;
+      id = K;  // the bucket after every expert
     }
     const uint64_t peers = peer_mask(valid ? id : 0, valid, bits);
     if (valid && lane_rank(peers) == 0) atomicAdd(&hist_w[id], (int32_t)__popcll(peers));
@@ -54,23 +58,26 @@ __device__ __forceinline__ void wave_hist(const int32_t* __restrict__ e, int64_t
 __global__ void __launch_bounds__(256) k_dispatch_hist(const int32_t* __restrict__ e, int64_t n, int K,
                                                        int bits, int32_t* __restrict__ block_counts,
                                                        int32_t* __restrict__ err) {
-  extern __shared__ int32_t hist[];  // [4][K]
-  for (int k = threadIdx.x; k < 4 * K; k += 256) hist[k] = 0;
+  extern __shared__ int32_t hist[];  // [4][K + 1]
+  const int KB = K + 1;
+  for (int k = threadIdx.x; k < 4 * KB; k += 256) hist[k] = 0;
   __syncthreads();
-  wave_hist(e, n, K, bits, hist + (threadIdx.x >> 6) * K, err);
+  wave_hist(e, n, K, bits, hist + (threadIdx.x >> 6) * KB, err);
   __syncthreads();
-  for (int k = threadIdx.x; k < K; k += 256)
-    block_counts[(int64_t)k * gridDim.x + blockIdx.x] = hist[k] + hist[K + k] + hist[2 * K + k] + hist[3 * K + k];
+  for (int k = threadIdx.x; k < KB; k += 256)
+    block_counts[(int64_t)k * gridDim.x + blockIdx.x] =
+        hist[k] + hist[KB + k] + hist[2 * KB + k] + hist[3 * KB + k];
 }
 
 // One wave per expert k: exclusive prefix over the blocks of block_counts[k][*] (in place) and
 // counts[k] = its total.  Lane l scans a contiguous run of the blocks, the runs are combined by
 // a wave scan.
+// Buckets 0 .. K (K: the out-of-range ids); counts[k] is written for the K experts only.
 __global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ block_counts, int nb, int K,
                                                           int32_t* __restrict__ counts) {
   const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
-  if (k >= K) return;
+  if (k > K) return;
   int32_t* col = block_counts + (int64_t)k * nb;
   const int per = (nb + 63) / 64;
   const int b0 = l * per;
@@ -91,7 +98,7 @@ __global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ 
       col[b0 + q] = run;
       run += t;
     }
-  if (l == 63) counts[k] = inc;
+  if (l == 63 && k < K) counts[k] = inc;
 }
 
 __global__ void __launch_bounds__(1024) k_dispatch_offsets(const int32_t* __restrict__ counts, int K,
@@ -117,27 +124,29 @@ __global__ void __launch_bounds__(256) k_dispatch_scatter(const int32_t* __restr
                                                           const int32_t* __restrict__ offsets,
                                                           int32_t* __restrict__ perm,
                                                           int32_t* __restrict__ inv) {
-  extern __shared__ int32_t hist[];  // [4][K] -> per-wave running slot
-  for (int k = threadIdx.x; k < 4 * K; k += 256) hist[k] = 0;
+  extern __shared__ int32_t hist[];  // [4][K + 1] -> per-wave running slot
+  const int KB = K + 1;
+  for (int k = threadIdx.x; k < 4 * KB; k += 256) hist[k] = 0;
   __syncthreads();
   const int w = threadIdx.x >> 6;
-  wave_hist(e, n, K, bits, hist + w * K, nullptr);
+  wave_hist(e, n, K, bits, hist + w * KB, nullptr);
   __syncthreads();
-  for (int k = threadIdx.x; k < K; k += 256) {
-    int32_t run = offsets[k] + block_base[(int64_t)k * gridDim.x + blockIdx.x];
+  for (int k = threadIdx.x; k < KB; k += 256) {
+    int32_t run = offsets[k] + block_base[(int64_t)k * gridDim.x + blockIdx.x];  // offsets[K]: past the experts
     for (int q = 0; q < 4; ++q) {
-      const int32_t t = hist[q * K + k];
-      hist[q * K + k] = run;
+      const int32_t t = hist[q * KB + k];
+      hist[q * KB + k] = run;
       run += t;
     }
   }
   __syncthreads();
-  int32_t* slot_w = hist + w * K;
+  int32_t* slot_w = hist + w * KB;
   const int l = threadIdx.x & 63;
   for (int c = 0; c < 4; ++c) {
     const int64_t i = (int64_t)blockIdx.x * kIdsPerBlock + w * 256 + c * 64 + l;
     int id = i < n ? e[i] : -1;
-    const bool valid = i < n && id >= 0 && id < K;
+    const bool valid = i < n;
+    if (valid && (id < 0 || id >= K)) id = K;
     const uint64_t peers = peer_mask(valid ? id : 0, valid, bits);
     if (valid) {
       const int rank = lane_rank(peers);
@@ -147,8 +156,6 @@ __global__ void __launch_bounds__(256) k_dispatch_scatter(const int32_t* __restr
       // every peer has read slot_w[id] above (same wave, program order) before the leader
       // advances it for the next chunk
       if (rank == 0) atomicAdd(&slot_w[id], (int32_t)__popcll(peers));
-    } else if (i < n) {
-      inv[i] = -1;
     }
   }
 }
@@ -162,23 +169,23 @@ static int id_bits(int K) {
 size_t dispatch_ws(int64_t n, int32_t K) {
   Workspace ws(nullptr, 0);
   const int64_t nb = cdiv(n, kIdsPerBlock);
-  ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * K);
+  ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * (K + 1));
   return ws.off;
 }
 
 int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int32_t* offsets,
                     int32_t* perm, int32_t* inv, Workspace& ws, hipStream_t st) {
   const int64_t nb = cdiv(n, kIdsPerBlock);
-  int32_t* bc = ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * K);
+  int32_t* bc = ws.take<int32_t>((size_t)(nb > 0 ? nb : 1) * (K + 1));
   if (!ws.fits()) return HMOE_EWORKSPACE;
-  const int bits = id_bits(K);
-  const size_t lds = 4 * (size_t)K * sizeof(int32_t);
+  const int bits = id_bits(K + 1);  // ids 0 .. K (K: out of range)
+  const size_t lds = 4 * (size_t)(K + 1) * sizeof(int32_t);
   if (nb > 0) {
     HMOE_LAUNCH("dispatch hist", k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        (int32_t*)nullptr);
   }
-  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K, 4)), dim3(256), 0, st, bc, (int)nb, K,
-                     counts);
+  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K + 1, 4)), dim3(256), 0, st, bc, (int)nb,
+              K, counts);
   HMOE_LAUNCH("dispatch offsets", k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
   if (nb > 0) {
     HMOE_LAUNCH("dispatch scatter", k_dispatch_scatter, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,

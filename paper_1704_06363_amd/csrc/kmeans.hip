@@ -450,7 +450,8 @@ __global__ void __launch_bounds__(1024) k_reseed_scan(const int32_t* __restrict_
   float best = -1.f;
   int64_t bi = INT64_MAX;
   for (int64_t i = i0 + threadIdx.x; i < i1; i += 1024) {
-    if (counts32[assign[i]] <= 1) continue;
+    const int32_t a = assign[i];
+    if ((unsigned)a >= (unsigned)K || counts32[a] <= 1) continue;  // out-of-range ids are never donors
     const float v = d1[i];
     if (v > best || (v == best && i < bi)) {
       best = v;
@@ -516,7 +517,7 @@ __global__ void __launch_bounds__(1024) k_reseed(const T* __restrict__ X, int64_
       } else {
         for (int64_t i = threadIdx.x; i < n; i += 1024) {
           const int32_t a = __hip_atomic_load(assign + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if (cnt[a] <= 1) continue;
+          if ((unsigned)a >= (unsigned)K || cnt[a] <= 1) continue;
           const float v = d1[i];
           if (v > best || (v == best && i < bi)) {
             best = v;

@@ -404,7 +404,8 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
     for (int j0 = w * 8; j0 < cn; j0 += 32) {
       const int j = j0 + g;
       float sdot = 0.f;
-      if (j < cn) {
+      // a tag outside [0, V) is never dereferenced: its logit counts as 0
+      if (j < cn && (unsigned)s_ttag[j] < (unsigned)V) {
         const int t = s_trow[j];
         const int32_t tg = s_ttag[j];
         const T* h = H + (r0 + t) * o;
@@ -439,7 +440,8 @@ __global__ void __launch_bounds__(256) k_dec_loss(const float* __restrict__ pm, 
       sdot += shfl_xor(sdot, 1);
       if (j < cn && gl == 0) {
         const int t = s_trow[j];
-        s_dot[j] = sdot + (bD ? to_f32(bD[(int64_t)s_exp[t] * V + s_ttag[j]]) : 0.f);
+        const bool ok = (unsigned)s_ttag[j] < (unsigned)V;
+        s_dot[j] = sdot + ((bD && ok) ? to_f32(bD[(int64_t)s_exp[t] * V + s_ttag[j]]) : 0.f);
       }
     }
     __syncthreads();

@@ -157,3 +157,25 @@ def test_empty_batch():
                           torch.empty(0, device="cuda"), want_dX=False)
     for k in ("dW1", "dW2", "dD", "dbD"):
         assert torch.count_nonzero(g[k]) == 0
+
+
+def test_dispatch_out_of_range_ids():
+    # ids outside [0, K) are the caller's error: their rows go after every expert's, in sample
+    # order, the counts exclude them, and perm / inv stay permutations of all rows
+    K, n = 5, 3000
+    rs = np.random.default_rng(31)
+    ids = rs.integers(0, K, n).astype(np.int32)
+    bad = rs.choice(n, 40, replace=False)
+    ids[bad[:20]] = -1
+    ids[bad[20:]] = K + rs.integers(0, 3, 20)
+    X = torch.randn(n, 64, device="cuda").to(torch.bfloat16)
+    d = hmoe.moe_dispatch(torch.as_tensor(ids).cuda(), K, rows=X)
+    key = np.where((ids >= 0) & (ids < K), ids, K)
+    order = np.argsort(key, kind="stable")
+    assert npi(d["counts"]).tolist() == np.bincount(ids[key < K], minlength=K).tolist()
+    assert npi(d["offsets"]).tolist() == [0] + np.cumsum(np.bincount(ids[key < K], minlength=K)).tolist()
+    assert np.array_equal(npi(d["perm"]), order)
+    inv = np.empty(n, np.int64)
+    inv[order] = np.arange(n)
+    assert np.array_equal(npi(d["inv"]), inv)
+    assert torch.equal(d["rows_sorted"], X[torch.as_tensor(order).cuda()])
