@@ -115,9 +115,9 @@ int hmoe_moe_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* coun
                       void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* ws,
                       size_t ws_bytes, void* stream);
 
-/* Row gather out[r] = in[index[r]] for r < n (rows of w elements of dtype dt).  With
- * index = inv it combines expert-ordered rows back to sample order; with perm it
- * dispatches.  in and out must not overlap. */
+/* Row gather out[r] = in[index[r]] for r < n (rows of w elements of dtype dt; in has n rows
+ * too).  With index = inv it combines expert-ordered rows back to sample order; with perm it
+ * dispatches.  An index outside [0, n) gives a row of zeros.  in and out must not overlap. */
 int hmoe_permute_rows(const void* in, void* out, const int32_t* index, int64_t n, int32_t w,
                       hmoe_dtype_t dt, void* stream);
 

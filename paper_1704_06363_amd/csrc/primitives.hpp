@@ -219,7 +219,8 @@ static __global__ void __launch_bounds__(256) k_permute_rows(const i32x4* __rest
     const int64_t r = q / vpr;
     const int v = (int)(q - r * vpr);
     const int32_t s = index[r];
-    out[q] = s >= 0 ? in[(int64_t)s * vpr + v] : i32x4{0, 0, 0, 0};
+    // in has n rows too; an index outside [0, n) gives a zero row instead of a stray read
+    out[q] = (uint32_t)s < (uint64_t)n ? in[(int64_t)s * vpr + v] : i32x4{0, 0, 0, 0};
   }
 }
 

@@ -179,3 +179,10 @@ def test_dispatch_out_of_range_ids():
     inv[order] = np.arange(n)
     assert np.array_equal(npi(d["inv"]), inv)
     assert torch.equal(d["rows_sorted"], X[torch.as_tensor(order).cuda()])
+    # the row gather with indices outside [0, n): zero rows, the others gathered
+    idx = torch.as_tensor(order.astype(np.int32)).cuda()
+    idx[7], idx[100], idx[2999] = -5, n, 1 << 30
+    out = hmoe.permute_rows(X, idx)
+    ref = X[torch.as_tensor(order).cuda()].clone()
+    ref[[7, 100, 2999]] = 0
+    assert torch.equal(out, ref)
