@@ -1,0 +1,31 @@
+// Test driver for the PCA fit's host linear algebra (csrc/host_linalg.hpp): reads
+// "chol n a00 a01 ..." or "eig n a00 a01 ..." (row-major) on stdin and prints the result:
+// chol -> "ok" and R^{-1} (row-major) or "notpd"; eig -> the eigenvalues, then V^T (row-major).
+#include <stdio.h>
+#include <string.h>
+
+#include "host_linalg.hpp"
+
+int main() {
+  char mode[8];
+  int n;
+  if (scanf("%7s %d", mode, &n) != 2) return 2;
+  std::vector<double> A((size_t)n * n);
+  for (double& x : A)
+    if (scanf("%lf", &x) != 1) return 2;
+  if (strcmp(mode, "chol") == 0) {
+    std::vector<double> Ri;
+    if (!hmoe::chol_inverse(A, n, Ri)) {
+      printf("notpd\n");
+      return 0;
+    }
+    printf("ok\n");
+    for (double x : Ri) printf("%.17g\n", x);
+  } else {
+    std::vector<double> w, VT;
+    hmoe::sym_eigen(A, n, w, VT);
+    for (double x : w) printf("%.17g\n", x);
+    for (double x : VT) printf("%.17g\n", x);
+  }
+  return 0;
+}
