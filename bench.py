@@ -46,15 +46,29 @@ def log(*a):
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decoder_forward_hbm_traffic.md")
 
 
-def kernel_source_digest():
-    """sha256 over the HIP sources and the C header, so a traffic figure measured on older
-    kernels is recognised as stale."""
+def _code_only(text: str) -> str:
+    """The source without comments, trailing spaces or blank lines (a comment edit changes no
+    kernel)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines())
+    return "\n".join(ln for ln in lines if ln)
+
+
+def kernel_source_digest(read=None):
+    """sha256 over the HIP sources and the C header without their comments, so a traffic figure
+    measured on older kernels is recognised as stale.  `read(relative_path)` supplies the text
+    (default: the working tree)."""
+    src_rel = "paper_1704_06363_amd/csrc"
+    if read is None:
+        def read(rel):
+            with open(os.path.join(ROOT, rel), encoding="utf-8") as fh:
+                return fh.read()
+        files = sorted(f for f in os.listdir(os.path.join(ROOT, src_rel)) if f.endswith((".hip", ".hpp")))
+    else:
+        files = sorted(f for f in read(None) if f.endswith((".hip", ".hpp")))
     h = hashlib.sha256()
-    src = os.path.join(ROOT, "paper_1704_06363_amd", "csrc")
-    files = sorted(f for f in os.listdir(src) if f.endswith((".hip", ".hpp")))
-    for f in files + ["../../include/hmoe.h"]:
-        with open(os.path.join(src, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+    for rel in [f"{src_rel}/{f}" for f in files] + ["include/hmoe.h"]:
+        h.update(rel.encode() + b"\0" + _code_only(read(rel)).encode())
     return h.hexdigest()[:16]
 
 

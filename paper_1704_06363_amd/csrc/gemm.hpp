@@ -1,4 +1,7 @@
-// gemm.hpp -- MFMA tile engine shared by every dense contraction of the hot path.
+// gemm.hpp -- the MFMA tile engines shared by every dense contraction of the hot path: the
+// register-staged engine described first (Cfg) and the direct-to-LDS engine further down
+// (CfgD), which runs the bf16 MoE contractions, the larger assignments and the fp32
+// contractions with K-contiguous operands.
 //
 // C[m, n] = sum_k A(m, k) * B(n, k) over one BM x BN output tile per workgroup, split into
 // (BM/WM) x (BN/WN) wavefronts of WM x WN.  Operands are staged through LDS in a row-major,
@@ -265,10 +268,10 @@ __device__ __forceinline__ void gemm_tile_reg(const typename C::type* __restrict
   }
 }
 
-// ------------------------------------------------------------------ direct-to-LDS engine (bf16)
+// ------------------------------------------------------------------ direct-to-LDS engine
 //
-// The same BM x BN tile and wave split, but operands travel from HBM to LDS without passing
-// through registers: global_load_lds_dwordx4 writes lane l's 16 bytes to LDS at (wave-uniform
+// The same BM x BN tile and wave split (bf16; fp32 for K-contiguous operands, see CfgD), but
+// operands travel from HBM to LDS without passing through registers: global_load_lds_dwordx4 writes lane l's 16 bytes to LDS at (wave-uniform
 // base) + 16 l, so the LDS layout -- including its bank swizzle -- is chosen by the global
 // address each lane loads.  A stage covers 32 K (64 bytes per row); NS stages form a ring and
 // the loads for stage kt + NS - 1 are issued while stage kt feeds the MFMAs, each wave waiting
