@@ -195,7 +195,8 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
  *   decreasing eigenvalue order, each row's largest-magnitude entry positive; eigvals float[r]
  *   out.  Subspace iteration: n_iter steps Q <- orth(C Q) from a start drawn from `seed`, then
  *   Rayleigh-Ritz; a component's accuracy depends on the gap between its eigenvalue and the
- *   (r+1)-th.  X [n x d] in dtype dt; n >= 2, 8 <= r <= d, r and d multiples of 8.  The
+ *   (r+1)-th.  A covariance of rank below r (fewer independent directions, or n <= r) gives
+ *   eigenvalues ~0 for the rest, with any orthonormal completion as their components.  X [n x d] in dtype dt; n >= 2, 8 <= r <= d, r and d multiples of 8.  The
  *   d x d x r work runs on the GPU and the r x r factorisations on the host (fp64), so the call
  *   synchronises `stream` (a preprocessing step; not for graph capture).  Device pointers
  *   throughout (eigvals too).

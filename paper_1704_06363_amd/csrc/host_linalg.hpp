@@ -25,10 +25,15 @@ inline double dot_f64(const double* a, const double* b, int n) {
 // S = L L^T (L lower triangular, row-major, built row by row from contiguous dot products);
 // returns R^{-1} for R = L^T in Ri (upper triangular, row-major): row j of R^{-1} is column j of
 // L^{-1}, the forward solve of L x = e_j.  False when S is not positive definite even after a
-// tiny diagonal shift.
-inline bool chol_inverse(const std::vector<double>& S, int r, std::vector<double>& Ri) {
-  double tr = 0.0;
-  for (int i = 0; i < r; ++i) tr += S[(size_t)i * r + i];
+// tiny diagonal shift, or when a pivot (before its square root) is at most min_rel_pivot times
+// the largest diagonal entry of S (the columns behind S have lost rank to that precision).
+inline bool chol_inverse(const std::vector<double>& S, int r, std::vector<double>& Ri,
+                         double min_rel_pivot = 0.0) {
+  double tr = 0.0, dmax = 0.0;
+  for (int i = 0; i < r; ++i) {
+    tr += S[(size_t)i * r + i];
+    dmax = S[(size_t)i * r + i] > dmax ? S[(size_t)i * r + i] : dmax;
+  }
   const double shift = 1e-12 * tr / r;
   std::vector<double> L((size_t)r * r, 0.0);
   for (int i = 0; i < r; ++i) {
@@ -37,7 +42,7 @@ inline bool chol_inverse(const std::vector<double>& S, int r, std::vector<double
       const double* Lj = &L[(size_t)j * r];
       const double v = S[(size_t)i * r + j] + (i == j ? shift : 0.0) - dot_f64(Li, Lj, j);
       if (i == j) {
-        if (!(v > 0.0)) return false;
+        if (!(v > 0.0) || !(v > min_rel_pivot * dmax)) return false;
         Li[i] = sqrt(v);
       } else {
         Li[j] = v / Lj[j];

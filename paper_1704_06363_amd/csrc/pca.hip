@@ -49,6 +49,19 @@ static __global__ void __launch_bounds__(256) k_pca_start(float* __restrict__ Q,
   Q[q] = (float)((double)(z >> 11) * (1.0 / 9007199254740992.0) * 2.0 - 1.0);
 }
 
+// Fresh directions for the columns of Z [d][r] that flags[] marks (rank lost): uniform in
+// [-1, 1) from SplitMix64 of seed + index, as k_pca_start.
+static __global__ void __launch_bounds__(256) k_pca_refill(float* __restrict__ Z, int d, int r,
+                                                           const int32_t* __restrict__ flags, uint64_t seed) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= (int64_t)d * r || !flags[q % r]) return;
+  uint64_t z = seed + (uint64_t)q + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  Z[q] = (float)((double)(z >> 11) * (1.0 / 9007199254740992.0) * 2.0 - 1.0);
+}
+
 // comps[j][:] = sign_j U[:, j], sign_j making the largest-magnitude entry of the column positive
 // (lowest index on ties).  One block per column.
 static __global__ void __launch_bounds__(256) k_pca_comps(const float* __restrict__ U, int d, int r,
@@ -141,18 +154,47 @@ static int h2d(void* dst, const void* src, size_t bytes, hipStream_t st) {
 
 // Q <- Q R^{-1} with Q^T Q = R^T R (CholeskyQR), `passes` times (the second pass restores the
 // orthonormality the fp32 Gram matrix loses on an ill-conditioned Q); Z is scratch of Q's size.
-static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* Rinv, int passes, Workspace& ws,
-                          hipStream_t st) {
+// Rank-revealing: when a pivot falls below 1e-9 of the largest diagonal of Q^T Q (the fp32
+// Gram matrix's noise; a covariance of rank below r does this), Q is rebuilt from the
+// eigenpairs (w_j, v_j) of Q^T Q -- column j = Q v_j / sqrt(w_j) where w_j stays above that
+// level, a fresh seeded random column where it does not -- and the passes start again.  The
+// kept columns span what Q determined; the fresh ones lie outside it with probability 1.
+static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* Rinv, int passes, uint64_t seed,
+                          Workspace& ws, hipStream_t st) {
+  constexpr double kRank = 1e-9;
   std::vector<float> hs((size_t)r * r);
   std::vector<double> Sd((size_t)r * r), Ri;
+  int refills = 0;
   for (int pass = 0; pass < passes; ++pass) {
     const size_t mark = ws.off;
     HMOE_TRY(launch_gemm_tn<float>(Q, Q, d, r, r, S, ws, st));
     HMOE_TRY(d2h(hs.data(), S, hs.size() * sizeof(float), st));
     for (size_t i = 0; i < hs.size(); ++i) Sd[i] = hs[i];
-    if (!chol_inverse(Sd, r, Ri)) {
-      set_error("pca: the subspace lost rank (is the covariance's rank below r?)");
-      return HMOE_EINVAL;
+    if (!chol_inverse(Sd, r, Ri, kRank)) {
+      if (++refills > 4) {
+        set_error("pca: could not complete an orthonormal basis of %d columns", r);
+        return HMOE_EINVAL;
+      }
+      std::vector<double> A = Sd, w, VT;
+      sym_eigen(A, r, w, VT);
+      double wmax = 0.0;
+      for (double x : w) wmax = x > wmax ? x : wmax;
+      std::vector<int32_t> flags(r, 0);
+      for (int j = 0; j < r; ++j) {
+        const bool keep = wmax > 0.0 && w[j] > kRank * wmax;
+        const double sc = keep ? 1.0 / sqrt(w[j]) : 0.0;
+        for (int i = 0; i < r; ++i) hs[(size_t)i * r + j] = (float)(VT[(size_t)j * r + i] * sc);
+        flags[j] = keep ? 0 : 1;
+      }
+      HMOE_TRY(h2d(Rinv, hs.data(), hs.size() * sizeof(float), st));
+      HMOE_TRY(launch_gemm_nn<float>(Q, Rinv, d, r, r, Z, ws, st));
+      ws.off = mark;
+      HMOE_TRY(h2d(S, flags.data(), flags.size() * sizeof(int32_t), st));  // S is free until the next pass
+      HMOE_LAUNCH("pca refill", k_pca_refill, dim3((unsigned)cdiv((int64_t)d * r, 256)), dim3(256), 0, st, Z, d, r,
+                  (const int32_t*)S, seed + 0x5851F42D4C957F2Dull * (uint64_t)refills);
+      std::swap(Q, Z);
+      pass = -1;  // orthonormalise the rebuilt block from scratch
+      continue;
     }
     for (size_t i = 0; i < hs.size(); ++i) hs[i] = (float)Ri[i];
     HMOE_TRY(h2d(Rinv, hs.data(), hs.size() * sizeof(float), st));
@@ -200,12 +242,13 @@ static int pca_fit_t(const T* X, int64_t n, int d, int r, int n_iter, uint64_t s
               (int64_t)d * r, seed);
   // one CholeskyQR pass per iteration keeps the subspace; the basis that enters Rayleigh-Ritz
   // gets two
-  HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, n_iter == 0 ? 2 : 1, ws, st));
+  HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, n_iter == 0 ? 2 : 1, seed ^ 0xA5A5A5A5u, ws, st));
   for (int it = 0; it < n_iter; ++it) {
     HMOE_TRY(launch_gemm_nn<float>(Cv, Q, d, d, r, Z, ws, st));
     ws.off = mark;
     std::swap(Q, Z);
-    HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, it == n_iter - 1 ? 2 : 1, ws, st));
+    HMOE_TRY(orthonormalise(Q, Z, d, r, S, Rinv, it == n_iter - 1 ? 2 : 1, seed + 0x9E3779B9u * (uint64_t)(it + 1), ws,
+                            st));
   }
   // Rayleigh-Ritz: the eigenpairs of Q^T C Q, sorted by decreasing eigenvalue
   HMOE_TRY(launch_gemm_nn<float>(Cv, Q, d, d, r, Z, ws, st));

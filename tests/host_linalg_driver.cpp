@@ -1,6 +1,7 @@
 // Test driver for the PCA fit's host linear algebra (csrc/host_linalg.hpp): reads
-// "chol n a00 a01 ..." or "eig n a00 a01 ..." (row-major) on stdin and prints the result:
-// chol -> "ok" and R^{-1} (row-major) or "notpd"; eig -> the eigenvalues, then V^T (row-major).
+// "chol n a00 a01 ...", "cholr n ..." (a pivot threshold of 1e-9 of the largest diagonal) or
+// "eig n a00 a01 ..." (row-major) on stdin and prints the result: chol / cholr -> "ok" and
+// R^{-1} (row-major) or "notpd"; eig -> the eigenvalues, then V^T (row-major).
 #include <stdio.h>
 #include <string.h>
 
@@ -13,9 +14,9 @@ int main() {
   std::vector<double> A((size_t)n * n);
   for (double& x : A)
     if (scanf("%lf", &x) != 1) return 2;
-  if (strcmp(mode, "chol") == 0) {
+  if (strcmp(mode, "chol") == 0 || strcmp(mode, "cholr") == 0) {
     std::vector<double> Ri;
-    if (!hmoe::chol_inverse(A, n, Ri)) {
+    if (!hmoe::chol_inverse(A, n, Ri, strcmp(mode, "cholr") == 0 ? 1e-9 : 0.0)) {
       printf("notpd\n");
       return 0;
     }

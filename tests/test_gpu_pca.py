@@ -61,6 +61,30 @@ def test_gater_width_mixture():
     assert s.min() > 0.99, s.min()
 
 
+@pytest.mark.parametrize("n,d,rank,r", [(5000, 64, 3, 8), (2000, 32, 20, 32), (3, 16, 2, 8)])
+def test_covariance_rank_below_r(n, d, rank, r):
+    # the method's degenerate case: fewer independent directions than components (n = 3 rows
+    # included).  The leading `rank` pairs match the oracle, the others have eigenvalue ~0 and
+    # any orthonormal completion is right: every component must be orthonormal to the rest and
+    # an eigenvector of the fp64 covariance.
+    g = torch.Generator(device="cpu").manual_seed(n + d)
+    B = torch.randn(rank, d, generator=g, dtype=torch.float64)
+    X = (torch.randn(n, rank, generator=g, dtype=torch.float64) * torch.linspace(5, 1, rank, dtype=torch.float64)) @ B
+    X = (X + torch.randn(d, generator=g, dtype=torch.float64)).float().cuda()
+    mean, comps, ev = hmoe.pca_fit(X, r, n_iter=30, seed=4)
+    Xh = np64(X)
+    m_ref, c_ref, e_ref = O.pca(Xh, r)
+    k = min(rank, n - 1)
+    U, w = np64(comps), np64(ev)
+    assert_close(ev[:k], e_ref[:k], 1e-3, "leading eigenvalues")
+    assert np.abs(w[k:]).max() <= 1e-5 * e_ref[0]
+    assert np.abs(U @ U.T - np.eye(r)).max() <= 1e-4
+    cos = np.abs(np.sum(U[:k] * c_ref[:k], axis=1))
+    assert cos.min() > 0.999, cos.min()
+    Cov = np.cov(Xh, rowvar=False)
+    assert np.linalg.norm(Cov @ U.T - U.T * w, axis=0).max() <= 1e-4 * e_ref[0]
+
+
 def test_argument_errors():
     X = torch.zeros(10, 64, device="cuda")
     with pytest.raises(hmoe.HmoeError, match="exceeds"):

@@ -74,3 +74,14 @@ def test_chol_inverse_matches_lapack(driver, n):
 def test_chol_inverse_rejects_indefinite(driver):
     S = np.diag([1.0, -1.0, 2.0])
     assert _run(driver, "chol", S)[0] == "notpd"
+
+
+def test_chol_inverse_pivot_threshold(driver):
+    # a Gram matrix of 8 columns spanning only 5 directions (in fp32 noise): rejected at the
+    # 1e-9 relative pivot threshold the PCA fit uses to detect lost rank, accepted without it
+    rs = np.random.default_rng(9)
+    B = rs.standard_normal((40, 5)) @ rs.standard_normal((5, 8))
+    S = (B.T @ B).astype(np.float32).astype(np.float64)
+    assert _run(driver, "cholr", S)[0] == "notpd"
+    full = rs.standard_normal((40, 8))
+    assert _run(driver, "cholr", full.T @ full)[0] == "ok"
