@@ -54,21 +54,27 @@ def _code_only(text: str) -> str:
     return "\n".join(ln for ln in lines if ln)
 
 
-def kernel_source_digest(read=None):
-    """sha256 over the HIP sources and the C header without their comments, so a traffic figure
-    measured on older kernels is recognised as stale.  `read(relative_path)` supplies the text
-    (default: the working tree)."""
+def kernel_source_digest(read=None, unit="moe.hip"):
+    """sha256 over the translation unit that builds the dominant kernel (csrc/moe.hip), the
+    headers it includes (recursively) and the C header, without their comments, so a traffic
+    figure measured on older kernels is recognised as stale while edits elsewhere (or to
+    comments) do not retire it.  `read(relative_path)` supplies the text (default: the tree)."""
     src_rel = "paper_1704_06363_amd/csrc"
     if read is None:
         def read(rel):
             with open(os.path.join(ROOT, rel), encoding="utf-8") as fh:
                 return fh.read()
-        files = sorted(f for f in os.listdir(os.path.join(ROOT, src_rel)) if f.endswith((".hip", ".hpp")))
-    else:
-        files = sorted(f for f in read(None) if f.endswith((".hip", ".hpp")))
+    texts, todo = {}, [f"{src_rel}/{unit}"]
+    while todo:
+        rel = todo.pop()
+        if rel in texts:
+            continue
+        texts[rel] = read(rel)
+        for name in re.findall(r'^\s*#\s*include\s+"([^"]+)"', texts[rel], flags=re.M):
+            todo.append(f"include/{name}" if name == "hmoe.h" else f"{src_rel}/{name}")
     h = hashlib.sha256()
-    for rel in [f"{src_rel}/{f}" for f in files] + ["include/hmoe.h"]:
-        h.update(rel.encode() + b"\0" + _code_only(read(rel)).encode())
+    for rel in sorted(texts):
+        h.update(rel.encode() + b"\0" + _code_only(texts[rel]).encode())
     return h.hexdigest()[:16]
 
 
