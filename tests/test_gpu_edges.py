@@ -120,7 +120,7 @@ def test_largest_K_assign_and_dispatch():
     assert np.array_equal(npi(dd["perm"]), perm) and np.array_equal(npi(dd["inv"]), inv)
 
 
-@pytest.mark.parametrize("dtype,K", [("f32", 40), ("bf16", 40), ("bf16", 100), ("bf16", 600)])
+@pytest.mark.parametrize("dtype,K", [("f32", 40), ("f32", 300), ("bf16", 40), ("bf16", 100), ("bf16", 600)])
 def test_duplicated_centres_break_ties_low(dtype, K):
     # centre 2j+1 is an exact copy of centre 2j: identical distances, so the lower index wins
     # on every row (the oracle's near-tie exemption would skip these rows, so check directly)
@@ -161,3 +161,15 @@ def test_reseed_search_across_blocks():
     assert npi(cnt).tolist() == counts_ref.tolist()
     assert np.array_equal(npi(a), a2_ref)
     assert_close(C, O.round_store(C_ref, "f32"), 1e-6, "centres")
+
+
+@pytest.mark.parametrize("dtype,K", [("f32", 64), ("f32", 300), ("bf16", 64), ("bf16", 300)])
+def test_assign_4096_wide_features(dtype, K):
+    # the paper's wider gater features (4096, an AlexNet layer) on the narrow and wide tiles
+    n, d = 3000, 4096
+    X = W.gmm_features(n, d, 32, seed=80, dtype=dtype, device="cuda")
+    C = W.gmm_features(K, d, 32, seed=81, dtype=dtype, device="cuda")
+    a, md = hmoe.kmeans_assign(X, C)
+    a_ref, d1, d2 = O.assign(np64(X), np64(C))
+    assert_assign(a, a_ref, d1, d2)
+    assert_close(md, d1, 1e-4, "min_dist")

@@ -85,6 +85,26 @@ def test_covariance_rank_below_r(n, d, rank, r):
     assert np.linalg.norm(Cov @ U.T - U.T * w, axis=0).max() <= 1e-4 * e_ref[0]
 
 
+def test_fit_4096_wide_features():
+    # 4096-wide features (an AlexNet layer) to 256 components: spiked data whose leading 64
+    # directions are well separated; the rest of the 256 sit on a flat noise floor, compared
+    # through the residual against the fp64 covariance
+    n, d, r, lead = 8192, 4096, 256, 64
+    X = _spiked(n, d, lead, seed=90, dtype="f32")
+    mean, comps, ev = hmoe.pca_fit(X, r, n_iter=20, seed=5)
+    Xh = np64(X)
+    m_ref, c_ref, e_ref = O.pca(Xh, r)
+    assert_close(mean, m_ref, 1e-5, "mean")
+    assert_close(ev[:lead], e_ref[:lead], 1e-3, "leading eigenvalues")
+    assert_close(comps[:lead], c_ref[:lead], 1e-2, "leading components")
+    U = np64(comps)
+    assert np.abs(U @ U.T - np.eye(r)).max() <= 1e-4
+    Z = hmoe.pca_project(X, mean, comps)
+    idx = np.random.default_rng(91).choice(n, 512, replace=False)
+    Zr = O.pca_project(Xh[idx], np64(mean), U)
+    assert_close(np64(Z)[idx], Zr, 1e-4, "projection (sampled rows)")
+
+
 def test_argument_errors():
     X = torch.zeros(10, 64, device="cuda")
     with pytest.raises(hmoe.HmoeError, match="exceeds"):
