@@ -5,6 +5,7 @@
 
 #include <math.h>
 
+#include <thread>
 #include <vector>
 
 namespace hmoe {
@@ -49,13 +50,24 @@ inline bool chol_inverse(const std::vector<double>& S, int r, std::vector<double
       }
     }
   }
+  // the columns of L^{-1} are independent solves: spread over a few threads (column j costs
+  // ~(r - j)^2 / 2, so thread t takes j = t, t + T, ... to balance them); each result is the
+  // same as the serial solve's
   Ri.assign((size_t)r * r, 0.0);
-  std::vector<double> x(r);
-  for (int j = 0; j < r; ++j) {
-    x[j] = 1.0 / L[(size_t)j * r + j];
-    for (int i = j + 1; i < r; ++i) x[i] = -dot_f64(&L[(size_t)i * r + j], &x[j], i - j) / L[(size_t)i * r + i];
-    for (int i = j; i < r; ++i) Ri[(size_t)j * r + i] = x[i];
-  }
+  auto solve = [&](int t, int T) {
+    std::vector<double> x(r);
+    for (int j = t; j < r; j += T) {
+      x[j] = 1.0 / L[(size_t)j * r + j];
+      for (int i = j + 1; i < r; ++i) x[i] = -dot_f64(&L[(size_t)i * r + j], &x[j], i - j) / L[(size_t)i * r + i];
+      for (int i = j; i < r; ++i) Ri[(size_t)j * r + i] = x[i];
+    }
+  };
+  const unsigned hw = std::thread::hardware_concurrency();
+  const int T = r >= 64 ? (int)(hw < 2 ? 1 : (hw > 8 ? 8 : hw)) : 1;
+  std::vector<std::thread> pool;
+  for (int t = 1; t < T; ++t) pool.emplace_back(solve, t, T);
+  solve(0, T);
+  for (std::thread& th : pool) th.join();
   return true;
 }
 

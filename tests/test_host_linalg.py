@@ -17,7 +17,7 @@ def driver(tmp_path_factory):
     if shutil.which("g++") is None:
         pytest.skip("g++ not available")
     exe = str(tmp_path_factory.mktemp("hla") / "host_linalg_driver")
-    subprocess.run(["g++", "-O2", "-std=c++17", "-I", os.path.join(ROOT, "paper_1704_06363_amd", "csrc"),
+    subprocess.run(["g++", "-O2", "-std=c++17", "-pthread", "-I", os.path.join(ROOT, "paper_1704_06363_amd", "csrc"),
                     os.path.join(ROOT, "tests", "host_linalg_driver.cpp"), "-o", exe], check=True)
     return exe
 
