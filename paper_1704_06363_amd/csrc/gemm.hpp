@@ -521,17 +521,42 @@ __device__ __forceinline__ void wait_stage(int pending_stages) {
 //            that issued exactly X further memory operations (per wave) between prime() and
 //            run() when after_prime is true: the waits for the primed stages let those X stay
 //            in flight instead of draining them first.
-template <class C, bool A_KC, bool B_KC>
+// A_SW > 0: A is K-contiguous and stored slab-major -- K split into slabs of A_SW columns,
+// slab s of every row at A + s a_sstride (a_sstride = rows x A_SW), lda = A_SW within a slab
+// -- so each stage's loads start from the base of the slab that holds it (A_SW is a multiple
+// of BK, so no stage straddles two slabs).  Set the stride with slab_a() before prime().
+template <class C, bool A_KC, bool B_KC, int A_SW = 0>
 struct DmaTile {
   using OA = DmaOperand<C::BM, C::THREADS, A_KC>;
   using OB = DmaOperand<C::BN, C::THREADS, B_KC>;
   static constexpr int LOADS = OA::NQ + OB::NQ;
+  static constexpr bool SLAB_A = A_SW > 0;
+  static_assert(!SLAB_A || (A_KC && A_SW % C::BK == 0), "slab-major A: K-contiguous, whole stages per slab");
   OA oa;
   OB ob;
   const bf16* A;
   const bf16* B;
   int64_t lda, ldb;
   int k_len;
+  int64_t a_sstride = 0;
+
+  __device__ __forceinline__ void slab_a(int64_t stride) { a_sstride = stride; }
+  __device__ __forceinline__ void issue_a(int k0, lds<char>* buf) const {
+    if constexpr (SLAB_A) {
+      const int sl = k0 / A_SW;
+      oa.issue(A + sl * a_sstride, lda, k0 - sl * A_SW, buf);
+    } else {
+      oa.issue(A, lda, k0, buf);
+    }
+  }
+  __device__ __forceinline__ void tail_a(int k0, lds<char>* buf) const {
+    if constexpr (SLAB_A) {
+      const int sl = k0 / A_SW;
+      oa.tail(A + sl * a_sstride, lda, k0 - sl * A_SW, k_len - sl * A_SW, buf);
+    } else {
+      oa.tail(A, lda, k0, k_len, buf);
+    }
+  }
 
   __device__ __forceinline__ static lds<char>* bufA(lds<char>* smem, int s) { return smem + s * C::STAGE; }
   __device__ __forceinline__ static lds<char>* bufB(lds<char>* smem, int s) {
@@ -552,7 +577,7 @@ struct DmaTile {
 #pragma unroll
     for (int s = 0; s < C::NS - 1; ++s)
       if (s < nfull) {
-        oa.issue(A, lda, s * C::BK, bufA(smem, s));
+        issue_a(s * C::BK, bufA(smem, s));
         ob.issue(B, ldb, s * C::BK, bufB(smem, s));
       }
   }
@@ -609,7 +634,7 @@ struct DmaTile {
         dma_read_frags<C, A_KC, B_KC>(bufA(smem, sc), bufB(smem, sc), fa, fb);
         const int nx = kt + C::NS - 1;
         if (nx < nfull) {
-          oa.issue(A, lda, nx * C::BK, bufA(smem, nx % C::NS));
+          issue_a(nx * C::BK, bufA(smem, nx % C::NS));
           ob.issue(B, ldb, nx * C::BK, bufB(smem, nx % C::NS));
         }
         if (g1 && kt + 1 < nfull) wait_own(kt + 1);
@@ -625,7 +650,7 @@ struct DmaTile {
         const int nx = kt + C::NS - 1;
         if (nx < nfull) {
           const int sb = nx % C::NS;
-          oa.issue(A, lda, nx * C::BK, bufA(smem, sb));
+          issue_a(nx * C::BK, bufA(smem, sb));
           ob.issue(B, ldb, nx * C::BK, bufB(smem, sb));
         }
         const int sc = kt % C::NS;
@@ -634,7 +659,7 @@ struct DmaTile {
     }
     if (nfull * C::BK < k_len) {
       const int sb = nfull % C::NS;
-      oa.tail(A, lda, nfull * C::BK, k_len, bufA(smem, sb));
+      tail_a(nfull * C::BK, bufA(smem, sb));
       ob.tail(B, ldb, nfull * C::BK, k_len, bufB(smem, sb));
       wg_barrier_lds();
       dma_mfma_stage<C, A_KC, B_KC, ROWNORM>(bufA(smem, sb), bufB(smem, sb), acc, xs);

@@ -623,7 +623,7 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
                                                        float inv_n, const int32_t* __restrict__ perm,
                                                        const int32_t* __restrict__ seg,
                                                        const int32_t* __restrict__ piece_start, int NG,
-                                                       T* __restrict__ G, float* __restrict__ part_db) {
+                                                       T* __restrict__ G, float* __restrict__ part_db, int slab) {
   constexpr int EPV = 16 / sizeof(T);
   constexpr int MAXT = 16;
   constexpr float kLog2e = 1.4426950408889634f;
@@ -712,7 +712,9 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
         cs[e] += g[e];
         ov[e] = from_f32<T>(g[e]);
       }
-      __builtin_nontemporal_store(outv, reinterpret_cast<i32x4*>(G + (r0 + t) * V + c0));
+      // slab-major G ([column slab][n][256 EPV]): a block's stores fill one contiguous run
+      T* gdst = slab ? G + ((int64_t)blockIdx.y * n + (r0 + t)) * (256 * EPV) + cl : G + (r0 + t) * V + c0;
+      __builtin_nontemporal_store(outv, reinterpret_cast<i32x4*>(gdst));
     }
   }
   float* dst = part_db + (int64_t)blockIdx.x * V + c0;
@@ -742,8 +744,9 @@ __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ 
   out[c] = s;
 }
 
-// dH = G D, written to expert order: dYs[inv[i]] = (G D)[i].
-template <class C>
+// dH = G D, written to expert order: dYs[inv[i]] = (G D)[i].  GW > 0: G is slab-major, [V / GW
+// slabs][n][GW] (direct-to-LDS engine only).
+template <class C, int GW = 0>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_dH(const typename C::type* __restrict__ G, const typename C::type* __restrict__ D, int64_t n, int V, int o,
              const int32_t* __restrict__ inv, typename C::type* __restrict__ dYs) {
@@ -753,7 +756,15 @@ __global__ void __launch_bounds__(C::THREADS)
   const TileCoord tc = tile_plain<C>(n, o, V);
   if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
-  gemm_tile<C, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
+  if constexpr (GW > 0) {
+    static_assert(C::DMA, "slab-major G on the direct-to-LDS engine");
+    DmaTile<C, true, false, GW> pipe;
+    pipe.slab_a(n * GW);
+    pipe.prime(G + tc.m0 * GW, GW, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem);
+    pipe.run(smem, acc);
+  } else {
+    gemm_tile<C, true, false>(G + tc.m0 * V, V, tc.m_rows, D + tc.n0, o, tc.n_cols, V, smem, acc);
+  }
   store_out<C, T>(tc, acc, smem, dYs, o, Ident{}, RowVia{inv, tc.m0}, NoVec{});
 }
 
@@ -769,16 +780,20 @@ template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_gemm_tn_split(const typename C::type* __restrict__ A, const typename C::type* __restrict__ B, int64_t rows,
                     int M, int N, float* __restrict__ out, int64_t t_full, int split, int64_t chunk,
-                    float* __restrict__ part) {
+                    float* __restrict__ part, int64_t a_sstride, int a_sw) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
   const int64_t T = cdiv(M, C::BM) * cdiv(N, C::BN);
   const int64_t b = blockIdx.x;
+  // A's columns m0 .. of a tile: row-major (ld M), or slab-major (a_sw > 0: a tile lies in one
+  // slab of a_sw columns, rows a_sw apart)
+  auto a_at = [&](int64_t m0) { return a_sw ? A + (m0 / a_sw) * a_sstride + (m0 % a_sw) : A + m0; };
+  const int64_t lda = a_sw ? a_sw : M;
   floatx4 acc[C::MI][C::NJ];
   if (b < t_full) {
     const TileCoord tc = tile_plain_at<C>(M, N, (int)rows, b);
     if (!tc.valid) return;
-    gemm_tile<C, false, false>(A + tc.m0, M, tc.m_rows, B + tc.n0, N, tc.n_cols, (int)rows, smem, acc);
+    gemm_tile<C, false, false>(a_at(tc.m0), lda, tc.m_rows, B + tc.n0, N, tc.n_cols, (int)rows, smem, acc);
     store_out<C, float>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, NoVec{});
     return;
   }
@@ -789,7 +804,8 @@ __global__ void __launch_bounds__(C::THREADS)
   const TileCoord tc = tile_plain_at<C>(M, N, (int)rows, t);
   const int64_t k0 = c * chunk;
   const int klen = (int)(rows - k0 < chunk ? rows - k0 : chunk);
-  gemm_tile<C, false, false>(A + tc.m0 + k0 * M, M, tc.m_rows, B + tc.n0 + k0 * N, N, tc.n_cols, klen, smem, acc);
+  gemm_tile<C, false, false>(a_at(tc.m0) + k0 * lda, lda, tc.m_rows, B + tc.n0 + k0 * N, N, tc.n_cols, klen, smem,
+                             acc);
   TileCoord lt = tc;
   lt.m0 = 0;
   lt.n0 = 0;
@@ -812,10 +828,11 @@ __global__ void __launch_bounds__(256) k_split_reduce(const float* __restrict__ 
 }
 
 // Launches k_gemm_tn_split (and its reduction) for out = A^T B; `part` holds kMaxSplitItems
-// tiles of fp32 partials.  rows > 0.
+// tiles of fp32 partials.  rows > 0.  a_sw > 0: A is slab-major (see k_gemm_tn_split).
 template <class C>
 static int launch_tn_split(const char* label, const typename C::type* A, const typename C::type* B, int64_t rows,
-                           int M, int N, float* out, float* part, hipStream_t st) {
+                           int M, int N, float* out, float* part, hipStream_t st, int64_t a_sstride = 0,
+                           int a_sw = 0) {
   // rounds of `slots` concurrent tiles (one workgroup per 160 KB of LDS per CU)
   const int64_t tiles = cdiv(M, C::BM) * cdiv(N, C::BN);
   int64_t slots = (int64_t)device_cus() * ((160 * 1024) / C::LDS);
@@ -829,7 +846,7 @@ static int launch_tn_split(const char* label, const typename C::type* A, const t
   if (chunk < 256) chunk = 256;
   split = (int)cdiv(rows, chunk);
   HMOE_LAUNCH(label, k_gemm_tn_split<C>, dim3((unsigned)(t_full + R * split)), dim3(C::THREADS), C::LDS, st, A, B,
-              rows, M, N, out, t_full, split, chunk, part);
+              rows, M, N, out, t_full, split, chunk, part, a_sstride, a_sw);
   if (R > 0)
     HMOE_LAUNCH("split-K reduce", k_split_reduce<C>, dim3((unsigned)cdiv(R * C::BM * C::BN, 256)), dim3(256), 0, st,
                 (const float*)part, rows, M, N, t_full, split, (int)R, out);
@@ -932,7 +949,8 @@ static size_t bwd_ws(const MoeShape& s) {
   Workspace ws(nullptr, 0);
   ws.take<int32_t>(s.K + 1);
   ws.take<int32_t>(s.K);
-  ws.take<T>((size_t)s.n * s.V);
+  constexpr int GW = 256 * (16 / (int)sizeof(T));  // G padded to whole slabs (backward_t)
+  ws.take<T>(sizeof(T) == 2 && s.nd == 1 ? (size_t)s.n * cdiv(s.V, GW) * GW : (size_t)s.n * s.V);
   ws.take<T>((size_t)s.n * s.o);
   ws.take<T>((size_t)s.n * s.h);
   const int64_t prow = cdiv(s.n, C::BM) > cdiv(s.n, kGradRows) ? cdiv(s.n, C::BM) : cdiv(s.n, kGradRows);
@@ -1010,7 +1028,12 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   const MoeShape s = shape_of(p, n);
   int32_t* ts = ws.take<int32_t>(s.K + 1);
   int32_t* order = ws.take<int32_t>(s.K);
-  T* G = ws.take<T>((size_t)n * s.V);
+  constexpr int EPV = 16 / sizeof(T);
+  // bf16 logits through the shared decoder: G slab-major, [V / GW slabs][n][GW] (see
+  // k_dec_grad_elem), which the grad kernel writes contiguously; the last slab is padded.
+  constexpr int GW = 256 * EPV;
+  const bool slab = sizeof(T) == 2 && Lg && s.nd == 1;
+  T* G = ws.take<T>(slab ? (size_t)n * cdiv(s.V, GW) * GW : (size_t)n * s.V);
   T* dYs = ws.take<T>((size_t)n * s.o);
   T* dZ = ws.take<T>((size_t)n * s.h);
   const int mt = (int)cdiv(n, C::BM);
@@ -1031,7 +1054,6 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   const int64_t mt_bound = cdiv(n, C::BM) + s.K;
   HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
   HMOE_TRY(launch_seg_order(offsets, s.K, order, st));
-  constexpr int EPV = 16 / sizeof(T);
   if (s.nd > 1) {
     // One decoder per expert, everything in slot order (the API guarantees saved logits):
     // g from the stored logits in pieces that stay within one expert, dbD_e from the pieces'
@@ -1039,7 +1061,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
     HMOE_TRY(launch_seg_tiles(offsets, s.K, kGradRows, gts, st));
     HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)(gr + s.K), (unsigned)cdiv(s.V, 256 * EPV)),
                 dim3(256), 0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), perm, offsets,
-                gts, s.K, G, pdb);
+                gts, s.K, G, pdb, 0);
     if (dbD)
       HMOE_LAUNCH("decoder bias grad", k_piece_colsum, dim3((unsigned)cdiv(s.V, 256), (unsigned)s.K), dim3(256), 0,
                   st, pdb, gts, s.V, dbD);
@@ -1056,7 +1078,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   if (Lg) {
     HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)gr, (unsigned)cdiv(s.V, 256 * EPV)), dim3(256),
                 0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), (const int32_t*)nullptr,
-                (const int32_t*)nullptr, (const int32_t*)nullptr, 0, G, pdb);
+                (const int32_t*)nullptr, (const int32_t*)nullptr, 0, G, pdb, (int)slab);
     prow = gr;
   } else {
     HMOE_LAUNCH("decoder grad", k_dec_grad<C>, dim3((unsigned)(mt * ntv)), dim3(C::THREADS), C::LDS, st, H, D,
@@ -1066,9 +1088,18 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   if (dbD)
     HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, prow,
                 s.V, dbD);
-  HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
-              (const T*)G, D, n, s.V, s.o, inv, dYs);
-  HMOE_TRY(launch_tn_split<C>("decoder dD", (const T*)G, H, n, s.V, s.o, dD, split_part, st));
+  if constexpr (sizeof(T) == 2) {
+    if (slab) {
+      HMOE_LAUNCH("decoder dH", (k_dec_dH<C, GW>), dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS),
+                  C::LDS, st, (const T*)G, D, n, s.V, s.o, inv, dYs);
+      HMOE_TRY(launch_tn_split<C>("decoder dD", (const T*)G, H, n, s.V, s.o, dD, split_part, st, n * GW, GW));
+    }
+  }
+  if (!slab) {
+    HMOE_LAUNCH("decoder dH", k_dec_dH<C>, dim3((unsigned)(mt * cdiv(s.o, C::BN))), dim3(C::THREADS), C::LDS, st,
+                (const T*)G, D, n, s.V, s.o, inv, dYs);
+    HMOE_TRY(launch_tn_split<C>("decoder dD", (const T*)G, H, n, s.V, s.o, dD, split_part, st));
+  }
   }
   // experts
   const size_t mark = ws.off;
