@@ -150,14 +150,11 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4
 // m = max over the tile's valid columns and s = sum exp(logit - m), merged over the WAVES_N
 // waves that share the row through rm / rs (LDS, [WAVES_N][BM] floats each) and written as the
 // tile's partials pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
+// The second half of dec_tile_stats: after the waves' row partials are in LDS, merge them per
+// row and write the tile's (max, sum) pair.
 template <class C>
-__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
-                                               lds<float>* rm, lds<float>* rs, int64_t n, float* __restrict__ pm,
-                                               float* __restrict__ ps) {
-  if (tc.n_cols == C::BN)
-    dec_row_stats<C, true>(tc, acc, rm, rs);
-  else
-    dec_row_stats<C, false>(tc, acc, rm, rs);
+__device__ __forceinline__ void dec_stats_merge(const TileCoord& tc, lds<float>* rm, lds<float>* rs, int64_t n,
+                                                float* __restrict__ pm, float* __restrict__ ps) {
   wg_barrier_lds();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     float M = rm[t];
@@ -170,6 +167,17 @@ __device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx
     pm[at] = M;
     ps[at] = S;
   }
+}
+
+template <class C>
+__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                               lds<float>* rm, lds<float>* rs, int64_t n, float* __restrict__ pm,
+                                               float* __restrict__ ps) {
+  if (tc.n_cols == C::BN)
+    dec_row_stats<C, true>(tc, acc, rm, rs);
+  else
+    dec_row_stats<C, false>(tc, acc, rm, rs);
+  dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
 }
 
 template <class C>
@@ -306,13 +314,21 @@ __global__ void __launch_bounds__(C::THREADS)
       pipe.prime(H + nc.m0 * o, o, nc.m_rows, D + (int64_t)nc.n0 * o, o, nc.n_cols, o, smem);
     }
     add_bias<C>(acc, bias);
-    dec_tile_stats<C>(tc, acc, rm, rs, n, pm, ps);
+    // the waves' row partials, then the logits stores, then the partials' merge (its barrier
+    // waits only for LDS traffic): measured faster than merging before the stores.  The
+    // merge's stores are younger than the logits stores, which only makes the next tile's
+    // waits stricter.
+    if (tc.n_cols == C::BN)
+      dec_row_stats<C, true>(tc, acc, rm, rs);
+    else
+      dec_row_stats<C, false>(tc, acc, rm, rs);
     // nothing may move between the primed loads and the stores: the next waits count them
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
     if (L)
       store_direct<C, bf16>(tc, acc, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
     __builtin_amdgcn_sched_barrier(0);
+    dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
     if (!more) break;
     stores_pending = L != nullptr && tc.m_rows == C::BM && tc.n_cols == C::BN;
     t = tn;
