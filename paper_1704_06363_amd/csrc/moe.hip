@@ -152,10 +152,10 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4
 // tile's partials pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
 // The second half of dec_tile_stats: after the waves' row partials are in LDS, merge them per
 // row and write the tile's (max, sum) pair.
-template <class C>
+template <class C, bool BARRIER = true>
 __device__ __forceinline__ void dec_stats_merge(const TileCoord& tc, lds<float>* rm, lds<float>* rs, int64_t n,
                                                 float* __restrict__ pm, float* __restrict__ ps) {
-  wg_barrier_lds();
+  if constexpr (BARRIER) wg_barrier_lds();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
     float M = rm[t];
 #pragma unroll
@@ -256,8 +256,10 @@ __global__ void __launch_bounds__(C::THREADS)
 // let those stay in flight (ragged tiles wait for everything).  The logits are stored with
 // ordinary stores: a wave's store covers 64 bytes of a row, and the L2 merges the two halves of
 // each 128-byte line before writing it back (non-temporal stores measured 1.5x the write
-// traffic).  rm / rs sit past the operand ring
-// (dynamic LDS = C::LDS + kDecStatLds).
+// traffic).  The row partials (rm / rs) sit past the operand ring in two buffers, alternating
+// by tile (dynamic LDS = C::LDS + 2 kDecStatLds): a tile's partials are merged across waves in
+// the next tile's epilogue, after that tile's K loop, whose barriers order the partials'
+// writes before the merge's reads and the merge's reads before the buffer is written again.
 constexpr int kDecStatLds = 2 * 4 * 256 * (int)sizeof(float);
 template <class C>
 __device__ __forceinline__ void dec_bias_packed(const TileCoord& tc, const bf16* __restrict__ bD,
@@ -278,8 +280,8 @@ __global__ void __launch_bounds__(C::THREADS)
   constexpr int STORES = direct_stores<C, bf16>();  // per wave, for a full tile
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
-  lds<float>* rm = reinterpret_cast<lds<float>*>(smem + C::LDS);
-  lds<float>* rs = rm + C::WAVES_N * C::BM;
+  lds<float>* rm0 = reinterpret_cast<lds<float>*>(smem + C::LDS);
+  constexpr int SB = 2 * C::WAVES_N * C::BM;  // one statistics buffer (floats)
   using F = Frag<C>;
   const int64_t tiles = cdiv(n, C::BM) * cdiv(V, C::BN);
   int64_t t = blockIdx.x;
@@ -290,9 +292,14 @@ __global__ void __launch_bounds__(C::THREADS)
   uint2 bp[C::NJ];
   dec_bias_packed<C>(tc, bD, bp);
   bool stores_pending = false;
+  int buf = 0;
+  TileCoord pc = tc;  // the previous tile, whose partials merge in this tile's epilogue
+  bool have_prev = false;
   for (;;) {
     floatx4 acc[C::MI][C::NJ];
     pipe.template run<false, STORES>(smem, acc, nullptr, stores_pending);
+    lds<float>* rm = rm0 + buf * SB;
+    lds<float>* rs = rm + C::WAVES_N * C::BM;
     float bias[F::NCOL];
 #pragma unroll
     for (int j = 0; j < C::NJ; ++j) {
@@ -314,10 +321,9 @@ __global__ void __launch_bounds__(C::THREADS)
       pipe.prime(H + nc.m0 * o, o, nc.m_rows, D + (int64_t)nc.n0 * o, o, nc.n_cols, o, smem);
     }
     add_bias<C>(acc, bias);
-    // the waves' row partials, then the logits stores, then the partials' merge (its barrier
-    // waits only for LDS traffic): measured faster than merging before the stores.  The
-    // merge's stores are younger than the logits stores, which only makes the next tile's
-    // waits stricter.
+    // the waves' row partials, then the logits stores, then the previous tile's merge:
+    // measured faster than merging before the stores.  The merge's stores are younger than
+    // the logits stores, which only makes the next tile's waits stricter.
     if (tc.n_cols == C::BN)
       dec_row_stats<C, true>(tc, acc, rm, rs);
     else
@@ -328,9 +334,20 @@ __global__ void __launch_bounds__(C::THREADS)
     if (L)
       store_direct<C, bf16>(tc, acc, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
     __builtin_amdgcn_sched_barrier(0);
-    dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
-    if (!more) break;
+    // the previous tile's partials were written before this tile's K loop, whose barriers
+    // order them; its buffer is rewritten only after the next K loop
+    if (have_prev) {
+      lds<float>* pm_l = rm0 + (buf ^ 1) * SB;
+      dec_stats_merge<C, false>(pc, pm_l, pm_l + C::WAVES_N * C::BM, n, pm, ps);
+    }
+    if (!more) {
+      dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
+      break;
+    }
     stores_pending = L != nullptr && tc.m_rows == C::BM && tc.n_cols == C::BN;
+    pc = tc;
+    have_prev = true;
+    buf ^= 1;
     t = tn;
     tc = nc;
   }
@@ -1020,7 +1037,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   if constexpr (C::DMA) {
     // persistent: one workgroup per resident slot
     const int64_t tiles = cdiv(n, C::BM) * ntv;
-    constexpr int lds_bytes = C::LDS + kDecStatLds;
+    constexpr int lds_bytes = C::LDS + 2 * kDecStatLds;
     int64_t slots = (int64_t)device_cus() * ((160 * 1024) / lds_bytes);
     if (slots > tiles) slots = tiles;
     HMOE_LAUNCH("decoder forward", k_dec_fwd_stream<C>, dim3((unsigned)slots), dim3(C::THREADS), lds_bytes, st,
