@@ -768,13 +768,29 @@ __global__ void __launch_bounds__(256) k_piece_colsum(const float* __restrict__ 
   out[(int64_t)e * V + c] = s;
 }
 
+// out[v] = sum over the rows of part[row][v] (the decoder bias gradient from per-block column
+// partials).  A block takes 64 columns; its four waves sum a quarter of the rows each (in row order, four
+// rows in flight) and the quarters are added in order, so the result does not depend on timing.
 __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int rows, int V,
                                                       float* __restrict__ out) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= V) return;
+  __shared__ float s_q[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  const int per = (rows + 3) / 4;
+  const int q0 = w * per, q1 = q0 + per < rows ? q0 + per : rows;
   float s = 0.f;
-  for (int q = 0; q < rows; ++q) s += part[(int64_t)q * V + c];
-  out[c] = s;
+  if (c < V) {
+    int q = q0;
+    for (; q + 4 <= q1; q += 4) {
+      const float a = part[(int64_t)q * V + c], b = part[(int64_t)(q + 1) * V + c];
+      const float d = part[(int64_t)(q + 2) * V + c], e = part[(int64_t)(q + 3) * V + c];
+      s = (((s + a) + b) + d) + e;
+    }
+    for (; q < q1; ++q) s += part[(int64_t)q * V + c];
+  }
+  s_q[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && c < V) out[c] = ((s_q[0][lane] + s_q[1][lane]) + s_q[2][lane]) + s_q[3][lane];
 }
 
 // dH = G D, written to expert order: dYs[inv[i]] = (G D)[i].  GW > 0: G is slab-major, [V / GW
@@ -1119,7 +1135,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
     prow = mt;
   }
   if (dbD)
-    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 256)), dim3(256), 0, st, pdb, prow,
+    HMOE_LAUNCH("decoder bias grad", k_colsum_final, dim3((unsigned)cdiv(s.V, 64)), dim3(256), 0, st, pdb, prow,
                 s.V, dbD);
   if constexpr (sizeof(T) == 2) {
     if (slab) {
