@@ -104,6 +104,19 @@ def test_decoder_tiles_outnumber_workgroups(saved):
     _step_vs_oracle(X, ids, K, p, rp, tg, "bf16", saved)
 
 
+def test_decoder_gradient_tail_in_a_later_slab():
+    # bf16 with saved logits keeps g in column slabs of 2048: V = 4104 gives two full slabs and
+    # an 8-column third, so dH's last K stage (4104 = 128 x 32 + 8) is a ragged tail read from
+    # the third slab and dD's last row tile (8 rows of g^T) starts that slab; n = 700 leaves
+    # ragged row tiles
+    n, d, h, o, V, K = 700, 64, 128, 64, 4104, 3
+    X = W.rectified_gaussian(n, d, seed=95, dtype="bf16", device="cuda")
+    ids = np.random.default_rng(96).integers(0, K, n).astype(np.int32)
+    rp, tg = W.zipf_labels(n, V, 8, seed=97)
+    p = W.moe_params(K, d, h, o, V, seed=98, dtype="bf16", device="cuda", bias=True)
+    _step_vs_oracle(X, ids, K, p, rp, tg, "bf16", True)
+
+
 def test_largest_K_assign_and_dispatch():
     n, d, K = 5000, 64, 4096
     X = W.gmm_features(n, d, 64, seed=70, dtype="bf16", device="cuda")
