@@ -10,11 +10,12 @@
  * Conventions
  *   - Every real number is a double.  Inputs are the exact values the device sees (fp32 or
  *     bf16 bytes widened to double by the caller).
- *   - Results are rounded to a storage precision only where the device library stores a
- *     tensor that a later step reads back: centroids (fp32), the expert hidden activations
- *     and outputs, the activation gradients (g, dh, dz) and the input gradient (the data
- *     dtype: "bf16 in, fp32 accumulate, bf16 out" for every layer).  `store` selects that rounding:
- *     0 = keep fp64, 1 = fp32 (round to nearest even), 2 = bf16 (round to nearest even).
+ *   - Results are rounded to a storage precision only where the library's interface hands a
+ *     tensor to its caller, who feeds it to a later step: centroids (fp32), the expert hidden
+ *     activations H1 and outputs H, and the input gradient dX (the data dtype: "bf16 in, fp32
+ *     accumulate, bf16 out" for every layer).  `store` selects that rounding: 0 = keep fp64,
+ *     1 = fp32 (round to nearest even), 2 = bf16 (round to nearest even).  Everything else,
+ *     the softmax and the activation gradients g, dh, dz included, stays in fp64.
  *   - Matrices are row-major.  Expert weights follow the [out][in] convention.
  *   - OpenMP is used only across independent samples / output rows; every sum runs in a
  *     fixed order (ascending sample index, ascending feature index), so results do not depend
@@ -310,8 +311,8 @@ int hmoe_orc_dispatch(int64_t n, int32_t K, const int32_t* e, int32_t* counts,
  *   lse = log sum_j exp(l_j);  loss_i = lse - (1/|P_i|) sum_{j in P_i} l_j
  * The target mass is spread uniformly over the positive tags P_i (tags listed in
  * tag[row_ptr[i] .. row_ptr[i+1]), distinct); the batch loss is the mean over samples.
- * b1, b2, bD may be NULL (no bias).  probs (n x V) is optional; logits (n x V), optional, receives
- * the logits rounded by `store` (the tensor a device saves for the backward). */
+ * b1, b2, bD may be NULL (no bias).  probs (n x V) and logits (n x V) are optional outputs, in
+ * fp64 like lse and loss. */
 int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
                          int32_t ndec, const double* X, const int32_t* a, const double* W1,
                          const double* b1, const double* W2, const double* b2, const double* D,
@@ -373,7 +374,7 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
       if (probs)
         for (int32_t v = 0; v < V; ++v) probs[i * (int64_t)V + v] = exp(lg[v] - L);
       if (logits)
-        for (int32_t v = 0; v < V; ++v) logits[i * (int64_t)V + v] = store_round(lg[v], store);
+        for (int32_t v = 0; v < V; ++v) logits[i * (int64_t)V + v] = lg[v];
     }
     free(lg);
   }
@@ -397,16 +398,18 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
  *          (per decoder: decoder e sums over the samples of expert e when ndec = K)
  *   db2_e = sum dh,  dW2_e = sum dh h1^T,  dh1 = W2_e^T dh,  dz = dh1 * [h1 > 0]
  *   db1_e = sum dz,  dW1_e = sum dz x^T,   dx = W1_e^T dz
- * The activation gradients g (as used by dD and dh), dh, dz and dx are the tensors a device
- * stores and reads back; `store` rounds them (dbD sums the unrounded g).  With logit_round the
- * recomputed logits are rounded by `store` first, as when a device saved them in the forward.
+ * Rounding: `store` rounds dx, the one activation gradient the caller receives (in the data
+ * dtype).  g, dh and dz are the paper's exact intermediate quantities and stay in fp64 unless
+ * `istore` asks for them rounded (a diagnostic that models a device which stores them; dbD
+ * always sums the unrounded g).  logit_round (diagnostic) rounds the recomputed logits by
+ * `istore` before the softmax.  The plain gradient of Eq. 3 is istore = 0, logit_round = 0.
  * Experts that receive no sample get zero gradients.  dX may be NULL. */
 int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
                           int32_t ndec, const double* X, const int32_t* a, const double* W1,
                           const double* W2, const double* D, const double* bD,
                           const int32_t* row_ptr, const int32_t* tag, const double* H1,
                           const double* H, const double* lse, double scale, int store,
-                          int logit_round, double* dW1, double* db1, double* dW2, double* db2,
+                          int istore, int logit_round, double* dW1, double* db1, double* dW2, double* db2,
                           double* dD, double* dbD, double* dX) {
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
   if (ndec != 1 && ndec != K) return -1;
@@ -432,28 +435,28 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
       double s = bDe ? bDe[v] : 0.0;
       const double* dv = De + (int64_t)v * o;
       for (int32_t j = 0; j < o; ++j) s += dv[j] * y[j];
-      if (logit_round) s = store_round(s, store);
+      if (logit_round) s = store_round(s, istore);
       g[v] = exp(s - lse[i]);
     }
     int32_t np = row_ptr[i + 1] - row_ptr[i];
     for (int32_t q = row_ptr[i]; q < row_ptr[i + 1]; ++q) g[tag[q]] -= 1.0 / (double)np;
     for (int32_t v = 0; v < V; ++v) g[v] *= scale;
     double* gs = GS + i * (int64_t)V;
-    for (int32_t v = 0; v < V; ++v) gs[v] = store_round(g[v], store);
+    for (int32_t v = 0; v < V; ++v) gs[v] = store_round(g[v], istore);
     double* dh = dH + i * (int64_t)o;
     for (int32_t j = 0; j < o; ++j) dh[j] = 0.0;
     for (int32_t v = 0; v < V; ++v) {
       const double* dv = De + (int64_t)v * o;
       for (int32_t j = 0; j < o; ++j) dh[j] += gs[v] * dv[j];
     }
-    for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], store);
+    for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], istore);
     const double* w2 = W2 + (int64_t)e * o * h;
     const double* h1 = H1 + i * (int64_t)h;
     double* dz = dZ + i * (int64_t)h;
     for (int32_t k = 0; k < h; ++k) dz[k] = 0.0;
     for (int32_t j = 0; j < o; ++j)
       for (int32_t k = 0; k < h; ++k) dz[k] += dh[j] * w2[(int64_t)j * h + k];
-    for (int32_t k = 0; k < h; ++k) dz[k] = (h1[k] > 0.0) ? store_round(dz[k], store) : 0.0;
+    for (int32_t k = 0; k < h; ++k) dz[k] = (h1[k] > 0.0) ? store_round(dz[k], istore) : 0.0;
     if (dX) {
       const double* w1 = W1 + (int64_t)e * h * d;
       double* dx = dX + i * (int64_t)d;

@@ -176,13 +176,24 @@ def test_finite_differences(orc):
 
 
 def test_store_rounding_points(orc):
-    """With bf16 storage the hidden activations and outputs are bf16 values and dX too."""
+    """With bf16 storage the hidden activations and outputs are bf16 values and dX too; the
+    softmax and the activation gradients g, dh, dz are not rounded."""
     c = _case(12)
     f = _fwd(orc, c, store="bf16")
     for k in ("H1", "H"):
         np.testing.assert_array_equal(orc.round_store(f[k], "bf16"), f[k])
     b = _bwd(orc, c, f, store="bf16")
     np.testing.assert_array_equal(orc.round_store(b["dX"], "bf16"), b["dX"])
+    # the gradient of Eq. 3 rounds nothing but the dX it hands back: every other output is the
+    # unrounded backward's, bit for bit, and dX is that backward's dX rounded once
+    b64 = _bwd(orc, c, f, store="f64")
+    for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD"):
+        np.testing.assert_array_equal(b[k], b64[k], err_msg=k)
+    np.testing.assert_array_equal(b["dX"], orc.round_store(b64["dX"], "bf16"))
+    # the diagnostic that rounds g, dh and dz does move the parameter gradients
+    bi = _bwd(orc, c, f, store="bf16", internal_store="bf16")
+    assert not np.array_equal(bi["dW1"], b64["dW1"])
+    np.testing.assert_array_equal(bi["dbD"], b64["dbD"])  # dbD sums the unrounded g
     f64 = _fwd(orc, c, store="f64")
     # the stored H differs from the unrounded one by at most half a bf16 ulp chain
     assert np.max(np.abs(f["H"] - f64["H"])) < 0.05
