@@ -403,14 +403,20 @@ int hmoe_orc_moe_forward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, 
  * `istore` asks for them rounded (a diagnostic that models a device which stores them; dbD
  * always sums the unrounded g).  logit_round (diagnostic) rounds the recomputed logits by
  * `istore` before the softmax.  The plain gradient of Eq. 3 is istore = 0, logit_round = 0.
- * Experts that receive no sample get zero gradients.  dX may be NULL. */
-int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
-                          int32_t ndec, const double* X, const int32_t* a, const double* W1,
-                          const double* W2, const double* D, const double* bD,
-                          const int32_t* row_ptr, const int32_t* tag, const double* H1,
-                          const double* H, const double* lse, double scale, int store,
-                          int istore, int logit_round, double* dW1, double* db1, double* dW2, double* db2,
-                          double* dD, double* dbD, double* dX) {
+ * Experts that receive no sample get zero gradients.  dX may be NULL.
+ * magnitude = 1 evaluates the same sums on absolute values -- |g|, then every product with
+ * each factor's absolute value, nothing rounded -- which gives, per output, the scale M of the
+ * standard first-order bound on the rounding error of the computation: an implementation
+ * that rounds its operands with unit roundoff u stays within (number of roundings) * u * M of
+ * the exact result (Higham, Accuracy and Stability of Numerical Algorithms, Section 3.1). */
+static int moe_backward_impl(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
+                             int32_t ndec, const double* X, const int32_t* a, const double* W1,
+                             const double* W2, const double* D, const double* bD,
+                             const int32_t* row_ptr, const int32_t* tag, const double* H1,
+                             const double* H, const double* lse, double scale, int store,
+                             int istore, int logit_round, int magnitude, double* dW1, double* db1,
+                             double* dW2, double* db2, double* dD, double* dbD, double* dX) {
+#define MAG(x) (magnitude ? fabs(x) : (x))
   if (n < 0 || d <= 0 || h <= 0 || o <= 0 || V <= 0 || K <= 0) return -1;
   if (ndec != 1 && ndec != K) return -1;
   for (int64_t i = 0; i < n; ++i) {
@@ -440,30 +446,31 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
     }
     int32_t np = row_ptr[i + 1] - row_ptr[i];
     for (int32_t q = row_ptr[i]; q < row_ptr[i + 1]; ++q) g[tag[q]] -= 1.0 / (double)np;
-    for (int32_t v = 0; v < V; ++v) g[v] *= scale;
+    for (int32_t v = 0; v < V; ++v) g[v] = MAG(g[v] * scale);
+    const int rstore = magnitude ? 0 : istore; /* the magnitude rounds nothing */
     double* gs = GS + i * (int64_t)V;
-    for (int32_t v = 0; v < V; ++v) gs[v] = store_round(g[v], istore);
+    for (int32_t v = 0; v < V; ++v) gs[v] = store_round(g[v], rstore);
     double* dh = dH + i * (int64_t)o;
     for (int32_t j = 0; j < o; ++j) dh[j] = 0.0;
     for (int32_t v = 0; v < V; ++v) {
       const double* dv = De + (int64_t)v * o;
-      for (int32_t j = 0; j < o; ++j) dh[j] += gs[v] * dv[j];
+      for (int32_t j = 0; j < o; ++j) dh[j] += gs[v] * MAG(dv[j]);
     }
-    for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], istore);
+    for (int32_t j = 0; j < o; ++j) dh[j] = store_round(dh[j], rstore);
     const double* w2 = W2 + (int64_t)e * o * h;
     const double* h1 = H1 + i * (int64_t)h;
     double* dz = dZ + i * (int64_t)h;
     for (int32_t k = 0; k < h; ++k) dz[k] = 0.0;
     for (int32_t j = 0; j < o; ++j)
-      for (int32_t k = 0; k < h; ++k) dz[k] += dh[j] * w2[(int64_t)j * h + k];
-    for (int32_t k = 0; k < h; ++k) dz[k] = (h1[k] > 0.0) ? store_round(dz[k], istore) : 0.0;
+      for (int32_t k = 0; k < h; ++k) dz[k] += dh[j] * MAG(w2[(int64_t)j * h + k]);
+    for (int32_t k = 0; k < h; ++k) dz[k] = (h1[k] > 0.0) ? store_round(dz[k], rstore) : 0.0;
     if (dX) {
       const double* w1 = W1 + (int64_t)e * h * d;
       double* dx = dX + i * (int64_t)d;
       for (int32_t j = 0; j < d; ++j) dx[j] = 0.0;
       for (int32_t k = 0; k < h; ++k)
-        for (int32_t j = 0; j < d; ++j) dx[j] += dz[k] * w1[(int64_t)k * d + j];
-      for (int32_t j = 0; j < d; ++j) dx[j] = store_round(dx[j], store);
+        for (int32_t j = 0; j < d; ++j) dx[j] += dz[k] * MAG(w1[(int64_t)k * d + j]);
+      for (int32_t j = 0; j < d; ++j) dx[j] = store_round(dx[j], magnitude ? 0 : store);
     }
   }
 
@@ -480,7 +487,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
       sb += G[i * (int64_t)V + v];
       const double g = GS[i * (int64_t)V + v];
       const double* y = H + i * (int64_t)o;
-      for (int32_t j = 0; j < o; ++j) dd[j] += g * y[j];
+      for (int32_t j = 0; j < o; ++j) dd[j] += g * MAG(y[j]);
     }
     if (dbD) dbD[r] = sb;
   }
@@ -497,7 +504,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
       double g = dH[i * (int64_t)o + j];
       sb += g;
       const double* h1 = H1 + i * (int64_t)h;
-      for (int32_t k = 0; k < h; ++k) w[k] += g * h1[k];
+      for (int32_t k = 0; k < h; ++k) w[k] += g * MAG(h1[k]);
     }
     if (db2) db2[(int64_t)e * o + j] = sb;
   }
@@ -512,7 +519,7 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
       double g = dZ[i * (int64_t)h + k];
       sb += g;
       const double* x = X + i * (int64_t)d;
-      for (int32_t j = 0; j < d; ++j) w[j] += g * x[j];
+      for (int32_t j = 0; j < d; ++j) w[j] += g * MAG(x[j]);
     }
     if (db1) db1[(int64_t)e * h + k] = sb;
   }
@@ -521,6 +528,19 @@ int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V,
   free(dH);
   free(dZ);
   return 0;
+#undef MAG
+}
+
+int hmoe_orc_moe_backward(int64_t n, int32_t d, int32_t h, int32_t o, int32_t V, int32_t K,
+                          int32_t ndec, const double* X, const int32_t* a, const double* W1,
+                          const double* W2, const double* D, const double* bD,
+                          const int32_t* row_ptr, const int32_t* tag, const double* H1,
+                          const double* H, const double* lse, double scale, int store,
+                          int istore, int logit_round, int magnitude, double* dW1, double* db1,
+                          double* dW2, double* db2, double* dD, double* dbD, double* dX) {
+  return moe_backward_impl(n, d, h, o, V, K, ndec, X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse,
+                           scale, store, istore, logit_round, magnitude, dW1, db1, dW2, db2, dD,
+                           dbD, dX);
 }
 
 /* ------------------------------------------------ Section 4.4: t_m, p@m (Eq. 4), q@m (Eq. 5) */

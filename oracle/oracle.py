@@ -209,13 +209,17 @@ def moe_forward(X, a, W1, b1, W2, b2, D, bD, row_ptr, tag, store: str = "f64",
 
 def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
                  store: str = "f64", want_dX: bool = True, internal_store: str = "f64",
-                 logit_round: bool = False):
+                 logit_round: bool = False, magnitude: bool = False):
     """Gradients of the mean loss w.r.t. every expert and decoder parameter (and X) given the
     saved activations (Section 2; Section 4.1, Eq. 3; the gater gets none, Section 2.2).
     Decoders as in moe_forward; dD and dbD have D's and bD's shapes.  `store` rounds dX, the
     activation gradient handed to the caller; g, dh and dz stay fp64 (the plain gradient).
     Diagnostics only: internal_store rounds g, dh and dz as a device storing them would, and
-    logit_round rounds the logits (in internal_store precision) before the softmax."""
+    logit_round rounds the logits (in internal_store precision) before the softmax.
+    magnitude: the same sums over absolute values (|g| = |p - y| scale, then |a||b| for every
+    product, nothing rounded): per output the scale M of the first-order rounding-error bound of
+    the computation (an evaluation that rounds its operands with unit roundoff u stays within
+    (number of roundings) u M of the exact gradient)."""
     X = _f64(X)
     n, d = X.shape
     K, h, _ = W1.shape
@@ -238,7 +242,7 @@ def moe_backward(X, a, W1, W2, D, bD, row_ptr, tag, H1, H, lse, scale=None,
         ctypes.c_int32(V), ctypes.c_int32(K), ctypes.c_int32(ndec), _p(X), _p(a), _p(W1), _p(W2), _p(D), _p(bD),
         _p(row_ptr), _p(tag), _p(H1), _p(H), _p(lse), ctypes.c_double(scale),
         ctypes.c_int(_STORE[store]), ctypes.c_int(_STORE[internal_store]),
-        ctypes.c_int(1 if logit_round else 0), _p(dW1), _p(db1),
+        ctypes.c_int(1 if logit_round else 0), ctypes.c_int(1 if magnitude else 0), _p(dW1), _p(db1),
         _p(dW2), _p(db2), _p(dD), _p(dbD), _p(dX))
     _check(rc, "moe_backward")
     return {"dW1": dW1, "db1": db1, "dW2": dW2, "db2": db2, "dD": dD, "dbD": dbD, "dX": dX}

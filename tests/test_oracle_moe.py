@@ -293,3 +293,35 @@ def test_independent_zero_decoders_give_log_v(orc):
     V = c["D"].shape[1]
     np.testing.assert_allclose(f["lse"], np.log(V), rtol=1e-15)
     np.testing.assert_allclose(f["loss"], np.log(V), rtol=1e-15)
+
+
+def test_backward_magnitude(orc):
+    """The magnitude mode is the backward's sums taken over absolute values: it bounds every
+    gradient entry (triangle inequality) and equals the chain |G||D| -> |W2| (ReLU mask) -> |W1|
+    written out with numpy matrix products per expert (G = (softmax - y)/n from scipy)."""
+    from scipy.special import softmax
+    c = _case(31, n=60, K=3, empty=1)
+    f = _fwd(orc, c)
+    b = _bwd(orc, c, f)
+    m = _bwd(orc, c, f, magnitude=True)
+    for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
+        assert np.all(m[k] >= np.abs(b[k]) * (1 - 1e-12)), k
+    n = c["X"].shape[0]
+    L = f["H"] @ c["D"].T + c["bD"]
+    Y = np.zeros_like(L)
+    for i in range(n):
+        t = c["tag"][c["row_ptr"][i]:c["row_ptr"][i + 1]]
+        Y[i, t] = 1.0 / len(t)
+    G = np.abs(softmax(L, axis=1) - Y) / n
+    np.testing.assert_allclose(m["dD"], G.T @ np.abs(f["H"]), rtol=1e-12)
+    np.testing.assert_allclose(m["dbD"], G.sum(0), rtol=1e-12)
+    dH = G @ np.abs(c["D"])
+    for e in range(3):
+        r = c["a"] == e
+        dZ = (dH[r] @ np.abs(c["W2"][e])) * (f["H1"][r] > 0)
+        np.testing.assert_allclose(m["dW2"][e], dH[r].T @ np.abs(f["H1"][r]), rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(m["db2"][e], dH[r].sum(0), rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(m["dW1"][e], dZ.T @ np.abs(c["X"][r]), rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(m["db1"][e], dZ.sum(0), rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(m["dX"][r], dZ @ np.abs(c["W1"][e]), rtol=1e-12, atol=1e-300)
+    assert np.all(m["dW1"][1] == 0)  # the empty expert
