@@ -162,7 +162,8 @@ class RoutedStep:
                     "lse": torch.empty(n, dtype=torch.float32, device=dev),
                     "loss": torch.empty(n, dtype=torch.float32, device=dev),
                     "loss_mean": torch.empty(1, dtype=torch.float32, device=dev),
-                    "logits": torch.empty(n, V, dtype=bf, device=dev)}
+                    "logits": torch.empty(n, V, dtype=bf, device=dev),
+                    "logit_anchor": torch.empty(hmoe.anchor_shape(n, V), dtype=torch.float32, device=dev)}
         f32 = torch.float32
         self.grads = {"dW1": torch.empty(K, h, d, dtype=f32, device=dev),
                       "db1": torch.empty(K, h, dtype=f32, device=dev),
@@ -188,7 +189,7 @@ class RoutedStep:
             return
         h.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], self.row_ptr,
                        self.tag, f["H1_sorted"], f["H"], f["lse"], out=self.grads, ws=self.ws,
-                       logits=f["logits"])
+                       logits=f["logits"], logit_anchor=f["logit_anchor"])
 
 
 def time_steps(fn, steps, warmup, timer=True):
@@ -427,7 +428,7 @@ def leg_inference(steps, warmup, m=10, draws=100000):
 
     def run():
         st.run(backward=False)
-        hmoe.topm(st.fwd["logits"], m, out={"idx": idx})
+        hmoe.topm(st.fwd["logits"], m, out={"idx": idx}, anchor=st.fwd["logit_anchor"])
         hmoe.topm_hits(idx, st.row_ptr, st.tag, qs, qt, out=hits)
 
     ms, rp = time_steps(run, steps, warmup)

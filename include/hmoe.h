@@ -17,7 +17,10 @@
  *   - Matrices are row-major.  Real tensors are HMOE_F32 (float) or HMOE_BF16 (bfloat16,
  *     round-to-nearest-even on store); accumulation is always fp32 or wider.
  *   - Row widths (d, d_hid, d_out, vocab for the decoder) must be multiples of 8 and device
- *     pointers 16-byte aligned, else HMOE_ESHAPE.  n may be 0 (nothing is launched).
+ *     pointers 16-byte aligned, else HMOE_ESHAPE.  n may be 0 (nothing is launched).  A
+ *     vocabulary of any size V is run by padding it to the next multiple of 8 with zero rows of
+ *     D and bias -inf: a padded tag then has logit -inf, probability 0 and zero gradients, so
+ *     lse, the loss and every gradient of the V real tags are those of the unpadded problem.
  *     Indices are int32 (n < 2^31); 1 <= K <= 4096.
  *   - Return value: HMOE_OK (0) or a negative code; argument errors are detected before any
  *     launch and described by hmoe_last_error() (thread-local).  Launch failures return
@@ -33,7 +36,15 @@
 extern "C" {
 #endif
 
-#define HMOE_VERSION 1
+#define HMOE_VERSION 2
+
+/* Layout of the anchors of stored logits (hmoe_moe_forward): one fp32 anchor per row and per
+ * HMOE_ANCHOR_COLS columns, in an array [ceil(vocab / HMOE_ANCHOR_TILE)][n][HMOE_ANCHOR_TILE /
+ * HMOE_ANCHOR_COLS]; column v of row i has its anchor at
+ * ((v / HMOE_ANCHOR_TILE) * n + i) * (HMOE_ANCHOR_TILE / HMOE_ANCHOR_COLS)
+ *   + (v % HMOE_ANCHOR_TILE) / HMOE_ANCHOR_COLS. */
+#define HMOE_ANCHOR_COLS 64
+#define HMOE_ANCHOR_TILE 256
 
 enum {
   HMOE_OK = 0,
@@ -156,33 +167,41 @@ typedef struct {
  *   perm int32[n] (slot -> sample).
  *   H1_sorted [n x d_hid] out: relu(W1_e x + b1_e) in expert order (saved for backward).
  *   H [n x d_out] out: expert outputs W2_e h1 + b2_e in SAMPLE order (the combine).
- *   logits [n x vocab] out or NULL: D H_i + bD in dtype dt, saved so that the backward does
- *     not recompute them (n * vocab * 2 bytes in bf16; pass NULL to save the memory).  Rows
- *     in sample order with a shared decoder; in slot order (row p is sample perm[p]) with
- *     per-expert decoders, where they are required by the backward.
+ *   logits [n x vocab] out or NULL: the logits D H_i + bD, saved so that the backward does
+ *     not recompute them (n * vocab * 2 bytes in bf16; pass NULL to save the memory), stored
+ *     in dtype dt as offsets from per-row anchors: logit = anchor + stored value, the sum
+ *     formed in fp32.  The anchor of a row and 64-column block is the largest fp32 logit of
+ *     the row in that block, so the largest logits (the ones that carry the probability mass)
+ *     keep close to fp32 accuracy in a bf16 store, whatever their magnitude.  Rows in sample
+ *     order with a shared decoder; in slot order (row p is sample perm[p]) with per-expert
+ *     decoders, where they are required by the backward.
+ *   logit_anchor float[ceil(vocab / 256) * n * 4] out (layout: HMOE_ANCHOR_*): required when
+ *     logits is given, ignored otherwise.
  *   lse float[n] out: log-sum-exp of the V logits (from the fp32 logits).
  *   loss float[n] out: lse_i - mean of the logits of the positive tags.
  *   loss_mean float[1] out: mean over the batch. */
 size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n);
 int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
                      const int32_t* offsets, const int32_t* perm, const hmoe_labels_t* y,
-                     void* H1_sorted, void* H, void* logits, float* lse, float* loss,
-                     float* loss_mean, void* ws, size_t ws_bytes, void* stream);
+                     void* H1_sorted, void* H, void* logits, float* logit_anchor, float* lse,
+                     float* loss, float* loss_mean, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward pass: gradients of loss_mean (the 1/n is included) with respect to every expert
  * and decoder parameter, and optionally the input features.  The gater is fixed (Section
  * 2.2), so nothing flows to the centres.  With p = softmax(D H_i + bD), y_i the target:
  *   g = (p - y)/n; dbD = sum g; dD = g^T H; dH = g D; per expert e: db2 = sum dH,
  *   dW2 = dH^T H1, dZ = (dH W2) * [H1 > 0]; db1 = sum dZ; dW1 = dZ^T X; dX = dZ W1.
- *   Inputs are the forward's saved tensors (H1_sorted, H, lse, and logits if it saved them:
- *   then p is formed from the stored logits; NULL recomputes them from H) and inv int32[n].
+ *   Inputs are the forward's saved tensors (H1_sorted, H, lse, and logits with logit_anchor
+ *   if it saved them: then p = exp(anchor + stored - lse); logits NULL recomputes them from H)
+ *   and inv int32[n].
  *   dW1, db1, dW2, db2, dD, dbD: float out (overwritten; experts without samples get 0, and
  *   so do their decoders when each expert has its own; dD and dbD have D's and bD's shapes);
  *   db1, db2, dbD may be NULL.  dX [n x d_in] in dtype dt, SAMPLE order, or NULL. */
 int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted,
                       const int32_t* offsets, const int32_t* perm, const int32_t* inv,
                       const hmoe_labels_t* y, const void* H1_sorted, const void* H,
-                      const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
+                      const void* logits, const float* logit_anchor, const float* lse,
+                      float* dW1, float* db1, float* dW2,
                       float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
                       void* stream);
 
@@ -225,15 +244,16 @@ int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t d
 
 /* ------------------------------------------------------------------ inference tail */
 
-/* t_m (Section 4.4): for every row of logits [n x vocab] (dtype dt; e.g. as stored by
- * hmoe_moe_forward -- the softmax keeps the order, so these are the m most probable tags), the
- * indices of its m largest entries in decreasing order, equal values in increasing index
- * order.  idx int32[n][m] out; val float[n][m] out or NULL (the entries at those indices).
- * 1 <= m <= 16, m <= vocab; the entries are assumed finite.  One wave per row; the logits are
- * read once.  Errors: HMOE_EINVAL (m out of range, NULL logits or idx), HMOE_ESHAPE (vocab
- * not a multiple of 8). */
-int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m, int32_t* idx,
-              float* val, void* stream);
+/* t_m (Section 4.4): for every row of logits [n x vocab] (dtype dt; the softmax keeps the
+ * order, so these are the m most probable tags), the indices of its m largest entries in
+ * decreasing order, equal values in increasing index order.  With anchor (float, the layout of
+ * HMOE_ANCHOR_*, as written by hmoe_moe_forward) an entry is anchor + stored value, formed in
+ * fp32; with anchor NULL it is the stored value.  idx int32[n][m] out; val float[n][m] out or
+ * NULL (the entries at those indices).  1 <= m <= 16, m <= vocab; the entries are assumed
+ * finite or -inf.  One wave per row; the logits are read once.  Errors: HMOE_EINVAL (m out of
+ * range, NULL logits or idx), HMOE_ESHAPE (vocab not a multiple of 8). */
+int hmoe_topm(const void* logits, const float* anchor, hmoe_dtype_t dt, int64_t n, int32_t vocab,
+              int32_t m, int32_t* idx, float* val, void* stream);
 
 /* The counts behind p@m (Eq. 4) and q@m (Eq. 5), Section 4.4, for every m' = 1..m, from the
  * top-m lists idx int32[n][m] (hmoe_topm):

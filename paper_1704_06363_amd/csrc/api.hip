@@ -299,8 +299,9 @@ size_t hmoe_moe_workspace(const hmoe_moe_params_t* p, int64_t n) {
 }
 
 int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
-                     const int32_t* perm, const hmoe_labels_t* y, void* H1_sorted, void* H, void* logits, float* lse,
-                     float* loss, float* loss_mean, void* ws, size_t ws_bytes, void* stream) {
+                     const int32_t* perm, const hmoe_labels_t* y, void* H1_sorted, void* H, void* logits,
+                     float* logit_anchor, float* lse, float* loss, float* loss_mean, void* ws, size_t ws_bytes,
+                     void* stream) {
   clear_error();
   HMOE_TRY(check_params(p));
   HMOE_TRY(check_n(n));
@@ -313,20 +314,24 @@ int hmoe_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted
   HMOE_TRY(check_ptr("labels.tag", y->tag, false));
   HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
   HMOE_TRY(check_ptr("H", H));
-  if (logits) HMOE_TRY(check_ptr("logits", logits));
+  if (logits) {
+    HMOE_TRY(check_ptr("logits", logits));
+    HMOE_TRY(check_ptr("logit_anchor (required with logits)", logit_anchor));
+  }
   HMOE_TRY(check_ptr("lse", lse, false));
   HMOE_TRY(check_ptr("loss", loss, false));
   HMOE_TRY(check_ptr("loss_mean", loss_mean, false));
   HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
   Workspace w(ws, ws_bytes);
-  return launch_moe_forward(p, n, X_sorted, offsets, perm, y, H1_sorted, H, logits, lse, loss, loss_mean, w,
-                            (hipStream_t)stream);
+  return launch_moe_forward(p, n, X_sorted, offsets, perm, y, H1_sorted, H, logits, logit_anchor, lse, loss,
+                            loss_mean, w, (hipStream_t)stream);
 }
 
 int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorted, const int32_t* offsets,
                       const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1_sorted,
-                      const void* H, const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
-                      float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes, void* stream) {
+                      const void* H, const void* logits, const float* logit_anchor, const float* lse, float* dW1,
+                      float* db1, float* dW2, float* db2, float* dD, float* dbD, void* dX, void* ws, size_t ws_bytes,
+                      void* stream) {
   clear_error();
   HMOE_TRY(check_params(p));
   HMOE_TRY(check_n(n));
@@ -356,14 +361,16 @@ int hmoe_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* X_sorte
   HMOE_TRY(check_ptr("H1_sorted", H1_sorted));
   HMOE_TRY(check_ptr("H", H));
   HMOE_TRY(check_ptr("lse", lse, false));
-  if (logits) HMOE_TRY(check_ptr("logits", logits));
-  else if (p->decoders > 1)
+  if (logits) {
+    HMOE_TRY(check_ptr("logits", logits));
+    HMOE_TRY(check_ptr("logit_anchor (required with logits)", logit_anchor));
+  } else if (p->decoders > 1)
     return fail(HMOE_EINVAL, "with one decoder per expert the backward needs the forward's saved logits");
   if (dX) HMOE_TRY(check_ptr("dX", dX));
   HMOE_TRY(check_ws(moe_ws_bytes(p, n), ws_bytes, ws));
   Workspace w(ws, ws_bytes);
-  return launch_moe_backward(p, n, X_sorted, offsets, perm, inv, y, H1_sorted, H, logits, lse, dW1, db1, dW2, db2,
-                             dD, dbD, dX, w, (hipStream_t)stream);
+  return launch_moe_backward(p, n, X_sorted, offsets, perm, inv, y, H1_sorted, H, logits, logit_anchor, lse, dW1,
+                             db1, dW2, db2, dD, dbD, dX, w, (hipStream_t)stream);
 }
 
 static int check_pca(hmoe_dtype_t dt, int64_t n, int32_t d, int32_t r) {
@@ -426,8 +433,8 @@ int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t d
                     (hipStream_t)stream);
 }
 
-int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m, int32_t* idx, float* val,
-              void* stream) {
+int hmoe_topm(const void* logits, const float* anchor, hmoe_dtype_t dt, int64_t n, int32_t vocab, int32_t m,
+              int32_t* idx, float* val, void* stream) {
   clear_error();
   HMOE_TRY(check_dtype(dt));
   HMOE_TRY(check_n(n));
@@ -436,7 +443,8 @@ int hmoe_topm(const void* logits, hmoe_dtype_t dt, int64_t n, int32_t vocab, int
   if (n == 0) return HMOE_OK;
   HMOE_TRY(check_ptr("logits", logits));
   HMOE_TRY(check_ptr("idx", idx, false));
-  return launch_topm(logits, dt, n, vocab, m, idx, val, (hipStream_t)stream);
+  if (anchor) HMOE_TRY(check_ptr("anchor", anchor, false));
+  return launch_topm(logits, anchor, dt, n, vocab, m, idx, val, (hipStream_t)stream);
 }
 
 int hmoe_topm_hits(const int32_t* idx, int64_t n, int32_t m, const hmoe_labels_t* y, const int32_t* q_sample,

@@ -63,6 +63,18 @@ __device__ __forceinline__ void argmin_merge(float& v, int& i, float v2, int i2)
 
 __host__ __device__ __forceinline__ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Stored decoder logits are offsets from a per-row anchor, one per 64 columns (the row maximum
+// over those columns): logit[row][v] = anc[v / 256][row][(v % 256) / 64] + stored[row][v].
+constexpr int kAnchorCols = HMOE_ANCHOR_COLS;
+constexpr int kAnchorTile = HMOE_ANCHOR_TILE;
+constexpr int kAnchorSlots = kAnchorTile / kAnchorCols;
+__host__ __device__ __forceinline__ int64_t anchor_index(int64_t n, int64_t row, int64_t col) {
+  return ((col / kAnchorTile) * n + row) * kAnchorSlots + (col % kAnchorTile) / kAnchorCols;
+}
+__host__ __forceinline__ int64_t anchor_count(int64_t n, int64_t vocab) {
+  return cdiv(vocab, kAnchorTile) * n * kAnchorSlots;
+}
+
 template <typename T>
 struct DT;
 template <>

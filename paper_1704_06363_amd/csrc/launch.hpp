@@ -30,7 +30,8 @@ int launch_pca_project(const void* X, hmoe_dtype_t dt, int64_t n, int d, const f
                        int r, void* Z, Workspace& ws, hipStream_t st);
 int launch_sgd(float* w, const float* g, float* v, void* wlo, hmoe_dtype_t dt, int64_t count, float lr, float wd,
                float mu, hipStream_t st);
-int launch_topm(const void* L, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st);
+int launch_topm(const void* L, const float* anc, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val,
+                hipStream_t st);
 int launch_topm_hits(const int32_t* idx, int64_t n, int m, const hmoe_labels_t* y, const int32_t* q_sample,
                      const int32_t* q_tag, int64_t S, int64_t* hits, hipStream_t st);
 size_t segsum_ws(int64_t n, int G, int w);
@@ -58,10 +59,11 @@ int launch_update(const void* X, hmoe_dtype_t dt, int64_t n, int32_t d, int32_t 
 size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n);
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                        const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits,
-                       float* lse, float* loss, float* loss_mean, Workspace& ws, hipStream_t st);
+                       float* anc, float* lse, float* loss, float* loss_mean, Workspace& ws, hipStream_t st);
 int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                         const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y,
-                        const void* H1s, const void* H, const void* logits, const float* lse, float* dW1,
+                        const void* H1s, const void* H, const void* logits, const float* anc, const float* lse,
+                        float* dW1,
                         float* db1, float* dW2, float* db2, float* dD, float* dbD, void* dX, Workspace& ws,
                         hipStream_t st);
 

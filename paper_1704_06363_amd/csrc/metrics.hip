@@ -2,8 +2,10 @@
 // (the softmax keeps their order, so these are the m most probable tags), and the counts
 // behind p@m (Eq. 4) and q@m (Eq. 5) for every m' <= m.
 //
-// k_topm: one wave per row.  Lane l reads the row's 16-byte vectors l, l + 64, ... (so it sees
-// its entries in increasing index order) and keeps its own M largest in a register list sorted
+// k_topm: one wave per row.  An entry is the stored value, plus its anchor when the logits are
+// stored relative to per-row anchors (the forward's layout), the sum formed in fp32.
+// Lane l reads the row's 16-byte vectors l, l + 64, ... (so it sees its entries in increasing
+// index order) and keeps its own M largest in a register list sorted
 // by decreasing value; an entry enters only when strictly greater than the list's last, which
 // with the index order keeps equal values in increasing index order, and only when it is not
 // below a wave-wide bound on the row's m-th value (the m-th largest of the lanes' maxima).
@@ -20,8 +22,8 @@
 namespace hmoe {
 
 template <typename T, int M>
-__global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n, int V, int m,
-                                              int32_t* __restrict__ idx, float* __restrict__ val) {
+__global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, const float* __restrict__ anc, int64_t n,
+                                              int V, int m, int32_t* __restrict__ idx, float* __restrict__ val) {
   constexpr int EPV = 16 / sizeof(T);
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
@@ -45,10 +47,16 @@ __global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n
   int step = 0;
   for (int b0 = 0; b0 < nvec; b0 += 64 * U, ++step) {
     i32x4 raw[U];
+    float an[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = b0 + 64 * u + l;
-      if (v < nvec) raw[u] = *reinterpret_cast<const i32x4*>(r + (int64_t)v * EPV);
+      an[u] = 0.f;
+      if (v < nvec) {
+        raw[u] = *reinterpret_cast<const i32x4*>(r + (int64_t)v * EPV);
+        // the vector's anchor (a 16-byte vector never straddles a 64-column block)
+        if (anc) an[u] = anc[anchor_index(n, row, (int64_t)v * EPV)];
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -59,7 +67,7 @@ __global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n
       float vmax = -INFINITY;
 #pragma unroll
       for (int z = 0; z < EPV; ++z) {
-        f[z] = to_f32(e[z]);
+        f[z] = anc ? an[u] + to_f32(e[z]) : to_f32(e[z]);
         vmax = fmaxf(vmax, f[z]);
       }
       if (!(vmax >= thr && vmax > lv[M - 1])) continue;  // the common case: nothing here enters
@@ -68,10 +76,13 @@ __global__ void __launch_bounds__(256) k_topm(const T* __restrict__ L, int64_t n
         float cv = f[z];
         if (cv >= thr && cv > lv[M - 1]) {
           int ci = v * EPV + z;
-          // carry the entry down the list: it goes before the first strictly smaller one
+          // carry the entry down the list, ordered by (value desc, index asc): the new entry has
+          // the largest index the lane has seen, so it goes before the first strictly smaller
+          // one; an entry it displaces is carried on by the same order, ahead of equal values
+          // with higher indices
 #pragma unroll
           for (int k = 0; k < M; ++k) {
-            const bool gt = cv > lv[k];
+            const bool gt = cv > lv[k] || (cv == lv[k] && ci < li[k]);
             const float tv = lv[k];
             const int ti = li[k];
             lv[k] = gt ? cv : tv;
@@ -171,38 +182,40 @@ __global__ void __launch_bounds__(256) k_topm_hits(const int32_t* __restrict__ i
 }
 
 template <typename T, int M>
-static int topm_launch(const T* L, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
-  HMOE_LAUNCH("top-m", (k_topm<T, M>), dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, L, n, V, m, idx, val);
+static int topm_launch(const T* L, const float* anc, int64_t n, int V, int m, int32_t* idx, float* val,
+                       hipStream_t st) {
+  HMOE_LAUNCH("top-m", (k_topm<T, M>), dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, L, anc, n, V, m, idx, val);
   return HMOE_OK;
 }
 
 // The register lists hold exactly m entries (the insertion and the registers scale with the
 // list length: a 16-entry list for m = 10 ran 25% slower than a 12-entry one).
 template <typename T>
-static int topm_t(const T* L, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
+static int topm_t(const T* L, const float* anc, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
   switch (m) {
-    case 1: return topm_launch<T, 1>(L, n, V, m, idx, val, st);
-    case 2: return topm_launch<T, 2>(L, n, V, m, idx, val, st);
-    case 3: return topm_launch<T, 3>(L, n, V, m, idx, val, st);
-    case 4: return topm_launch<T, 4>(L, n, V, m, idx, val, st);
-    case 5: return topm_launch<T, 5>(L, n, V, m, idx, val, st);
-    case 6: return topm_launch<T, 6>(L, n, V, m, idx, val, st);
-    case 7: return topm_launch<T, 7>(L, n, V, m, idx, val, st);
-    case 8: return topm_launch<T, 8>(L, n, V, m, idx, val, st);
-    case 9: return topm_launch<T, 9>(L, n, V, m, idx, val, st);
-    case 10: return topm_launch<T, 10>(L, n, V, m, idx, val, st);
-    case 11: return topm_launch<T, 11>(L, n, V, m, idx, val, st);
-    case 12: return topm_launch<T, 12>(L, n, V, m, idx, val, st);
-    case 13: return topm_launch<T, 13>(L, n, V, m, idx, val, st);
-    case 14: return topm_launch<T, 14>(L, n, V, m, idx, val, st);
-    case 15: return topm_launch<T, 15>(L, n, V, m, idx, val, st);
-    default: return topm_launch<T, 16>(L, n, V, m, idx, val, st);
+    case 1: return topm_launch<T, 1>(L, anc, n, V, m, idx, val, st);
+    case 2: return topm_launch<T, 2>(L, anc, n, V, m, idx, val, st);
+    case 3: return topm_launch<T, 3>(L, anc, n, V, m, idx, val, st);
+    case 4: return topm_launch<T, 4>(L, anc, n, V, m, idx, val, st);
+    case 5: return topm_launch<T, 5>(L, anc, n, V, m, idx, val, st);
+    case 6: return topm_launch<T, 6>(L, anc, n, V, m, idx, val, st);
+    case 7: return topm_launch<T, 7>(L, anc, n, V, m, idx, val, st);
+    case 8: return topm_launch<T, 8>(L, anc, n, V, m, idx, val, st);
+    case 9: return topm_launch<T, 9>(L, anc, n, V, m, idx, val, st);
+    case 10: return topm_launch<T, 10>(L, anc, n, V, m, idx, val, st);
+    case 11: return topm_launch<T, 11>(L, anc, n, V, m, idx, val, st);
+    case 12: return topm_launch<T, 12>(L, anc, n, V, m, idx, val, st);
+    case 13: return topm_launch<T, 13>(L, anc, n, V, m, idx, val, st);
+    case 14: return topm_launch<T, 14>(L, anc, n, V, m, idx, val, st);
+    case 15: return topm_launch<T, 15>(L, anc, n, V, m, idx, val, st);
+    default: return topm_launch<T, 16>(L, anc, n, V, m, idx, val, st);
   }
 }
 
-int launch_topm(const void* L, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
-  if (dt == HMOE_BF16) return topm_t<bf16>((const bf16*)L, n, V, m, idx, val, st);
-  return topm_t<float>((const float*)L, n, V, m, idx, val, st);
+int launch_topm(const void* L, const float* anc, hmoe_dtype_t dt, int64_t n, int V, int m, int32_t* idx, float* val,
+                hipStream_t st) {
+  if (dt == HMOE_BF16) return topm_t<bf16>((const bf16*)L, anc, n, V, m, idx, val, st);
+  return topm_t<float>((const float*)L, anc, n, V, m, idx, val, st);
 }
 
 int launch_topm_hits(const int32_t* idx, int64_t n, int m, const hmoe_labels_t* y, const int32_t* q_sample,

@@ -85,11 +85,14 @@ __device__ __forceinline__ void add_bias(floatx4 (&acc)[C::MI][C::NJ], const flo
 }
 
 // Per-wave row statistics of a logits tile: m = max over the wave's valid columns of the row,
-// s = sum exp(logit - m) (as exp2 of logit log2(e) - m log2(e)), into rm / rs [WAVES_N][BM].
+// s = sum exp(logit - m), into rm / rs [WAVES_N][BM].  The valid accumulators become the
+// offsets logit - m in place (m is the row's anchor for this wave's 64 columns: what a stored
+// logit is relative to), and s is the sum of exp2(offset log2(e)).
 // FULL: every column of the tile is valid (no column guards).
 template <class C, bool FULL>
-__device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+__device__ __forceinline__ void dec_row_stats(const TileCoord& tc, floatx4 (&acc)[C::MI][C::NJ],
                                               lds<float>* rm, lds<float>* rs) {
+  static_assert(C::WN == kAnchorCols, "one anchor per wave and row");
   using F = Frag<C>;
   const F f;
   constexpr float kLog2e = 1.4426950408889634f;
@@ -105,13 +108,15 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4
           if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
       mx = fmaxf(mx, shfl_xor(mx, 16));
       mx = fmaxf(mx, shfl_xor(mx, 32));
-      const float mb = mx * kLog2e;
       float s = 0.f;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
+          if (FULL || f.col(j, r) < tc.n_cols) {
+            acc[i][j][r] -= mx;
+            s += __builtin_amdgcn_exp2f(acc[i][j][r] * kLog2e);
+          }
       s += shfl_xor(s, 16);
       s += shfl_xor(s, 32);
       if (f.lg == 0) {
@@ -131,11 +136,13 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4
           if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
-        const float mb = mx * kLog2e;
         float s = 0.f;
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j)
-          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
+          if (FULL || f.col(j, r) < tc.n_cols) {
+            acc[i][j][r] -= mx;
+            s += __builtin_amdgcn_exp2f(acc[i][j][r] * kLog2e);
+          }
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
         if (f.lr == 0) {
@@ -151,33 +158,44 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4
 // waves that share the row through rm / rs (LDS, [WAVES_N][BM] floats each) and written as the
 // tile's partials pm[n-tile][row], ps[n-tile][row].  Entered by the whole workgroup.
 // The second half of dec_tile_stats: after the waves' row partials are in LDS, merge them per
-// row and write the tile's (max, sum) pair.
+// row and write the tile's (max, sum) pair, and (anc != NULL) the waves' row maxima as the
+// anchors of the stored logits: anc[v / 256][row][(v % 256) / 64] for column v.  A wave with no
+// valid column writes -FLT_MAX into a slot no stored logit refers to.
 template <class C, bool BARRIER = true>
 __device__ __forceinline__ void dec_stats_merge(const TileCoord& tc, lds<float>* rm, lds<float>* rs, int64_t n,
-                                                float* __restrict__ pm, float* __restrict__ ps) {
+                                                float* __restrict__ pm, float* __restrict__ ps,
+                                                float* __restrict__ anc) {
+  static_assert(C::WN == kAnchorCols && (kAnchorTile / C::BN) * C::BN == kAnchorTile, "anchor slots per tile");
+  typedef float avec __attribute__((ext_vector_type(C::WAVES_N)));
   if constexpr (BARRIER) wg_barrier_lds();
   for (int t = threadIdx.x; t < tc.m_rows; t += C::THREADS) {
-    float M = rm[t];
+    avec mw;
 #pragma unroll
-    for (int w = 1; w < C::WAVES_N; ++w) M = fmaxf(M, rm[w * C::BM + t]);
+    for (int w = 0; w < C::WAVES_N; ++w) mw[w] = rm[w * C::BM + t];
+    float M = mw[0];
+#pragma unroll
+    for (int w = 1; w < C::WAVES_N; ++w) M = fmaxf(M, mw[w]);
     float S = 0.f;
 #pragma unroll
-    for (int w = 0; w < C::WAVES_N; ++w) S += rs[w * C::BM + t] * __expf(rm[w * C::BM + t] - M);
+    for (int w = 0; w < C::WAVES_N; ++w) S += rs[w * C::BM + t] * __expf(mw[w] - M);
     const int64_t at = (int64_t)(tc.n0 / C::BN) * n + tc.m0 + t;
     pm[at] = M;
     ps[at] = S;
+    if (anc)
+      *reinterpret_cast<avec*>(anc + ((int64_t)(tc.n0 / kAnchorTile) * n + tc.m0 + t) * kAnchorSlots +
+                               (tc.n0 % kAnchorTile) / kAnchorCols) = mw;
   }
 }
 
 template <class C>
-__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, floatx4 (&acc)[C::MI][C::NJ],
                                                lds<float>* rm, lds<float>* rs, int64_t n, float* __restrict__ pm,
-                                               float* __restrict__ ps) {
+                                               float* __restrict__ ps, float* __restrict__ anc) {
   if (tc.n_cols == C::BN)
     dec_row_stats<C, true>(tc, acc, rm, rs);
   else
     dec_row_stats<C, false>(tc, acc, rm, rs);
-  dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
+  dec_stats_merge<C>(tc, rm, rs, n, pm, ps, anc);
 }
 
 template <class C>
@@ -193,13 +211,13 @@ __device__ __forceinline__ void dec_tile_bias(const TileCoord& tc, const typenam
 }
 
 // Per row and V-tile: the softmax partials (dec_tile_stats); the logits themselves are stored
-// to L when L is given (saved for the backward).  One tile per workgroup (register-staged
-// engine).
+// to L when L is given (saved for the backward), as offsets from their anchors (anc).  One tile
+// per workgroup (register-staged engine).
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_fwd(const typename C::type* __restrict__ H, const typename C::type* __restrict__ D,
               const typename C::type* __restrict__ bD, int64_t n, int V, int o, float* __restrict__ pm,
-              float* __restrict__ ps, typename C::type* __restrict__ L) {
+              float* __restrict__ ps, typename C::type* __restrict__ L, float* __restrict__ anc) {
   using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
@@ -212,7 +230,7 @@ __global__ void __launch_bounds__(C::THREADS)
   dec_tile_bias<C>(tc, bD, bias);
   add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
     store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
@@ -221,13 +239,13 @@ __global__ void __launch_bounds__(C::THREADS)
 
 // One decoder per expert (row-grouped): the slot rows of expert e against D_e [V][o] and
 // bD_e; the softmax partials (dec_tile_stats, rows in slot order) and, when L is given, the
-// logits in slot order.  One tile per workgroup.
+// logits (offsets from their anchors) and the anchors in slot order.  One tile per workgroup.
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_fwd_grouped(const typename C::type* __restrict__ Hs, const typename C::type* __restrict__ D,
                       const typename C::type* __restrict__ bD, const int32_t* __restrict__ seg,
                       const int32_t* __restrict__ tile_start, int G, int64_t n, int V, int o, float* __restrict__ pm,
-                      float* __restrict__ ps, typename C::type* __restrict__ L) {
+                      float* __restrict__ ps, typename C::type* __restrict__ L, float* __restrict__ anc) {
   using T = typename C::type;
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds<char>* smem = (lds<char>*)smem_raw;
@@ -241,7 +259,7 @@ __global__ void __launch_bounds__(C::THREADS)
   dec_tile_bias<C>(tc, bD ? bD + (int64_t)tc.group * V : nullptr, bias);
   add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps);
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
     store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
@@ -274,7 +292,8 @@ __device__ __forceinline__ void dec_bias_packed(const TileCoord& tc, const bf16*
 template <class C>
 __global__ void __launch_bounds__(C::THREADS)
     k_dec_fwd_stream(const bf16* __restrict__ H, const bf16* __restrict__ D, const bf16* __restrict__ bD, int64_t n,
-                     int V, int o, float* __restrict__ pm, float* __restrict__ ps, bf16* __restrict__ L) {
+                     int V, int o, float* __restrict__ pm, float* __restrict__ ps, bf16* __restrict__ L,
+                     float* __restrict__ anc) {
   static_assert(C::DMA && C::TRANS, "persistent decoder forward runs the direct-to-LDS engine");
   static_assert(2 * C::WAVES_N * C::BM * (int)sizeof(float) <= kDecStatLds, "statistics scratch");
   constexpr int STORES = direct_stores<C, bf16>();  // per wave, for a full tile
@@ -338,10 +357,10 @@ __global__ void __launch_bounds__(C::THREADS)
     // order them; its buffer is rewritten only after the next K loop
     if (have_prev) {
       lds<float>* pm_l = rm0 + (buf ^ 1) * SB;
-      dec_stats_merge<C, false>(pc, pm_l, pm_l + C::WAVES_N * C::BM, n, pm, ps);
+      dec_stats_merge<C, false>(pc, pm_l, pm_l + C::WAVES_N * C::BM, n, pm, ps, anc);
     }
     if (!more) {
-      dec_stats_merge<C>(tc, rm, rs, n, pm, ps);
+      dec_stats_merge<C>(tc, rm, rs, n, pm, ps, anc);
       break;
     }
     stores_pending = L != nullptr && tc.m_rows == C::BM && tc.n_cols == C::BN;
@@ -636,8 +655,10 @@ __global__ void __launch_bounds__(C::THREADS)
   store_out<C, T>(tc, acc, smem, G, V, Ident{}, RowId{tc.m0}, NoVec{});
 }
 
-// Saved-logits path: g = (exp(L - lse) - y) / n elementwise over [n x V]; each thread owns one
-// 16-byte column vector over kGradRows rows and writes its column sums to part_db[rowblock][V].
+// Saved-logits path: g = (exp(anchor + L - lse) - y) / n elementwise over [n x V] (L holds the
+// logits as offsets from their anchors, anc, one per row and 64 columns); each thread owns one
+// 16-byte column vector over kGradRows rows, whose anchors are one per row (a vector never
+// straddles a 64-column block), and writes its column sums to part_db[rowblock][V].
 // A block covers a slab of 256 x EPV columns; per row it keeps (in LDS) only the tags that fall
 // inside its slab, so the per-element work is an fma and an exp, and a tag costs one compare
 // per row in the few rows that have one here.  A row with more than MAXT tags in the slab
@@ -650,7 +671,8 @@ __global__ void __launch_bounds__(C::THREADS)
 constexpr int kGradRows = 256;
 
 template <typename T>
-__global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, const float* __restrict__ lse,
+__global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, const float* __restrict__ anc,
+                                                       const float* __restrict__ lse,
                                                        const int32_t* __restrict__ row_ptr,
                                                        const int32_t* __restrict__ tag, int64_t n, int V,
                                                        float inv_n, const int32_t* __restrict__ perm,
@@ -698,22 +720,29 @@ __global__ void __launch_bounds__(256) k_dec_grad_elem(const T* __restrict__ L, 
   float cs[EPV];
 #pragma unroll
   for (int e = 0; e < EPV; ++e) cs[e] = 0.f;
+  // this thread's anchors: anc[c0 / 256][row][(c0 % 256) / 64], kAnchorSlots floats per row
+  const float* arow = anc + anchor_index(n, r0, c0);
   // rows in groups of U: all U loads in flight before the arithmetic of the group
   constexpr int U = 4;
   for (int t0 = 0; t0 < rows; t0 += U) {
     i32x4 raw[U];
+    float an[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (t0 + u < rows) raw[u] = *reinterpret_cast<const i32x4*>(L + (r0 + t0 + u) * V + c0);
+      if (t0 + u < rows) {
+        raw[u] = *reinterpret_cast<const i32x4*>(L + (r0 + t0 + u) * V + c0);
+        an[u] = arow[(int64_t)(t0 + u) * kAnchorSlots];
+      }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int t = t0 + u;
       if (t >= rows) break;
       const T* lv = reinterpret_cast<const T*>(&raw[u]);
-      const float l2 = s_lse2[t];
+      // exp(anchor + offset - lse) = exp2(offset log2(e) + (anchor log2(e) - lse log2(e)))
+      const float l2 = fmaf(an[u], kLog2e, -s_lse2[t]);
       float g[EPV];
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) g[e] = __builtin_amdgcn_exp2f(fmaf(to_f32(lv[e]), kLog2e, -l2)) * inv_n;
+      for (int e = 0; e < EPV; ++e) g[e] = __builtin_amdgcn_exp2f(fmaf(to_f32(lv[e]), kLog2e, l2)) * inv_n;
       const int32_t k = s_cnt[t];
       if (k != 0) {
         const float yn = s_yn[t];
@@ -1022,8 +1051,8 @@ size_t moe_ws_bytes(const hmoe_moe_params_t* p, int64_t n) {
 
 template <typename T>
 static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
-                     const hmoe_labels_t* y, T* H1s, T* H, T* Lg, float* lse, float* loss, float* loss_mean,
-                     Workspace& ws, hipStream_t st) {
+                     const hmoe_labels_t* y, T* H1s, T* H, T* Lg, float* anc, float* lse, float* loss,
+                     float* loss_mean, Workspace& ws, hipStream_t st) {
   using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
   const int ntv = (int)cdiv(s.V, C::BN);
@@ -1035,6 +1064,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   const T* W1 = (const T*)p->W1;
   const T* W2 = (const T*)p->W2;
   const T* D = (const T*)p->D;
+  if (!Lg) anc = nullptr;
   HMOE_TRY(launch_seg_tiles(offsets, s.K, C::BM, ts, st));
   const int64_t mt_bound = cdiv(n, C::BM) + s.K;
   HMOE_LAUNCH("expert layer 1", (k_expert_fwd<C, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
@@ -1045,7 +1075,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
     // one decoder per expert: decode in slot order
     HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
     HMOE_LAUNCH("decoder forward", k_dec_fwd_grouped<C>, dim3((unsigned)(mt_bound * ntv)), dim3(C::THREADS), C::LDS,
-                st, (const T*)Hs, D, (const T*)p->bD, offsets, ts, s.K, n, s.V, s.o, pm, ps, Lg);
+                st, (const T*)Hs, D, (const T*)p->bD, offsets, ts, s.K, n, s.V, s.o, pm, ps, Lg, anc);
     HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, kLossRows)), dim3(256), 0, st, pm, ps, ntv,
                 (const T*)Hs, D, (const T*)p->bD, n, s.o, s.V, perm, offsets, s.K, y->row_ptr, y->tag, lse, loss);
     return launch_sum_f32(loss, n, 1.0 / (double)n, nullptr, loss_mean, ws, st);
@@ -1057,10 +1087,10 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
     int64_t slots = (int64_t)device_cus() * ((160 * 1024) / lds_bytes);
     if (slots > tiles) slots = tiles;
     HMOE_LAUNCH("decoder forward", k_dec_fwd_stream<C>, dim3((unsigned)slots), dim3(C::THREADS), lds_bytes, st,
-                (const bf16*)H, (const bf16*)D, (const bf16*)p->bD, n, s.V, s.o, pm, ps, (bf16*)Lg);
+                (const bf16*)H, (const bf16*)D, (const bf16*)p->bD, n, s.V, s.o, pm, ps, (bf16*)Lg, anc);
   } else {
     HMOE_LAUNCH("decoder forward", k_dec_fwd<C>, dim3((unsigned)(cdiv(n, C::BM) * ntv)), dim3(C::THREADS), C::LDS,
-                st, (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg);
+                st, (const T*)H, D, (const T*)p->bD, n, s.V, s.o, pm, ps, Lg, anc);
   }
   HMOE_LAUNCH("decoder loss", k_dec_loss<T>, dim3((unsigned)cdiv(n, kLossRows)), dim3(256), 0, st, pm, ps, ntv, (const T*)H, D,
               (const T*)p->bD, n, s.o, s.V, (const int32_t*)nullptr, (const int32_t*)nullptr, 0, y->row_ptr,
@@ -1071,7 +1101,7 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
 template <typename T>
 static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const int32_t* offsets, const int32_t* perm,
                       const int32_t* inv, const hmoe_labels_t* y, const T* H1s, const T* H, const T* Lg,
-                      const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX,
+                      const float* anc, const float* lse, float* dW1, float* db1, float* dW2, float* db2, float* dD, float* dbD, T* dX,
                       Workspace& ws, hipStream_t st) {
   using C = typename Pick<T>::C;
   const MoeShape s = shape_of(p, n);
@@ -1109,7 +1139,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
     // column sums, dH = g D_e (row-grouped), dD_e = g_e^T H_e (reduction-grouped).
     HMOE_TRY(launch_seg_tiles(offsets, s.K, kGradRows, gts, st));
     HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)(gr + s.K), (unsigned)cdiv(s.V, 256 * EPV)),
-                dim3(256), 0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), perm, offsets,
+                dim3(256), 0, st, Lg, anc, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), perm, offsets,
                 gts, s.K, G, pdb, 0);
     if (dbD)
       HMOE_LAUNCH("decoder bias grad", k_piece_colsum, dim3((unsigned)cdiv(s.V, 256), (unsigned)s.K), dim3(256), 0,
@@ -1126,7 +1156,7 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
   int prow;
   if (Lg) {
     HMOE_LAUNCH("decoder grad", k_dec_grad_elem<T>, dim3((unsigned)gr, (unsigned)cdiv(s.V, 256 * EPV)), dim3(256),
-                0, st, Lg, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), (const int32_t*)nullptr,
+                0, st, Lg, anc, lse, y->row_ptr, y->tag, n, s.V, (float)(1.0 / (double)n), (const int32_t*)nullptr,
                 (const int32_t*)nullptr, (const int32_t*)nullptr, 0, G, pdb, (int)slab);
     prow = gr;
   } else {
@@ -1221,24 +1251,25 @@ template int launch_gemm_tn<bf16>(const bf16*, const bf16*, int64_t, int, int, f
 template int launch_gemm_nn<float>(const float*, const float*, int64_t, int, int, float*, Workspace&, hipStream_t);
 
 int launch_moe_forward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
-                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits, float* lse,
-                       float* loss, float* loss_mean, Workspace& ws, hipStream_t st) {
+                       const int32_t* perm, const hmoe_labels_t* y, void* H1s, void* H, void* logits, float* anc,
+                       float* lse, float* loss, float* loss_mean, Workspace& ws, hipStream_t st) {
   if (p->dt == HMOE_BF16)
-    return forward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, y, (bf16*)H1s, (bf16*)H, (bf16*)logits, lse, loss,
-                           loss_mean, ws, st);
-  return forward_t<float>(p, n, (const float*)Xs, offsets, perm, y, (float*)H1s, (float*)H, (float*)logits, lse, loss,
-                          loss_mean, ws, st);
+    return forward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, y, (bf16*)H1s, (bf16*)H, (bf16*)logits, anc, lse,
+                           loss, loss_mean, ws, st);
+  return forward_t<float>(p, n, (const float*)Xs, offsets, perm, y, (float*)H1s, (float*)H, (float*)logits, anc, lse,
+                          loss, loss_mean, ws, st);
 }
 
 int launch_moe_backward(const hmoe_moe_params_t* p, int64_t n, const void* Xs, const int32_t* offsets,
                         const int32_t* perm, const int32_t* inv, const hmoe_labels_t* y, const void* H1s,
-                        const void* H, const void* logits, const float* lse, float* dW1, float* db1, float* dW2,
-                        float* db2, float* dD, float* dbD, void* dX, Workspace& ws, hipStream_t st) {
+                        const void* H, const void* logits, const float* anc, const float* lse, float* dW1,
+                        float* db1, float* dW2, float* db2, float* dD, float* dbD, void* dX, Workspace& ws,
+                        hipStream_t st) {
   if (p->dt == HMOE_BF16)
     return backward_t<bf16>(p, n, (const bf16*)Xs, offsets, perm, inv, y, (const bf16*)H1s, (const bf16*)H,
-                            (const bf16*)logits, lse, dW1, db1, dW2, db2, dD, dbD, (bf16*)dX, ws, st);
+                            (const bf16*)logits, anc, lse, dW1, db1, dW2, db2, dD, dbD, (bf16*)dX, ws, st);
   return backward_t<float>(p, n, (const float*)Xs, offsets, perm, inv, y, (const float*)H1s, (const float*)H,
-                           (const float*)logits, lse, dW1, db1, dW2, db2, dD, dbD, (float*)dX, ws, st);
+                           (const float*)logits, anc, lse, dW1, db1, dW2, db2, dD, dbD, (float*)dX, ws, st);
 }
 
 }  // namespace hmoe

@@ -81,16 +81,16 @@ def lib():
                                         _P, _SZ, _P]
         L.hmoe_permute_rows.argtypes = [_P, _P, _P, _I64, _I32, _c.c_int, _P]
         L.hmoe_moe_forward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P,
-                                       _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+                                       _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
         L.hmoe_moe_backward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P, _P,
                                         _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                        _P, _P, _P, _SZ, _P]
+                                        _P, _P, _P, _P, _SZ, _P]
         L.hmoe_pca_workspace.restype = _SZ
         L.hmoe_pca_workspace.argtypes = [_I64, _I32, _I32, _c.c_int]
         L.hmoe_pca_fit.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _I32, _c.c_uint64, _P, _P, _P, _P, _SZ, _P]
         L.hmoe_pca_project.argtypes = [_P, _c.c_int, _I64, _I32, _P, _P, _I32, _P, _P, _SZ, _P]
         L.hmoe_sgd_step.argtypes = [_P, _P, _P, _P, _c.c_int, _I64, _c.c_float, _c.c_float, _c.c_float, _P]
-        L.hmoe_topm.argtypes = [_P, _c.c_int, _I64, _I32, _I32, _P, _P, _P]
+        L.hmoe_topm.argtypes = [_P, _P, _c.c_int, _I64, _I32, _I32, _P, _P, _P]
         L.hmoe_topm_hits.argtypes = [_P, _I64, _I32, _c.POINTER(Labels), _P, _P, _I64, _P, _P]
         L.hmoe_timer_enable.argtypes = [_c.c_int]
         L.hmoe_timer_enable.restype = _c.c_int
@@ -300,11 +300,20 @@ def moe_workspace(params: MoeParams, n) -> int:
     return lib().hmoe_moe_workspace(ctypes.byref(params), n)
 
 
+ANCHOR_COLS, ANCHOR_TILE = 64, 256  # include/hmoe.h: HMOE_ANCHOR_COLS, HMOE_ANCHOR_TILE
+
+
+def anchor_shape(n: int, V: int):
+    """Shape of the anchors of n rows of V stored logits: [ceil(V / 256), n, 4]."""
+    return ((V + ANCHOR_TILE - 1) // ANCHOR_TILE, n, ANCHOR_TILE // ANCHOR_COLS)
+
+
 def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None,
                 save_logits=False):
     """Expert MLPs + decoder(s) + multilabel softmax loss (Eq. 3).  With save_logits the
     [n, V] logits are returned too (for a backward that does not recompute them; in slot
-    order, row p = sample perm[p], when every expert has its own decoder, which needs them)."""
+    order, row p = sample perm[p], when every expert has its own decoder, which needs them),
+    stored as offsets from per-row anchors (returned as logit_anchor, anchor_shape(n, V))."""
     prm = make_params(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
@@ -318,18 +327,22 @@ def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=Non
     lg = o.get("logits")
     if lg is None and save_logits:
         lg = torch.empty(n, prm.vocab, dtype=dt, device=dev)
+    anc = o.get("logit_anchor")
+    if anc is None and lg is not None:
+        anc = torch.empty(anchor_shape(n, prm.vocab), dtype=torch.float32, device=dev)
     lab = Labels(_ptr(row_ptr), _ptr(tag))
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
     _chk(lib().hmoe_moe_forward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
-                                ctypes.byref(lab), _ptr(H1s), _ptr(H), _ptr(lg), _ptr(lse),
+                                ctypes.byref(lab), _ptr(H1s), _ptr(H), _ptr(lg), _ptr(anc), _ptr(lse),
                                 _ptr(loss), _ptr(lm), _ptr(w), wb, _stream()), "moe_forward")
-    return {"H1_sorted": H1s, "H": H, "lse": lse, "loss": loss, "loss_mean": lm, "logits": lg}
+    return {"H1_sorted": H1s, "H": H, "lse": lse, "loss": loss, "loss_mean": lm, "logits": lg,
+            "logit_anchor": anc}
 
 
 def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted, H, lse,
-                 want_dX=True, out=None, ws=None, logits=None):
+                 want_dX=True, out=None, ws=None, logits=None, logit_anchor=None):
     """Gradients of the mean loss for all expert and decoder parameters (fp32) and dX.  With
-    logits (saved by the forward) the decoder logits are not recomputed."""
+    logits and logit_anchor (saved by the forward) the decoder logits are not recomputed."""
     prm = make_params(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
@@ -348,7 +361,7 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
     _chk(lib().hmoe_moe_backward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
                                  _ptr(inv), ctypes.byref(lab), _ptr(H1_sorted), _ptr(H),
-                                 _ptr(logits), _ptr(lse),
+                                 _ptr(logits), _ptr(logit_anchor), _ptr(lse),
                                  _ptr(g["dW1"]), _ptr(g["db1"]), _ptr(g["dW2"]), _ptr(g["db2"]),
                                  _ptr(g["dD"]), _ptr(g["dbD"]), _ptr(g["dX"]), _ptr(w), wb,
                                  _stream()), "moe_backward")
@@ -357,9 +370,11 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
 
 # ------------------------------------------------------------------ inference tail
 
-def topm(logits, m: int, out=None, want_values=False):
+def topm(logits, m: int, out=None, want_values=False, anchor=None):
     """t_m (Section 4.4): the indices [n, m] of each row's m largest logits, decreasing, equal
-    values by increasing index (and their values, fp32, with want_values)."""
+    values by increasing index (and their values, fp32, with want_values).  anchor: the
+    forward's logit_anchor when logits are its stored offsets (an entry is then anchor +
+    offset in fp32)."""
     n, V = logits.shape
     dev = logits.device
     o = out or {}
@@ -367,7 +382,10 @@ def topm(logits, m: int, out=None, want_values=False):
     val = None
     if want_values:
         val = o["val"] if "val" in o else torch.empty(n, m, dtype=torch.float32, device=dev)
-    _chk(lib().hmoe_topm(_ptr(logits), _dt(logits), n, V, m, _ptr(idx), _ptr(val), _stream()), "topm")
+    if anchor is not None and tuple(anchor.shape) != anchor_shape(n, V):
+        raise HmoeError(f"anchor of shape {tuple(anchor.shape)}, {anchor_shape(n, V)} needed")
+    _chk(lib().hmoe_topm(_ptr(logits), _ptr(anchor), _dt(logits), n, V, m, _ptr(idx), _ptr(val), _stream()),
+         "topm")
     return (idx, val) if want_values else idx
 
 

@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_error_string(lib):
-    assert hmoe.version() == 1
+    assert hmoe.version() == 2
     assert isinstance(hmoe.last_error(), str)
 
 
@@ -72,21 +72,29 @@ def test_argument_errors_are_reported_before_launch(lib):
     # moe forward with vocab not a multiple of 8
     p = hmoe.MoeParams(2, 64, 128, 64, 1001, 0, 16, None, 16, None, 16, None)
     lab = hmoe.Labels(16, 16)
-    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, 16,
-                              16, 16, None, 0, None)
+    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, None,
+                              16, 16, 16, None, 0, None)
     assert rc == -3 and "vocab" in hmoe.last_error()
+    # stored logits without their anchors
+    p = hmoe.MoeParams(2, 64, 128, 64, 1000, 0, 16, None, 16, None, 16, None)
+    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, 16, None,
+                              16, 16, 16, None, 0, None)
+    assert rc == -1 and "logit_anchor" in hmoe.last_error()
+    rc = lib.hmoe_moe_backward(ctypes.byref(p), 10, 16, 16, 16, 16, ctypes.byref(lab), 16, 16, 16, None,
+                               16, 16, None, 16, None, 16, None, None, None, 0, None)
+    assert rc == -1 and "logit_anchor" in hmoe.last_error()
     # update with an unknown mode
     rc = lib.hmoe_kmeans_update(16, 0, 10, 16, 3, 16, 16, 16, 16, 16, 9, 0, None, 0, None)
     assert rc == -1 and "mode" in hmoe.last_error()
     # a decoder count that is neither 1 nor K
     p = hmoe.MoeParams(4, 64, 128, 64, 1000, 0, 16, None, 16, None, 16, None, 3)
-    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, 16,
-                              16, 16, None, 0, None)
+    rc = lib.hmoe_moe_forward(ctypes.byref(p), 10, 16, 16, 16, ctypes.byref(lab), 16, 16, None, None,
+                              16, 16, 16, None, 0, None)
     assert rc == -1 and "decoders" in hmoe.last_error()
     # top-m: m outside [1, 16], and a vocabulary that is not a multiple of 8
-    rc = lib.hmoe_topm(16, 1, 10, 64, 17, 16, None, None)
+    rc = lib.hmoe_topm(16, None, 1, 10, 64, 17, 16, None, None)
     assert rc == -1 and "m = 17" in hmoe.last_error()
-    rc = lib.hmoe_topm(16, 1, 10, 60, 5, 16, None, None)
+    rc = lib.hmoe_topm(16, None, 1, 10, 60, 5, 16, None, None)
     assert rc == -3 and "vocab" in hmoe.last_error()
     rc = lib.hmoe_topm_hits(16, 10, 0, ctypes.byref(lab), None, None, 0, 16, None)
     assert rc == -1 and "m = 0" in hmoe.last_error()

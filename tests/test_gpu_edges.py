@@ -9,7 +9,8 @@ import torch
 from oracle import oracle as O
 from paper_1704_06363_amd import hmoe
 from paper_1704_06363_amd import workloads as W
-from tests.parity import RTOL, assert_assign, assert_close, assert_scalar_close, np64, npi
+from tests.parity import (RTOL, anchored, assert_assign, assert_close, assert_grad_close, assert_scalar_close,
+                          assert_stored_logits, np64, npi, unanchored)
 
 pytestmark = pytest.mark.gpu
 
@@ -34,18 +35,19 @@ def _step_vs_oracle(X, ids, K, p, rp, tg, store, saved):
     assert_close(f["loss"], ref["loss"], rt, "loss")
     assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
     if saved:
-        assert_close(f["logits"], ref["logits"], rt, "logits")
+        assert_stored_logits(f["logits"], f["logit_anchor"], ref["logits"], store)
     tdt = torch.bfloat16 if store == "bf16" else torch.float32
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(tdt).cuda()
     H = torch.tensor(ref["H"], dtype=torch.float32).to(tdt).cuda()
     lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
-    Lg = torch.tensor(ref["logits"], dtype=torch.float32).to(tdt).cuda() if saved else None
+    Lg, An = anchored(ref["logits"], tdt) if saved else (None, None)
     g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag, H1s, H,
-                          lse, logits=Lg)
-    gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
-                        ref["lse"], store=store, logit_round=saved)
+                          lse, logits=Lg, logit_anchor=An)
+    args = (Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"], ref["lse"])
+    gr = O.moe_backward(*args, store=store)
+    gm = O.moe_backward(*args, magnitude=True)
     for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
-        assert_close(g[k], gr[k], rt, k)
+        assert_grad_close(g[k], gr[k], gm[k], store, k)
 
 
 @pytest.mark.parametrize("saved", [False, True])
@@ -186,3 +188,44 @@ def test_assign_4096_wide_features(dtype, K):
     a_ref, d1, d2 = O.assign(np64(X), np64(C))
     assert_assign(a, a_ref, d1, d2)
     assert_close(md, d1, 1e-4, "min_dist")
+
+
+@pytest.mark.parametrize("store,saved", [("bf16", True), ("bf16", False), ("f32", True)])
+def test_vocabulary_padded_to_a_multiple_of_8(store, saved):
+    """A vocabulary of 1001 tags runs as 1008: seven zero rows of D with bias -inf.  Every result
+    for the 1001 real tags is the unpadded problem's (the oracle runs V = 1001), and the padded
+    tags get exact zero gradients."""
+    n, d, h, o, V, Vp, K = 500, 64, 128, 72, 1001, 1008, 3
+    tdt = torch.bfloat16 if store == "bf16" else torch.float32
+    X = W.rectified_gaussian(n, d, seed=70, dtype=store, device="cuda")
+    ids = np.random.default_rng(71).integers(0, K, n).astype(np.int32)
+    rp, tg = W.zipf_labels(n, V, 8, seed=72)
+    p = W.moe_params(K, d, h, o, V, seed=73, dtype=store, device="cuda", bias=True)
+    pp = dict(p)
+    pp["D"] = torch.cat([p["D"], torch.zeros(Vp - V, o, dtype=tdt, device="cuda")])
+    pp["bD"] = torch.cat([p["bD"], torch.full((Vp - V,), float("-inf"), dtype=tdt, device="cuda")])
+    rt = RTOL[store]
+    a = torch.as_tensor(ids).cuda()
+    dd = hmoe.moe_dispatch(a, K, rows=X)
+    row_ptr, tag = torch.tensor(rp, device="cuda"), torch.tensor(tg, device="cuda")
+    f = hmoe.moe_forward(pp, dd["rows_sorted"], dd["offsets"], dd["perm"], row_ptr, tag, save_logits=saved)
+    g = hmoe.moe_backward(pp, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], row_ptr, tag, f["H1_sorted"],
+                          f["H"], f["lse"], logits=f["logits"], logit_anchor=f["logit_anchor"])
+    Xh = np64(X)
+    ph = {k: np64(v) for k, v in p.items()}
+    ref = O.moe_forward(Xh, ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg, store=store,
+                        want_logits=True)
+    assert_close(f["lse"], ref["lse"], rt, "lse")
+    assert_close(f["loss"], ref["loss"], rt, "loss")
+    if saved:
+        Lr = unanchored(f["logits"], f["logit_anchor"])
+        assert_stored_logits(f["logits"][:, :V], f["logit_anchor"], ref["logits"], store)
+        assert np.all(Lr[:, V:] == -np.inf)
+    args = (Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"], ref["lse"])
+    gr = O.moe_backward(*args, store=store)
+    gm = O.moe_backward(*args, magnitude=True)
+    for k in ("dW1", "db1", "dW2", "db2", "dX"):
+        assert_grad_close(g[k], gr[k], gm[k], store, k)
+    assert_grad_close(g["dD"][:V], gr["dD"], gm["dD"], store, "dD")
+    assert_grad_close(g["dbD"][:V], gr["dbD"], gm["dbD"], store, "dbD")
+    assert torch.count_nonzero(g["dD"][V:]).item() == 0 and torch.count_nonzero(g["dbD"][V:]).item() == 0

@@ -20,7 +20,8 @@ def _buffers(inp):
     disp = {"counts": z(K, dt=i32), "offsets": z(K + 1, dt=i32), "perm": z(n, dt=i32), "inv": z(n, dt=i32),
             "rows_sorted": z(n, d, dt=bf)}
     fwd = {"H1_sorted": z(n, h, dt=bf), "H": z(n, o, dt=bf), "lse": z(n, dt=f32), "loss": z(n, dt=f32),
-           "loss_mean": z(1, dt=f32), "logits": z(n, V, dt=bf)}
+           "loss_mean": z(1, dt=f32), "logits": z(n, V, dt=bf),
+           "logit_anchor": z(*hmoe.anchor_shape(n, V), dt=f32)}
     grads = {"dW1": z(K, h, d, dt=f32), "db1": z(K, h, dt=f32), "dW2": z(K, o, h, dt=f32), "db2": z(K, o, dt=f32),
              "dD": z(V, o, dt=f32), "dbD": z(V, dt=f32), "dX": z(n, d, dt=bf)}
     prm = hmoe.make_params(inp["params"])
@@ -37,7 +38,7 @@ def _step(inp, b, rp, tg):
     hmoe.moe_dispatch(b["ids"], inp["shape"]["K"], rows=inp["X"], out=dd, ws=b["ws"])
     f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], rp, tg, out=b["fwd"], ws=b["ws"])
     hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, f["H1_sorted"], f["H"],
-                      f["lse"], out=b["grads"], ws=b["ws"], logits=f["logits"])
+                      f["lse"], out=b["grads"], ws=b["ws"], logits=f["logits"], logit_anchor=f["logit_anchor"])
 
 
 def _snapshot(b):

@@ -9,7 +9,8 @@ import torch
 from oracle import oracle as O
 from paper_1704_06363_amd import hmoe
 from paper_1704_06363_amd import workloads as W
-from tests.parity import RTOL, assert_close, assert_scalar_close, np64, npi
+from tests.parity import (RTOL, anchored, assert_close, assert_grad_close, assert_scalar_close, assert_stored_logits,
+                          np64, npi, unanchored)
 
 pytestmark = pytest.mark.gpu
 
@@ -42,19 +43,20 @@ def _check(X, ids, rp, tg, p, K, store):
     assert_close(f["lse"], ref["lse"], rt, "lse")
     assert_close(f["loss"], ref["loss"], rt, "loss")
     assert_scalar_close(f["loss_mean"].item(), ref["loss_mean"], rt, "loss_mean")
-    assert_close(f["logits"], ref["logits"][perm], rt, "logits (slot order)")
+    assert_stored_logits(f["logits"], f["logit_anchor"], ref["logits"][perm], store, "stored logits (slot order)")
     # backward from the oracle's saved activations and logits (slot order)
     tdt = torch.bfloat16 if store == "bf16" else torch.float32
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32).to(tdt).cuda()
     H = torch.tensor(ref["H"], dtype=torch.float32).to(tdt).cuda()
     lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
-    Lg = torch.tensor(ref["logits"][perm], dtype=torch.float32).to(tdt).cuda()
+    Lg, An = anchored(ref["logits"][perm], tdt)
     g = hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], row_ptr, tag, H1s, H,
-                          lse, logits=Lg)
-    gr = O.moe_backward(Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"],
-                        ref["lse"], store=store, logit_round=True)
+                          lse, logits=Lg, logit_anchor=An)
+    args = (Xh, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"], ref["lse"])
+    gr = O.moe_backward(*args, store=store)
+    gm = O.moe_backward(*args, magnitude=True)
     for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
-        assert_close(g[k], gr[k], rt, k)
+        assert_grad_close(g[k], gr[k], gm[k], store, k)
     return g
 
 
@@ -98,12 +100,13 @@ def test_equal_decoders_reduce_to_the_shared_one():
         assert torch.equal(fs[k], fe[k]), k
     assert_close(fe["lse"], fs["lse"], 1e-5, "lse")
     assert_close(fe["loss"], fs["loss"], 1e-5, "loss")
-    perm = dd["perm"].long()
-    assert_close(fe["logits"], fs["logits"][perm], 1e-2, "logits")
+    perm = npi(dd["perm"])
+    assert_close(unanchored(fe["logits"], fe["logit_anchor"]),
+                 unanchored(fs["logits"], fs["logit_anchor"])[perm], 1e-2, "logits")
     gs = hmoe.moe_backward(ps, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, fs["H1_sorted"],
-                           fs["H"], fs["lse"], logits=fs["logits"])
+                           fs["H"], fs["lse"], logits=fs["logits"], logit_anchor=fs["logit_anchor"])
     ge = hmoe.moe_backward(pe, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, fe["H1_sorted"],
-                           fe["H"], fe["lse"], logits=fe["logits"])
+                           fe["H"], fe["lse"], logits=fe["logits"], logit_anchor=fe["logit_anchor"])
     for k in ("dW1", "db1", "dW2", "db2", "dX"):
         assert_close(ge[k], gs[k], rt, k)
     assert_close(ge["dD"].sum(0), gs["dD"], rt, "sum_e dD_e")
@@ -139,7 +142,7 @@ def test_independent_step_full_size():
     tg = torch.as_tensor(inp["tag"]).cuda()
     f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], rp, tg, save_logits=True)
     g = hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, f["H1_sorted"],
-                          f["H"], f["lse"], logits=f["logits"])
+                          f["H"], f["lse"], logits=f["logits"], logit_anchor=f["logit_anchor"])
     torch.cuda.synchronize()
     rt = RTOL["bf16"]
     a_np = npi(a)
@@ -158,9 +161,10 @@ def test_independent_step_full_size():
     assert_close(np64(f["H"])[rows], ref["H"], rt, "H (sampled rows)")
     assert_close(np64(f["lse"])[rows], ref["lse"], rt, "lse (sampled rows)")
     assert_close(np64(f["loss"])[rows], ref["loss"], rt, "loss (sampled rows)")
-    gr = O.moe_backward(Xs, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], srp, stg, ref["H1"], ref["H"],
-                        ref["lse"], scale=1.0 / n, store="bf16", logit_round=True)
-    assert_close(np64(g["dX"])[rows], gr["dX"], rt, "dX (sampled rows)")
+    args = (Xs, ids, ph["W1"], ph["W2"], ph["D"], ph["bD"], srp, stg, ref["H1"], ref["H"], ref["lse"])
+    gr = O.moe_backward(*args, scale=1.0 / n, store="bf16")
+    gm = O.moe_backward(*args, scale=1.0 / n, magnitude=True)
+    assert_grad_close(np64(g["dX"])[rows], gr["dX"], gm["dX"], "bf16", "dX (sampled rows)")
     dbD = np64(g["dbD"])
     assert np.all(np.abs(dbD.sum(axis=1)) <= 1e-3 * np.abs(dbD).sum(axis=1))
     db2 = np64(g["db2"])

@@ -45,7 +45,7 @@ def test_training_step_lowers_the_loss():
     args = (dd["rows_sorted"], dd["offsets"], dd["perm"], rp, tg)
     f0 = hmoe.moe_forward(p, *args, save_logits=True)
     g = hmoe.moe_backward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dd["inv"], rp, tg, f0["H1_sorted"],
-                          f0["H"], f0["lse"], logits=f0["logits"])
+                          f0["H"], f0["lse"], logits=f0["logits"], logit_anchor=f0["logit_anchor"])
     loss0 = f0["loss_mean"].item()
     for k in p:
         hmoe.sgd_step(master[k], g["d" + k], lr=0.5, weight_decay=1e-4, w_lo=p[k])

@@ -8,7 +8,8 @@ import torch
 from oracle import oracle as O
 from paper_1704_06363_amd import hmoe
 from paper_1704_06363_amd import workloads as W
-from tests.parity import RTOL, assert_assign, assert_close, assert_scalar_close, np64, npi
+from tests.parity import (RTOL, anchored, assert_assign, assert_close, assert_grad_close, assert_scalar_close,
+                          assert_stored_logits, np64, npi)
 
 pytestmark = pytest.mark.gpu
 RT = RTOL["f32"]
@@ -85,7 +86,7 @@ def test_forward_backward_match_oracle(tiny, bias, saved):
     ref = O.moe_forward(Xh, a_np, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
                         store="f32", want_logits=saved)
     if saved:
-        assert_close(f["logits"], ref["logits"], RT, "logits")
+        assert_stored_logits(f["logits"], f["logit_anchor"], ref["logits"], "f32")
     perm = npi(d["perm"])
     assert_close(f["H1_sorted"], ref["H1"][perm], RT, "H1_sorted")
     assert_close(f["H"], ref["H"], RT, "H")
@@ -96,13 +97,14 @@ def test_forward_backward_match_oracle(tiny, bias, saved):
     H1s = torch.tensor(ref["H1"][perm], dtype=torch.float32, device="cuda")
     H = torch.tensor(ref["H"], dtype=torch.float32, device="cuda")
     lse = torch.tensor(ref["lse"], dtype=torch.float32, device="cuda")
-    Lg = torch.tensor(ref["logits"], dtype=torch.float32, device="cuda") if saved else None
+    Lg, An = anchored(ref["logits"], torch.float32) if saved else (None, None)
     g = hmoe.moe_backward(p, d["rows_sorted"], d["offsets"], d["perm"], d["inv"], row_ptr, tag,
-                          H1s, H, lse, logits=Lg)
-    gr = O.moe_backward(Xh, a_np, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"],
-                        ref["H"], ref["lse"], store="f32", logit_round=saved)
+                          H1s, H, lse, logits=Lg, logit_anchor=An)
+    args = (Xh, a_np, ph["W1"], ph["W2"], ph["D"], ph["bD"], rp, tg, ref["H1"], ref["H"], ref["lse"])
+    gr = O.moe_backward(*args, store="f32")
+    gm = O.moe_backward(*args, magnitude=True)
     for k in ("dW1", "db1", "dW2", "db2", "dD", "dbD", "dX"):
-        assert_close(g[k], gr[k], RT, k)
+        assert_grad_close(g[k], gr[k], gm[k], "f32", k)
     # invariants: the softmax rows sum to one, so the decoder-bias gradient sums to zero
     assert abs(float(g["dbD"].double().sum())) < 1e-6
 

@@ -11,7 +11,7 @@ import torch
 from oracle import oracle as O
 from paper_1704_06363_amd import hmoe
 from paper_1704_06363_amd import workloads as W
-from tests.parity import np64, npi
+from tests.parity import anchor_of_columns, np64, npi
 
 pytestmark = pytest.mark.gpu
 
@@ -35,6 +35,25 @@ def test_topm_bit_exact(dtype, n, V, m, ties):
     ref = O.topm(np64(L), m)
     assert np.array_equal(npi(idx), ref)
     np.testing.assert_array_equal(np64(val), np.take_along_axis(np64(L), ref.astype(np.int64), axis=1))
+
+
+@pytest.mark.parametrize("dtype,n,V,m", [("bf16", 500, 1000, 10), ("bf16", 33, 50000, 16), ("f32", 200, 520, 5),
+                                          ("bf16", 70, 264, 3)])
+def test_topm_anchored_bit_exact(dtype, n, V, m):
+    """Logits stored as offsets from per-row anchors (the forward's layout): an entry is anchor +
+    offset formed in fp32, on both sides.  Anchors differ between the 64-column blocks of a row,
+    and the offsets are drawn so that entries of different blocks tie after the addition."""
+    g = torch.Generator(device="cpu").manual_seed(n + V)
+    nt = (V + 255) // 256
+    anc = (torch.randint(-3, 4, (nt, n, 4), generator=g).float() * 0.5)
+    off = torch.randint(-12, 1, (n, V), generator=g).float() * 0.25  # exact in bf16; ties across blocks
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    L, A = off.to(tdt).cuda(), anc.cuda()
+    idx, val = hmoe.topm(L, m, want_values=True, anchor=A)
+    full = (anchor_of_columns(A, V) + np64(L).astype(np.float32)).astype(np.float32)
+    ref = O.topm(full, m)
+    assert np.array_equal(npi(idx), ref)
+    np.testing.assert_array_equal(np64(val), np.take_along_axis(full, ref.astype(np.int64), axis=1))
 
 
 def test_hits_exact():
@@ -73,7 +92,7 @@ def test_inference_path_against_the_oracle():
         rp, tg = inp["row_ptr"], inp["tag"]
         dev = lambda a: torch.as_tensor(a).cuda()  # noqa: E731
         f = hmoe.moe_forward(p, dd["rows_sorted"], dd["offsets"], dd["perm"], dev(rp), dev(tg), save_logits=True)
-        idx = npi(hmoe.topm(f["logits"], m))
+        idx = npi(hmoe.topm(f["logits"], m, anchor=f["logit_anchor"]))
         ph = {k: (np64(v) if v is not None else None) for k, v in p.items()}
         ref = O.moe_forward(np64(inp["X"]), ids, ph["W1"], ph["b1"], ph["W2"], ph["b2"], ph["D"], ph["bD"], rp, tg,
                             store=store, want_logits=True)
