@@ -9,7 +9,8 @@
  *
  * Conventions for every entry point:
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns all memory.
- *     The library allocates nothing and keeps no state between calls.
+ *     The library allocates nothing and keeps no state between calls (the one exception is
+ *     hmoe_moe_dispatch_noalloc's scratch array, below).
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Every call is
  *     asynchronous on that stream and performs no host synchronisation.
  *   - Scratch memory comes from the caller through (ws, ws_bytes); the matching *_workspace()
@@ -125,6 +126,22 @@ int hmoe_moe_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* coun
                       int32_t* offsets, int32_t* perm, int32_t* inv, const void* rows,
                       void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* ws,
                       size_t ws_bytes, void* stream);
+
+/* Allocation-free variant of hmoe_moe_dispatch, for callers that cannot allocate device memory
+ * or pass a workspace: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The same stable counting sort and row gather, with the same arguments minus the
+ * workspace; its scratch (the per-block bucket counts, (K + 1) * ceil(n / 1024) int32) lives in
+ * a device array of HMOE_DISPATCH_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends (looked up on the first call on that GPU).  The call allocates
+ * nothing.  Every call on a GPU shares that GPU's array, which keeps the last call's contents;
+ * nothing in it needs clearing (each call writes what it reads), but calls that overlap on one
+ * GPU (on other streams or threads) race on it -- calls on one stream are ordered.  A size whose
+ * scratch exceeds the array (e.g. K = 4096 with more than 2^20 rows) returns HMOE_EWORKSPACE
+ * before anything is launched. */
+#define HMOE_DISPATCH_SCRATCH_BYTES (16u << 20)
+int hmoe_moe_dispatch_noalloc(const int32_t* expert, int64_t n, int32_t K, int32_t* counts,
+                              int32_t* offsets, int32_t* perm, int32_t* inv, const void* rows,
+                              void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* stream);
 
 /* Row gather out[r] = in[index[r]] for r < n (rows of w elements of dtype dt; in has n rows
  * too).  With index = inv it combines expert-ordered rows back to sample order; with perm it

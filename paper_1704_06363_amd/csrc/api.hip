@@ -2,6 +2,7 @@
 // checks and dispatch to the launchers.  Host code only.
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -96,6 +97,65 @@ static int check_n(int64_t n) {
 static int check_ws(size_t need, size_t have, const void* ws) {
   if (need > 0 && (have < need || ws == nullptr))
     return fail(HMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", have, need);
+  return HMOE_OK;
+}
+
+// ------------------------------------------------------------------ allocation-free dispatch
+// The scratch of hmoe_moe_dispatch_noalloc: one array per GPU the library runs on, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not the array: its
+// device address is looked up once per device (with that device current) and only that address
+// is handed to kernels.
+constexpr size_t kDispatchScratch = HMOE_DISPATCH_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kDispatchScratch];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_at[kMaxDevices];  // device address of `scratch` per device, NULL until looked up
+}  // namespace
+
+static int dispatch_scratch(void** at) {
+  int dev = 0;
+  HMOE_TRY(hip_check(hipGetDevice(&dev), "hipGetDevice"));
+  if (dev < 0 || dev >= kMaxDevices) return fail(HMOE_EHIP, "device %d beyond the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_at[dev]) {
+    void* p = nullptr;
+    HMOE_TRY(hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+    if (!p) return fail(HMOE_EHIP, "hipGetSymbolAddress(scratch) gave NULL");
+    g_scratch_at[dev] = p;
+  }
+  *at = g_scratch_at[dev];
+  return HMOE_OK;
+}
+
+// Argument checks shared by the two dispatch entry points.
+static int check_dispatch(const int32_t* expert, int64_t n, int32_t K, const int32_t* counts, const int32_t* offsets,
+                          const int32_t* perm, const int32_t* inv, const void* rows, const void* rows_sorted,
+                          hmoe_dtype_t dt, int32_t w) {
+  HMOE_TRY(check_n(n));
+  HMOE_TRY(check_k(K));
+  HMOE_TRY(check_ptr("counts", counts, false));
+  HMOE_TRY(check_ptr("offsets", offsets, false));
+  if (n > 0) {
+    HMOE_TRY(check_ptr("expert", expert, false));
+    HMOE_TRY(check_ptr("perm", perm, false));
+    HMOE_TRY(check_ptr("inv", inv, false));
+  }
+  if (rows && n > 0) {
+    HMOE_TRY(check_dtype(dt));
+    HMOE_TRY(check_width("w", w));
+    HMOE_TRY(check_ptr("rows", rows));
+    HMOE_TRY(check_ptr("rows_sorted", rows_sorted));
+  }
+  return HMOE_OK;
+}
+
+static int run_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* counts, int32_t* offsets,
+                        int32_t* perm, int32_t* inv, const void* rows, void* rows_sorted, hmoe_dtype_t dt, int32_t w,
+                        Workspace& wsp, hipStream_t st) {
+  HMOE_TRY(launch_dispatch(expert, n, K, counts, offsets, perm, inv, wsp, st));
+  if (rows && n > 0) HMOE_TRY(launch_permute(rows, rows_sorted, perm, n, w, dt, st));
   return HMOE_OK;
 }
 
@@ -239,27 +299,27 @@ int hmoe_moe_dispatch(const int32_t* expert, int64_t n, int32_t K, int32_t* coun
                       int32_t* inv, const void* rows, void* rows_sorted, hmoe_dtype_t dt, int32_t w, void* ws,
                       size_t ws_bytes, void* stream) {
   clear_error();
-  HMOE_TRY(check_n(n));
-  HMOE_TRY(check_k(K));
-  HMOE_TRY(check_ptr("counts", counts, false));
-  HMOE_TRY(check_ptr("offsets", offsets, false));
-  if (n > 0) {
-    HMOE_TRY(check_ptr("expert", expert, false));
-    HMOE_TRY(check_ptr("perm", perm, false));
-    HMOE_TRY(check_ptr("inv", inv, false));
-  }
-  if (rows && n > 0) {
-    HMOE_TRY(check_dtype(dt));
-    HMOE_TRY(check_width("w", w));
-    HMOE_TRY(check_ptr("rows", rows));
-    HMOE_TRY(check_ptr("rows_sorted", rows_sorted));
-  }
+  HMOE_TRY(check_dispatch(expert, n, K, counts, offsets, perm, inv, rows, rows_sorted, dt, w));
   HMOE_TRY(check_ws(dispatch_ws(n, K), ws_bytes, ws));
   Workspace wsp(ws, ws_bytes);
-  hipStream_t st = (hipStream_t)stream;
-  HMOE_TRY(launch_dispatch(expert, n, K, counts, offsets, perm, inv, wsp, st));
-  if (rows && n > 0) HMOE_TRY(launch_permute(rows, rows_sorted, perm, n, w, dt, st));
-  return HMOE_OK;
+  return run_dispatch(expert, n, K, counts, offsets, perm, inv, rows, rows_sorted, dt, w, wsp, (hipStream_t)stream);
+}
+
+int hmoe_moe_dispatch_noalloc(const int32_t* expert, int64_t n, int32_t K, int32_t* counts, int32_t* offsets,
+                              int32_t* perm, int32_t* inv, const void* rows, void* rows_sorted, hmoe_dtype_t dt,
+                              int32_t w, void* stream) {
+  clear_error();
+  HMOE_TRY(check_dispatch(expert, n, K, counts, offsets, perm, inv, rows, rows_sorted, dt, w));
+  const size_t need = dispatch_ws(n, K);
+  if (need > kDispatchScratch)
+    return fail(HMOE_EWORKSPACE,
+                "the dispatch of n = %lld rows into K = %d experts needs %zu bytes of scratch; the allocation-free "
+                "dispatch holds %zu (use hmoe_moe_dispatch with a workspace)",
+                (long long)n, K, need, kDispatchScratch);
+  void* at = nullptr;
+  HMOE_TRY(dispatch_scratch(&at));
+  Workspace wsp(at, kDispatchScratch);
+  return run_dispatch(expert, n, K, counts, offsets, perm, inv, rows, rows_sorted, dt, w, wsp, (hipStream_t)stream);
 }
 
 int hmoe_permute_rows(const void* in, void* out, const int32_t* index, int64_t n, int32_t w, hmoe_dtype_t dt,

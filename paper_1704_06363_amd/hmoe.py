@@ -24,7 +24,7 @@ SYMBOLS = (
     "hmoe_kmeans_assign_workspace", "hmoe_kmeans_assign",
     "hmoe_kmeans_fit_workspace", "hmoe_kmeans_fit",
     "hmoe_kmeans_update_workspace", "hmoe_kmeans_update",
-    "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_permute_rows",
+    "hmoe_moe_dispatch_workspace", "hmoe_moe_dispatch", "hmoe_moe_dispatch_noalloc", "hmoe_permute_rows",
     "hmoe_moe_workspace", "hmoe_moe_forward", "hmoe_moe_backward",
     "hmoe_pca_workspace", "hmoe_pca_fit", "hmoe_pca_project",
     "hmoe_sgd_step", "hmoe_topm", "hmoe_topm_hits",
@@ -79,6 +79,7 @@ def lib():
                                          _I32, _I32, _P, _SZ, _P]
         L.hmoe_moe_dispatch.argtypes = [_P, _I64, _I32, _P, _P, _P, _P, _P, _P, _c.c_int, _I32,
                                         _P, _SZ, _P]
+        L.hmoe_moe_dispatch_noalloc.argtypes = [_P, _I64, _I32, _P, _P, _P, _P, _P, _P, _c.c_int, _I32, _P]
         L.hmoe_permute_rows.argtypes = [_P, _P, _P, _I64, _I32, _c.c_int, _P]
         L.hmoe_moe_forward.argtypes = [_c.POINTER(MoeParams), _I64, _P, _P, _P,
                                        _c.POINTER(Labels), _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
@@ -97,7 +98,7 @@ def lib():
         L.hmoe_timer_report.argtypes = [_c.c_char_p, _SZ]
         L.hmoe_timer_report.restype = _I64
         for name in ("hmoe_kmeans_assign", "hmoe_kmeans_fit", "hmoe_kmeans_update",
-                     "hmoe_moe_dispatch", "hmoe_permute_rows", "hmoe_moe_forward",
+                     "hmoe_moe_dispatch", "hmoe_moe_dispatch_noalloc", "hmoe_permute_rows", "hmoe_moe_forward",
                      "hmoe_moe_backward", "hmoe_pca_fit", "hmoe_pca_project", "hmoe_sgd_step",
                      "hmoe_topm", "hmoe_topm_hits"):
             getattr(L, name).restype = _c.c_int
@@ -269,6 +270,32 @@ def moe_dispatch(expert, K, rows=None, out=None, ws=None):
                                  _stream()), "moe_dispatch")
     return {"counts": counts, "offsets": offsets, "perm": perm, "inv": inv,
             "rows_sorted": rows_sorted}
+
+
+DISPATCH_SCRATCH_BYTES = 16 << 20  # include/hmoe.h: HMOE_DISPATCH_SCRATCH_BYTES
+
+
+def moe_dispatch_noalloc(expert, K, rows=None, out=None):
+    """moe_dispatch without a workspace: the library's own device scratch array (for callers
+    that cannot allocate; calls that overlap on one GPU race on it).  Outputs are allocated here
+    unless passed in `out`."""
+    n = expert.shape[0]
+    dev = expert.device
+    o = out or {}
+    counts = _out(o, "counts", lambda: torch.empty(K, dtype=torch.int32, device=dev))
+    offsets = _out(o, "offsets", lambda: torch.empty(K + 1, dtype=torch.int32, device=dev))
+    perm = _out(o, "perm", lambda: torch.empty(n, dtype=torch.int32, device=dev))
+    inv = _out(o, "inv", lambda: torch.empty(n, dtype=torch.int32, device=dev))
+    rows_sorted = None
+    w = 0
+    dt = F32
+    if rows is not None:
+        rows_sorted = _out(o, "rows_sorted", lambda: torch.empty_like(rows))
+        w = rows.shape[1]
+        dt = _dt(rows)
+    _chk(lib().hmoe_moe_dispatch_noalloc(_ptr(expert), n, K, _ptr(counts), _ptr(offsets), _ptr(perm), _ptr(inv),
+                                         _ptr(rows), _ptr(rows_sorted), dt, w, _stream()), "moe_dispatch_noalloc")
+    return {"counts": counts, "offsets": offsets, "perm": perm, "inv": inv, "rows_sorted": rows_sorted}
 
 
 def permute_rows(inp, index, out=None):

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 22
+    assert len(names) == 23
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(hmoe.SYMBOLS)
@@ -69,6 +69,12 @@ def test_argument_errors_are_reported_before_launch(lib):
     # dispatch with a NULL perm
     rc = lib.hmoe_moe_dispatch(16, 10, 3, 16, 16, None, 16, None, None, 0, 0, None, 0, None)
     assert rc == -1 and "perm" in hmoe.last_error()
+    # the allocation-free dispatch: the same checks, and sizes beyond its scratch array refused
+    # before the device is touched (K = 4096 over 2^21 rows needs 32 MiB of bucket counts)
+    rc = lib.hmoe_moe_dispatch_noalloc(16, 10, 3, 16, 16, None, 16, None, None, 0, 0, None)
+    assert rc == -1 and "perm" in hmoe.last_error()
+    rc = lib.hmoe_moe_dispatch_noalloc(16, 1 << 21, 4096, 16, 16, 16, 16, None, None, 0, 0, None)
+    assert rc == -4 and "scratch" in hmoe.last_error()
     # moe forward with vocab not a multiple of 8
     p = hmoe.MoeParams(2, 64, 128, 64, 1001, 0, 16, None, 16, None, 16, None)
     lab = hmoe.Labels(16, 16)
