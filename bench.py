@@ -125,6 +125,38 @@ def gemm_flops(s):
     }
 
 
+def step_bytes(s, nnz):
+    """Algorithmic HBM bytes per step of each labelled kernel of one routed step (all its
+    launches): every operand read once and every output written once, in the stored dtypes
+    (bf16 data, fp32 gradients, int32 indices).  Partial sums a kernel keeps for a later one
+    (the split-K partials) count for the kernel that writes and the one that reads them."""
+    n, d, h, o, V, K = s["n"], s["d"], s["h"], s["o"], s["V"], s["K"]
+    b, f, i = 2, 4, 4
+    ntv = -(-V // 256)
+    nb = -(-n // 1024)
+    return {
+        "assign": n * d * b + K * d * b + n * (i + f),
+        "dispatch hist": n * i + nb * (K + 1) * i,
+        "dispatch colscan": 2 * nb * (K + 1) * i + K * i,
+        "dispatch scatter": n * i + nb * (K + 1) * i + 2 * n * i,
+        "permute rows": 2 * n * d * b + n * i,
+        "expert layer 1": n * d * b + K * h * d * b + n * h * b,
+        "expert layer 2": n * h * b + K * o * h * b + n * o * b + n * i,
+        # H and D read, logits and their anchors written, the per-tile (max, sum) partials
+        "decoder forward": n * o * b + V * o * b + n * V * b + n * ntv * 16 + 2 * n * ntv * f,
+        "decoder loss": 2 * n * ntv * f + n * o * b + V * o * b + (n + 1 + nnz) * i + 2 * n * f,
+        "decoder grad": n * V * b + n * ntv * 16 + n * f + (n + 1 + nnz) * i + n * V * b + (-(-n // 256)) * V * f,
+        "decoder bias grad": (-(-n // 256)) * V * f + V * f,
+        "decoder dH": n * V * b + V * o * b + n * o * b + n * i,
+        "decoder dD": n * V * b + n * o * b + V * o * f,
+        "segsum partial": n * (o + h) * b,
+        "expert dW2": n * o * b + n * h * b + K * o * h * f,
+        "expert dH1": n * o * b + K * o * h * b + 2 * n * h * b,
+        "expert dW1": n * h * b + n * d * b + K * h * d * f,
+        "expert dX": n * h * b + K * h * d * b + n * d * b + n * i,
+    }
+
+
 def step_flops(s, assign=True):
     f = gemm_flops(s)
     tot = sum(v for k, v in f.items() if k != "assign")
@@ -212,16 +244,43 @@ def time_steps(fn, steps, warmup, timer=True):
     return ms, rep
 
 
-def kernel_table(rep, flops, peak_tflops, steps):
+def kernel_table(rep, flops, peak_tflops, steps, nbytes=None):
+    """Per kernel label: launches and average time; against the MFMA roof (FLOPs per launch in
+    `flops`), against the HBM roof (bytes per step in `nbytes`), and where both are known, the
+    roof that bounds it -- the larger of FLOPs / MFMA peak and bytes / HBM peak -- with the
+    fraction of that roof reached."""
     out = {}
     for label, (cnt, ms) in rep.items():
         e = {"launches_per_step": cnt / steps, "avg_ms": ms / cnt}
+        t_step = ms / steps * 1e-3  # seconds per step in this label
+        t_mfma = t_hbm = None
         if label in flops:
             tf = flops[label] / (ms / cnt * 1e-3) / 1e12
             e["tflops"] = round(tf, 2)
-            e["frac_peak"] = round(tf / peak_tflops, 4)
+            e["frac_mfma_peak"] = round(tf / peak_tflops, 4)
+            t_mfma = flops[label] * (cnt / steps) / (peak_tflops * 1e12)
+        if nbytes and label in nbytes:
+            gbs = nbytes[label] / t_step / 1e9
+            e["gb_per_s"] = round(gbs, 1)
+            e["frac_hbm_peak"] = round(gbs / PEAK_HBM_GBS, 4)
+            t_hbm = nbytes[label] / (PEAK_HBM_GBS * 1e9)
+        if t_mfma is not None or t_hbm is not None:
+            roof = max(x for x in (t_mfma, t_hbm) if x is not None)
+            e["bound"] = "mfma" if (t_mfma or 0.0) >= (t_hbm or 0.0) else "hbm"
+            e["frac_roof"] = round(roof / t_step, 4)
         out[label] = e
     return out
+
+
+def hbm_summary(rep, nbytes, steps, labels):
+    """Achieved HBM bandwidth of a group of kernels (bytes per step over their summed time)."""
+    ms = sum(rep[k][1] for k in labels if k in rep) / steps
+    by = sum(nbytes[k] for k in labels if k in rep)
+    if ms <= 0:
+        return None
+    gbs = by / (ms * 1e-3) / 1e9
+    return {"kernels": [k for k in labels if k in rep], "ms": round(ms, 4), "bytes": int(by),
+            "gb_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def dominant(rep, flops):
@@ -376,13 +435,16 @@ def leg_skewed(steps, warmup):
     ms, rep = time_steps(st.run, steps, warmup)
     s = inp["shape"]
     fl = gemm_flops(s)
+    nby = step_bytes(s, int(inp["row_ptr"][-1]))
     tot = step_flops(s, assign=False)
     out = {"workload": "skewed routed step: n=32768 bf16, d=2048, K=128 Zipf(1.3) buckets, "
                        "MLP 2048-2048-1024, V=100000, fwd+bwd",
            "samples_per_s": round(s["n"] / (ms * 1e-3), 1), "ms_per_step": round(ms, 3),
            "tflops": round(tot / (ms * 1e-3) / 1e12, 1),
            "frac_bf16_peak": round(tot / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-           "kernels": kernel_table(rep, fl, PEAK_BF16_TFLOPS, steps)}
+           "kernels": kernel_table(rep, fl, PEAK_BF16_TFLOPS, steps, nby),
+           "hbm": {"dispatch_row_gather": hbm_summary(rep, nby, steps, ["permute rows"]),
+                   "reduction_bias_grads": hbm_summary(rep, nby, steps, ["segsum partial"])}}
     del st, inp
     torch.cuda.empty_cache()
     return out
@@ -565,7 +627,9 @@ def main():
     log("balanced step: timing")
     ms, rep = time_steps(st.run, args.steps, args.warmup)
     fl = gemm_flops(s)
-    kern = kernel_table(rep, fl, PEAK_BF16_TFLOPS, args.steps)
+    nnz = int(inp["row_ptr"][-1])
+    nby = step_bytes(s, nnz)
+    kern = kernel_table(rep, fl, PEAK_BF16_TFLOPS, args.steps, nby)
     dom = dominant(rep, fl)
     cnt, tot_ms = rep[dom]
     avg = tot_ms / cnt
@@ -593,6 +657,14 @@ def main():
                      "traffic": tr["bytes_per_launch"] if tr else None,
                      "avg_ms": round(avg, 4), "flop_per_launch": fl[dom]},
         "kernels": kern,
+        # dispatch = the counting sort and the row gather into expert order (the combine is the
+        # second expert layer's epilogue, which writes rows back to sample order); reduction =
+        # the experts' bias-gradient segmented sums (the centre update's is in legs.gater_fit)
+        "hbm": {"dispatch": hbm_summary(rep, nby, args.steps, ["dispatch hist", "dispatch colscan",
+                                                               "dispatch scatter", "permute rows"]),
+                "dispatch_row_gather": hbm_summary(rep, nby, args.steps, ["permute rows"]),
+                "reduction_bias_grads": hbm_summary(rep, nby, args.steps, ["segsum partial"]),
+                "decoder_grad_elementwise": hbm_summary(rep, nby, args.steps, ["decoder grad"])},
     }
     loss = float(st.fwd["loss_mean"].item())
     res["loss_mean"] = round(loss, 5)

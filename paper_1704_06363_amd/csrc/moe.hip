@@ -85,13 +85,15 @@ __device__ __forceinline__ void add_bias(floatx4 (&acc)[C::MI][C::NJ], const flo
 }
 
 // Per-wave row statistics of a logits tile: m = max over the wave's valid columns of the row,
-// s = sum exp(logit - m), into rm / rs [WAVES_N][BM].  The valid accumulators become the
-// offsets logit - m in place (m is the row's anchor for this wave's 64 columns: what a stored
-// logit is relative to), and s is the sum of exp2(offset log2(e)).
+// s = sum exp(logit - m) (as exp2 of logit log2(e) - m log2(e)), into rm / rs [WAVES_N][BM].
+// m is also the row's anchor for this wave's 64 columns, the value a stored logit is relative
+// to; with mxo given it is kept there too, mxo[4 i + r] for accumulator row (i, r) (TRANS: one
+// row per i, at mxo[4 i]).  The accumulators are only read: subtracting in place measured
+// 12 -> 424 bytes of spill per lane in the persistent forward.
 // FULL: every column of the tile is valid (no column guards).
 template <class C, bool FULL>
-__device__ __forceinline__ void dec_row_stats(const TileCoord& tc, floatx4 (&acc)[C::MI][C::NJ],
-                                              lds<float>* rm, lds<float>* rs) {
+__device__ __forceinline__ void dec_row_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
+                                              lds<float>* rm, lds<float>* rs, float* mxo = nullptr) {
   static_assert(C::WN == kAnchorCols, "one anchor per wave and row");
   using F = Frag<C>;
   const F f;
@@ -108,15 +110,14 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, floatx4 (&acc
           if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
       mx = fmaxf(mx, shfl_xor(mx, 16));
       mx = fmaxf(mx, shfl_xor(mx, 32));
+      if (mxo) mxo[4 * i] = mx;
+      const float mb = mx * kLog2e;
       float s = 0.f;
 #pragma unroll
       for (int j = 0; j < C::NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (FULL || f.col(j, r) < tc.n_cols) {
-            acc[i][j][r] -= mx;
-            s += __builtin_amdgcn_exp2f(acc[i][j][r] * kLog2e);
-          }
+          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
       s += shfl_xor(s, 16);
       s += shfl_xor(s, 32);
       if (f.lg == 0) {
@@ -136,13 +137,12 @@ __device__ __forceinline__ void dec_row_stats(const TileCoord& tc, floatx4 (&acc
           if (FULL || f.col(j, r) < tc.n_cols) mx = fmaxf(mx, acc[i][j][r]);
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) mx = fmaxf(mx, shfl_xor(mx, m));
+        if (mxo) mxo[4 * i + r] = mx;
+        const float mb = mx * kLog2e;
         float s = 0.f;
 #pragma unroll
         for (int j = 0; j < C::NJ; ++j)
-          if (FULL || f.col(j, r) < tc.n_cols) {
-            acc[i][j][r] -= mx;
-            s += __builtin_amdgcn_exp2f(acc[i][j][r] * kLog2e);
-          }
+          if (FULL || f.col(j, r) < tc.n_cols) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -mb));
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) s += shfl_xor(s, m);
         if (f.lr == 0) {
@@ -188,15 +188,25 @@ __device__ __forceinline__ void dec_stats_merge(const TileCoord& tc, lds<float>*
 }
 
 template <class C>
-__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, floatx4 (&acc)[C::MI][C::NJ],
+__device__ __forceinline__ void dec_tile_stats(const TileCoord& tc, const floatx4 (&acc)[C::MI][C::NJ],
                                                lds<float>* rm, lds<float>* rs, int64_t n, float* __restrict__ pm,
-                                               float* __restrict__ ps, float* __restrict__ anc) {
+                                               float* __restrict__ ps, float* __restrict__ anc, float* mxo) {
   if (tc.n_cols == C::BN)
-    dec_row_stats<C, true>(tc, acc, rm, rs);
+    dec_row_stats<C, true>(tc, acc, rm, rs, mxo);
   else
-    dec_row_stats<C, false>(tc, acc, rm, rs);
+    dec_row_stats<C, false>(tc, acc, rm, rs, mxo);
   dec_stats_merge<C>(tc, rm, rs, n, pm, ps, anc);
 }
+
+// The stored logit of accumulator element (i, j, r): its offset from the wave's row maximum
+// (mx as kept by dec_row_stats; held by value, so that it stays in registers).
+template <class C>
+struct Anchored {
+  float mx[4 * C::MI];
+  __device__ __forceinline__ float operator()(int i, int, int r, float v) const {
+    return v - mx[C::TRANS ? 4 * i : 4 * i + r];
+  }
+};
 
 template <class C>
 __device__ __forceinline__ void dec_tile_bias(const TileCoord& tc, const typename C::type* __restrict__ bD,
@@ -230,10 +240,11 @@ __global__ void __launch_bounds__(C::THREADS)
   dec_tile_bias<C>(tc, bD, bias);
   add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr);
+  Anchored<C> an;
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr, an.mx);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
-    store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, L, V, an, RowId{tc.m0}, NoVec{});
   }
 }
 
@@ -259,10 +270,11 @@ __global__ void __launch_bounds__(C::THREADS)
   dec_tile_bias<C>(tc, bD ? bD + (int64_t)tc.group * V : nullptr, bias);
   add_bias<C>(acc, bias);
   lds<float>* rm = reinterpret_cast<lds<float>*>(smem);  // reuses the operand buffers
-  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr);
+  Anchored<C> an;
+  dec_tile_stats<C>(tc, acc, rm, rm + C::WAVES_N * C::BM, n, pm, ps, L ? anc : nullptr, an.mx);
   if (L) {
     if constexpr (!F::T) __syncthreads();  // the LDS-staged store reuses rm / rs
-    store_out<C, T>(tc, acc, smem, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
+    store_out<C, T>(tc, acc, smem, L, V, an, RowId{tc.m0}, NoVec{});
   }
 }
 
@@ -302,6 +314,7 @@ __global__ void __launch_bounds__(C::THREADS)
   lds<float>* rm0 = reinterpret_cast<lds<float>*>(smem + C::LDS);
   constexpr int SB = 2 * C::WAVES_N * C::BM;  // one statistics buffer (floats)
   using F = Frag<C>;
+  const F f0;
   const int64_t tiles = cdiv(n, C::BM) * cdiv(V, C::BN);
   int64_t t = blockIdx.x;
   if (t >= tiles) return;
@@ -350,8 +363,13 @@ __global__ void __launch_bounds__(C::THREADS)
     // nothing may move between the primed loads and the stores: the next waits count them
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    if (L)
-      store_direct<C, bf16>(tc, acc, L, V, [](int, int, int, float v) { return v; }, RowId{tc.m0}, NoVec{});
+    if (L) {
+      // the anchor of each row: this wave's row maximum, read back from the partials it has
+      // just written (a wave's LDS accesses complete in order; the registers are full here)
+      const lds<float>* rmw = rm + f0.wn * C::BM;
+      store_direct<C, bf16>(tc, acc, L, V, [&](int i, int, int, float v) { return v - rmw[f0.row(i, 0)]; },
+                            RowId{tc.m0}, NoVec{});
+    }
     __builtin_amdgcn_sched_barrier(0);
     // the previous tile's partials were written before this tile's K loop, whose barriers
     // order them; its buffer is rewritten only after the next K loop
