@@ -600,6 +600,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--large-chunks", type=int, default=16)
+    ap.add_argument("--skip-step", action="store_true",
+                    help="run only the legs, not the balanced step (for profiling a leg on its own; the JSON line "
+                         "then carries no step figures)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -620,6 +623,10 @@ def main():
         log(f"calibration copy: {args.calib_copy_mib} MiB")
         calib_copy(args.calib_copy_mib)
 
+    if args.skip_step:
+        legs = run_legs(args)
+        print(json.dumps({"metric": METRIC, "legs": legs}), flush=True)
+        return
     log("balanced step: generating inputs")
     inp = W.balanced_inputs(device="cuda", seed=0)
     s = inp["shape"]
@@ -676,23 +683,27 @@ def main():
     del inp
     torch.cuda.empty_cache()
     if not args.no_legs:
-        legs = {}
-        table = [("gater_fit", "gater fit", lambda: leg_gater_fit(steps=2)),
-                 ("gater_pca", "gater features with PCA", lambda: leg_gater_pca(steps=2)),
-                 ("skewed", "skewed routing", lambda: leg_skewed(steps=max(2, args.steps // 2), warmup=1)),
-                 ("independent", "independent decoders",
-                  lambda: leg_independent(steps=max(2, args.steps // 2), warmup=1)),
-                 ("inference", "inference tail", lambda: leg_inference(steps=max(2, args.steps // 2), warmup=1)),
-                 ("sgd_update", "sgd update", lambda: leg_sgd_update(steps=max(2, args.steps // 2), warmup=1)),
-                 ("large_assign", "large assign", lambda: leg_large_assign(args.large_chunks))]
-        chosen = set(x for x in args.legs.split(",") if x)
-        for key, what, run in table:
-            if chosen and key not in chosen:
-                continue
-            log(f"leg: {what}")
-            legs[key] = run()
-        res["legs"] = legs
+        res["legs"] = run_legs(args)
     print(json.dumps(res), flush=True)
+
+
+def run_legs(args):
+    legs = {}
+    table = [("gater_fit", "gater fit", lambda: leg_gater_fit(steps=2)),
+             ("gater_pca", "gater features with PCA", lambda: leg_gater_pca(steps=2)),
+             ("skewed", "skewed routing", lambda: leg_skewed(steps=max(2, args.steps // 2), warmup=1)),
+             ("independent", "independent decoders",
+              lambda: leg_independent(steps=max(2, args.steps // 2), warmup=1)),
+             ("inference", "inference tail", lambda: leg_inference(steps=max(2, args.steps // 2), warmup=1)),
+             ("sgd_update", "sgd update", lambda: leg_sgd_update(steps=max(2, args.steps // 2), warmup=1)),
+             ("large_assign", "large assign", lambda: leg_large_assign(args.large_chunks))]
+    chosen = set(x for x in args.legs.split(",") if x)
+    for key, what, run in table:
+        if chosen and key not in chosen:
+            continue
+        log(f"leg: {what}")
+        legs[key] = run()
+    return legs
 
 
 if __name__ == "__main__":
