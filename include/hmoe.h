@@ -53,7 +53,8 @@ enum {
   HMOE_EDTYPE = -2,     /* unknown dtype */
   HMOE_ESHAPE = -3,     /* width not a multiple of 8, misaligned pointer */
   HMOE_EWORKSPACE = -4, /* ws_bytes smaller than the *_workspace() answer */
-  HMOE_EHIP = -5        /* a HIP launch or runtime call failed */
+  HMOE_EHIP = -5,       /* a HIP launch or runtime call failed */
+  HMOE_ENUMERIC = -6    /* a host-side factorisation did not converge (hmoe_pca_fit) */
 };
 
 typedef enum { HMOE_F32 = 0, HMOE_BF16 = 1 } hmoe_dtype_t;

@@ -313,16 +313,10 @@ struct CfgD {
   static_assert(sizeof(T) == 2 || sizeof(T) == 4, "bf16 or fp32 operands");
 };
 
-#ifndef HMOE_PINGPONG
-#define HMOE_PINGPONG 1
-#endif
-
-#ifndef HMOE_DMA_STAGES
-#define HMOE_DMA_STAGES 4
-#endif
-
-typedef CfgD<bf16, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDma;
-typedef CfgD<float, 256, 256, 128, 64, HMOE_DMA_STAGES> CfgDmaF32;        // fp32, K-contiguous operands
+// 256 x 256 tiles, eight waves of 128 x 64, a 4-stage ring (128 KB): 3 and 5 stages measured
+// slower for the decoder and expert GEMMs.
+typedef CfgD<bf16, 256, 256, 128, 64, 4> CfgDma;
+typedef CfgD<float, 256, 256, 128, 64, 4> CfgDmaF32;        // fp32, K-contiguous operands
 // fp32 with at most 64 columns (the gater's assignment, K <= 64): 128 x 64 tiles of four waves
 // and a 3-stage ring (36 KB), four workgroups per CU -- measured against 256 x 64 (4 stages:
 // 11% slower; 3 stages: 15%), 128 x 64 with 2 or 4 stages (10%, 8%) and 64 x 64 (17%)
@@ -598,7 +592,7 @@ struct DmaTile {
     // Ping-pong schedule for contractions with at least one K-contiguous operand.  With both
     // operands K-strided (two ds_read_b64_tr_b16 per fragment) the read phase outlasts the
     // MFMA phase and the single-group schedule below measured faster (dD, weight gradients).
-    constexpr bool PP = HMOE_PINGPONG && (A_KC || B_KC);
+    constexpr bool PP = A_KC || B_KC;
     auto wait_own = [&](int k) {  // this wave's loads of stage k
       const int ahead = nfull - 1 - k;
       const int pend = ahead < C::NS - 2 ? ahead : C::NS - 2;

@@ -76,7 +76,12 @@ inline bool chol_inverse(const std::vector<double>& S, int r, std::vector<double
 // (bulge chasing with Givens rotations, deflating negligible off-diagonal entries) diagonalise
 // T.  Both transformations are accumulated into the rows of VT, so on return row j of VT is the
 // unit eigenvector of eigenvalue w[j] (unsorted).  All updates run along contiguous rows.
-inline void sym_eigen(std::vector<double>& A, int n, std::vector<double>& w, std::vector<double>& VT) {
+// Returns false when the QR steps have not deflated every off-diagonal entry within max_steps
+// (default 60 n, about 30 times what the shift needs in practice); w and VT are then not
+// eigenpairs.
+inline bool sym_eigen(std::vector<double>& A, int n, std::vector<double>& w, std::vector<double>& VT,
+                      int max_steps = -1) {
+  if (max_steps < 0) max_steps = 60 * n;
   VT.assign((size_t)n * n, 0.0);
   for (int i = 0; i < n; ++i) VT[(size_t)i * n + i] = 1.0;
   std::vector<double> d(n), e(n, 0.0), u(n), p(n), acc(n);
@@ -117,7 +122,7 @@ inline void sym_eigen(std::vector<double>& A, int n, std::vector<double>& w, std
   if (n >= 2) e[n - 2] = A[(size_t)(n - 2) * n + n - 1];
   const double eps = 2.220446049250313e-16;
   int hi = n - 1;
-  for (int guard = 0; hi > 0 && guard < 60 * n;) {
+  for (int guard = 0; hi > 0 && guard < max_steps;) {
     if (fabs(e[hi - 1]) <= eps * (fabs(d[hi - 1]) + fabs(d[hi]))) {  // d[hi] has converged
       e[hi - 1] = 0.0;
       --hi;
@@ -156,6 +161,7 @@ inline void sym_eigen(std::vector<double>& A, int n, std::vector<double>& w, std
     }
   }
   w = d;
+  return hi <= 0;
 }
 
 }  // namespace hmoe

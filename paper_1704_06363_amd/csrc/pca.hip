@@ -176,7 +176,10 @@ static int orthonormalise(float*& Q, float*& Z, int d, int r, float* S, float* R
         return HMOE_EINVAL;
       }
       std::vector<double> A = Sd, w, VT;
-      sym_eigen(A, r, w, VT);
+      if (!sym_eigen(A, r, w, VT)) {
+        set_error("pca: the eigensolve of the %d x %d Gram matrix did not converge", r, r);
+        return HMOE_ENUMERIC;
+      }
       double wmax = 0.0;
       for (double x : w) wmax = x > wmax ? x : wmax;
       std::vector<int32_t> flags(r, 0);
@@ -260,7 +263,10 @@ static int pca_fit_t(const T* X, int64_t n, int d, int r, int n_iter, uint64_t s
   std::vector<double> Tm((size_t)r * r), w, VT;
   for (int i = 0; i < r; ++i)
     for (int j = 0; j < r; ++j) Tm[(size_t)i * r + j] = 0.5 * ((double)hs[(size_t)i * r + j] + hs[(size_t)j * r + i]);
-  sym_eigen(Tm, r, w, VT);
+  if (!sym_eigen(Tm, r, w, VT)) {
+    set_error("pca: the eigensolve of the %d x %d Rayleigh-Ritz matrix did not converge", r, r);
+    return HMOE_ENUMERIC;
+  }
   std::vector<int> ord(r);
   for (int i = 0; i < r; ++i) ord[i] = i;
   std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) { return w[a] > w[b]; });

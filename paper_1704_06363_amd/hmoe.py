@@ -164,6 +164,17 @@ def _dt(t):
         raise HmoeError(f"unsupported dtype {t.dtype}") from None
 
 
+def _expect(t, shape, dtype, what):
+    """t (if given) must have this shape (None entries match any size) and dtype: a tensor of
+    another dtype or size would make the library read or write past its bytes."""
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise HmoeError(f"{what}: dtype {t.dtype}, {dtype} expected")
+    if len(t.shape) != len(shape) or any(e is not None and a != e for a, e in zip(t.shape, shape)):
+        raise HmoeError(f"{what}: shape {tuple(t.shape)}, {tuple(shape)} expected")
+
+
 def _workspace(nbytes, ws, device):
     if nbytes == 0:
         return None, 0
@@ -185,6 +196,9 @@ def kmeans_assign(X, C, assign=None, min_dist=None, want_min_dist=True, ws=None)
     n, d = X.shape
     K = C.shape[0]
     dev = X.device
+    _expect(C, (K, d), X.dtype, "C")
+    _expect(assign, (n,), torch.int32, "assign")
+    _expect(min_dist, (n,), torch.float32, "min_dist")
     if assign is None:
         assign = torch.empty(n, dtype=torch.int32, device=dev)
     if min_dist is None and want_min_dist:
@@ -207,6 +221,7 @@ def kmeans_fit(X, K, n_iter, init_uniforms=None, C=None, reseed=True, ws=None):
     dev = X.device
     if (init_uniforms is None) == (C is None):
         raise HmoeError("give exactly one of init_uniforms or C")
+    _expect(C, (K, d), torch.float32, "C (fp32 master centres)")
     Cout = torch.empty(K, d, dtype=torch.float32, device=dev) if C is None else C.clone()
     u = None
     if init_uniforms is not None:
@@ -235,6 +250,12 @@ def kmeans_update(X, K, assign, min_dist, sums, counts, C, mode=UPDATE_FULL, res
     [K,d]), counts (int64 [K]), C (fp32 [K,d]) and assign are updated in place."""
     n, d = (X.shape if X is not None else (0, C.shape[1]))
     dev = C.device
+    _expect(C, (K, d), torch.float32, "C")
+    _expect(sums, (K, d), torch.float64, "sums")
+    _expect(counts, (K,), torch.int64, "counts")
+    if X is not None:
+        _expect(assign, (n,), torch.int32, "assign")
+        _expect(min_dist, (n,), torch.float32, "min_dist")
     dt = _dt(X) if X is not None else F32
     w, wb = _workspace(lib().hmoe_kmeans_update_workspace(n, d, K, dt), ws, dev)
     _chk(lib().hmoe_kmeans_update(_ptr(X), dt, n, d, K, _ptr(assign), _ptr(min_dist), _ptr(sums),
@@ -248,11 +269,22 @@ def moe_dispatch_workspace(n, K) -> int:
     return lib().hmoe_moe_dispatch_workspace(n, K)
 
 
+def _check_dispatch(expert, K, rows, o):
+    n = expert.shape[0]
+    _expect(expert, (n,), torch.int32, "expert")
+    for k, shape in (("counts", (K,)), ("offsets", (K + 1,)), ("perm", (n,)), ("inv", (n,))):
+        _expect(o.get(k), shape, torch.int32, k)
+    if rows is not None:
+        _expect(rows, (n, None), None, "rows")
+        _expect(o.get("rows_sorted"), tuple(rows.shape), rows.dtype, "rows_sorted")
+
+
 def moe_dispatch(expert, K, rows=None, out=None, ws=None):
     """Stable bucketing of the batch by expert; optionally gathers rows into expert order."""
     n = expert.shape[0]
     dev = expert.device
     o = out or {}
+    _check_dispatch(expert, K, rows, o)
     counts = _out(o, "counts", lambda: torch.empty(K, dtype=torch.int32, device=dev))
     offsets = _out(o, "offsets", lambda: torch.empty(K + 1, dtype=torch.int32, device=dev))
     perm = _out(o, "perm", lambda: torch.empty(n, dtype=torch.int32, device=dev))
@@ -282,6 +314,7 @@ def moe_dispatch_noalloc(expert, K, rows=None, out=None):
     n = expert.shape[0]
     dev = expert.device
     o = out or {}
+    _check_dispatch(expert, K, rows, o)
     counts = _out(o, "counts", lambda: torch.empty(K, dtype=torch.int32, device=dev))
     offsets = _out(o, "offsets", lambda: torch.empty(K + 1, dtype=torch.int32, device=dev))
     perm = _out(o, "perm", lambda: torch.empty(n, dtype=torch.int32, device=dev))
@@ -301,6 +334,9 @@ def moe_dispatch_noalloc(expert, K, rows=None, out=None):
 def permute_rows(inp, index, out=None):
     """out[r] = inp[index[r]]."""
     n = index.shape[0]
+    _expect(index, (n,), torch.int32, "index")
+    _expect(inp, (n, None), None, "inp")
+    _expect(out, tuple(inp.shape), inp.dtype, "out")
     if out is None:
         out = torch.empty((n, inp.shape[1]), dtype=inp.dtype, device=inp.device)
     _chk(lib().hmoe_permute_rows(_ptr(inp), _ptr(out), _ptr(index), n, inp.shape[1], _dt(inp),
@@ -310,9 +346,27 @@ def permute_rows(inp, index, out=None):
 
 # ------------------------------------------------------------------ experts + decoder
 
+class _Dims:
+    """The sizes of a parameter dict, checked for consistency (shapes and one dtype)."""
+
+    def __init__(self, p: dict):
+        K, h, d = p["W1"].shape
+        o = p["W2"].shape[1]
+        per_expert = p["D"].dim() == 3
+        if per_expert and p["D"].shape[0] != K:
+            raise HmoeError(f"per-expert decoders need D [K, V, o] with K = {K}, got {tuple(p['D'].shape)}")
+        V = p["D"].shape[-2]
+        dec = (K,) if per_expert else ()
+        for k, shape in (("W1", (K, h, d)), ("b1", (K, h)), ("W2", (K, o, h)), ("b2", (K, o)),
+                         ("D", dec + (V, o)), ("bD", dec + (V,))):
+            _expect(p.get(k), shape, p["W1"].dtype, k)
+        self.K, self.d_in, self.d_hid, self.d_out, self.vocab = K, d, h, o, V
+
+
 def make_params(p: dict) -> MoeParams:
     """p: W1 [K,h,d], b1 [K,h] or None, W2 [K,o,h], b2 [K,o] or None, and the decoder: shared,
     D [V,o] with bD [V] or None, or one per expert, D [K,V,o] with bD [K,V] or None."""
+    _Dims(p)
     K, h, d = p["W1"].shape
     o = p["W2"].shape[1]
     per_expert = p["D"].dim() == 3
@@ -335,17 +389,33 @@ def anchor_shape(n: int, V: int):
     return ((V + ANCHOR_TILE - 1) // ANCHOR_TILE, n, ANCHOR_TILE // ANCHOR_COLS)
 
 
+def _check_moe_io(prm, n, dt, X_sorted, offsets, perm, o):
+    """The activations in the parameters' dtype and the shapes the library assumes."""
+    _expect(X_sorted, (n, prm.d_in), dt, "X_sorted")
+    _expect(offsets, (prm.K + 1,), torch.int32, "offsets")
+    _expect(perm, (n,), torch.int32, "perm")
+    _expect(o.get("H1_sorted"), (n, prm.d_hid), dt, "H1_sorted")
+    _expect(o.get("H"), (n, prm.d_out), dt, "H")
+
+
 def moe_forward(p: dict, X_sorted, offsets, perm, row_ptr, tag, out=None, ws=None,
                 save_logits=False):
     """Expert MLPs + decoder(s) + multilabel softmax loss (Eq. 3).  With save_logits the
     [n, V] logits are returned too (for a backward that does not recompute them; in slot
     order, row p = sample perm[p], when every expert has its own decoder, which needs them),
     stored as offsets from per-row anchors (returned as logit_anchor, anchor_shape(n, V))."""
-    prm = make_params(p)
+    dims = _Dims(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
-    dt = X_sorted.dtype
+    dt = p["W1"].dtype
     o = out or {}
+    _check_moe_io(dims, n, dt, X_sorted, offsets, perm, o)
+    prm = make_params(p)
+    _expect(o.get("logits"), (n, prm.vocab), dt, "logits")
+    _expect(o.get("logit_anchor"), anchor_shape(n, prm.vocab), torch.float32, "logit_anchor")
+    for k in ("lse", "loss"):
+        _expect(o.get(k), (n,), torch.float32, k)
+    _expect(o.get("loss_mean"), (1,), torch.float32, "loss_mean")
     H1s = _out(o, "H1_sorted", lambda: torch.empty(n, prm.d_hid, dtype=dt, device=dev))
     H = _out(o, "H", lambda: torch.empty(n, prm.d_out, dtype=dt, device=dev))
     lse = _out(o, "lse", lambda: torch.empty(n, dtype=torch.float32, device=dev))
@@ -370,20 +440,33 @@ def moe_backward(p: dict, X_sorted, offsets, perm, inv, row_ptr, tag, H1_sorted,
                  want_dX=True, out=None, ws=None, logits=None, logit_anchor=None):
     """Gradients of the mean loss for all expert and decoder parameters (fp32) and dX.  With
     logits and logit_anchor (saved by the forward) the decoder logits are not recomputed."""
-    prm = make_params(p)
+    prm = _Dims(p)
     n = X_sorted.shape[0]
     dev = X_sorted.device
     K, d, h, o_, V = prm.K, prm.d_in, prm.d_hid, prm.d_out, prm.vocab
     f32 = torch.float32
     o = out or {}
+    dt = p["W1"].dtype
+    _check_moe_io(prm, n, dt, X_sorted, offsets, perm, {"H1_sorted": H1_sorted, "H": H})
+    _expect(inv, (n,), torch.int32, "inv")
+    _expect(lse, (n,), f32, "lse")
+    _expect(logits, (n, V), dt, "logits")
+    _expect(logit_anchor, anchor_shape(n, V), f32, "logit_anchor")
+    if (logits is None) != (logit_anchor is None):
+        raise HmoeError("logits and logit_anchor go together (the forward's stored form)")
+    for k, shape in (("dW1", (K, h, d)), ("db1", (K, h)), ("dW2", (K, o_, h)), ("db2", (K, o_)),
+                     ("dD", tuple(p["D"].shape)), ("dbD", tuple(p["D"].shape[:-1]))):
+        _expect(o.get(k), shape, f32, k)
+    _expect(o.get("dX"), (n, d), dt, "dX")
     g = {"dW1": _out(o, "dW1", lambda: torch.empty(K, h, d, dtype=f32, device=dev)),
          "db1": _out(o, "db1", lambda: torch.empty(K, h, dtype=f32, device=dev)),
          "dW2": _out(o, "dW2", lambda: torch.empty(K, o_, h, dtype=f32, device=dev)),
          "db2": _out(o, "db2", lambda: torch.empty(K, o_, dtype=f32, device=dev)),
          "dD": _out(o, "dD", lambda: torch.empty(p["D"].shape, dtype=f32, device=dev)),
          "dbD": _out(o, "dbD", lambda: torch.empty(p["D"].shape[:-1], dtype=f32, device=dev)),
-         "dX": (_out(o, "dX", lambda: torch.empty(n, d, dtype=X_sorted.dtype, device=dev))
+         "dX": (_out(o, "dX", lambda: torch.empty(n, d, dtype=dt, device=dev))
                 if want_dX else None)}
+    prm = make_params(p)
     lab = Labels(_ptr(row_ptr), _ptr(tag))
     w, wb = _workspace(moe_workspace(prm, n), ws, dev)
     _chk(lib().hmoe_moe_backward(ctypes.byref(prm), n, _ptr(X_sorted), _ptr(offsets), _ptr(perm),
@@ -405,12 +488,13 @@ def topm(logits, m: int, out=None, want_values=False, anchor=None):
     n, V = logits.shape
     dev = logits.device
     o = out or {}
+    _expect(o.get("idx"), (n, m), torch.int32, "idx")
+    _expect(o.get("val") if want_values else None, (n, m), torch.float32, "val")
     idx = o["idx"] if "idx" in o else torch.empty(n, m, dtype=torch.int32, device=dev)
     val = None
     if want_values:
         val = o["val"] if "val" in o else torch.empty(n, m, dtype=torch.float32, device=dev)
-    if anchor is not None and tuple(anchor.shape) != anchor_shape(n, V):
-        raise HmoeError(f"anchor of shape {tuple(anchor.shape)}, {anchor_shape(n, V)} needed")
+    _expect(anchor, anchor_shape(n, V), torch.float32, "anchor")
     _chk(lib().hmoe_topm(_ptr(logits), _ptr(anchor), _dt(logits), n, V, m, _ptr(idx), _ptr(val), _stream()),
          "topm")
     return (idx, val) if want_values else idx
@@ -437,6 +521,10 @@ def sgd_step(w, g, lr: float, weight_decay: float = 0.0, momentum: float = 0.0, 
     dtype (bf16 or fp32)."""
     if w.dtype != torch.float32 or g.dtype != torch.float32 or g.numel() != w.numel():
         raise HmoeError("sgd_step needs fp32 w and g of the same size")
+    if w_lo is not None and w_lo.numel() != w.numel():
+        raise HmoeError(f"w_lo has {w_lo.numel()} elements, w {w.numel()}")
+    if v is not None and (v.dtype != torch.float32 or v.numel() != w.numel()):
+        raise HmoeError("v must be fp32 with as many elements as w")
     dt = _dt(w_lo) if w_lo is not None else 1
     _chk(lib().hmoe_sgd_step(_ptr(w), _ptr(g), _ptr(v), _ptr(w_lo), dt, w.numel(), lr, weight_decay, momentum,
                              _stream()), "sgd_step")
@@ -467,6 +555,9 @@ def pca_project(X, mean, comps, out=None, ws=None):
     """(X - mean) comps^T in X's dtype: the features the K-means runs on."""
     n, d = X.shape
     r = comps.shape[0]
+    _expect(mean, (d,), torch.float32, "mean")
+    _expect(comps, (r, d), torch.float32, "comps")
+    _expect(out, (n, r), X.dtype, "out")
     Z = out if out is not None else torch.empty(n, r, dtype=X.dtype, device=X.device)
     w, wb = _workspace(pca_workspace(n, d, r, X.dtype), ws, X.device)
     _chk(lib().hmoe_pca_project(_ptr(X), _dt(X), n, d, _ptr(mean), _ptr(comps), r, _ptr(Z), _ptr(w), wb, _stream()),

@@ -122,3 +122,24 @@ def test_binding_refuses_host_tensors(lib):
     import torch
     with pytest.raises(hmoe.HmoeError):
         hmoe.kmeans_assign(torch.zeros(4, 8), torch.zeros(2, 8))
+
+
+def test_binding_refuses_mismatched_dtypes_and_shapes():
+    # checked before any pointer is taken: a tensor of another dtype or size would make the
+    # library read or write past its bytes
+    import torch
+    with pytest.raises(hmoe.HmoeError, match="dtype"):
+        hmoe.kmeans_assign(torch.zeros(4, 8), torch.zeros(2, 8, dtype=torch.bfloat16))
+    with pytest.raises(hmoe.HmoeError, match="shape"):
+        hmoe.kmeans_assign(torch.zeros(4, 8), torch.zeros(2, 16))
+    p = {"W1": torch.zeros(2, 16, 8, dtype=torch.bfloat16), "b1": None,
+         "W2": torch.zeros(2, 8, 16, dtype=torch.bfloat16), "b2": None,
+         "D": torch.zeros(24, 8, dtype=torch.bfloat16), "bD": None}
+    with pytest.raises(hmoe.HmoeError, match="X_sorted: dtype"):
+        hmoe.moe_forward(p, torch.zeros(4, 8), torch.zeros(3, dtype=torch.int32), torch.zeros(4, dtype=torch.int32),
+                         None, None)
+    bad = dict(p, W2=torch.zeros(2, 8, 16))
+    with pytest.raises(hmoe.HmoeError, match="W2: dtype"):
+        hmoe.make_params(bad)
+    with pytest.raises(hmoe.HmoeError, match="counts: shape"):
+        hmoe.moe_dispatch(torch.zeros(4, dtype=torch.int32), 3, out={"counts": torch.zeros(4, dtype=torch.int32)})

@@ -55,6 +55,14 @@ def test_sym_eigen_matches_lapack(driver, name, A):
     assert np.abs(A @ VT.T - VT.T * w).max() <= 1e-12 * scale  # A v_j = w_j v_j
 
 
+def test_sym_eigen_reports_non_convergence(driver):
+    # allowed a single implicit QR step, a 64 x 64 random matrix cannot deflate: the solver must
+    # say so instead of returning its partial result as eigenpairs
+    M = np.random.default_rng(9).standard_normal((64, 64))
+    assert _run(driver, "eigcap", M + M.T) == ["notconverged"]
+    assert _run(driver, "eigcap", np.diag(np.arange(4.0))) == ["converged"]  # already diagonal
+
+
 @pytest.mark.parametrize("n", [1, 5, 64, 256])
 def test_chol_inverse_matches_lapack(driver, n):
     rs = np.random.default_rng(n)

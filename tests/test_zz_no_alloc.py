@@ -31,7 +31,7 @@ def test_noalloc_dispatch_matches_workspace_dispatch(n, K, w, dtype):
     # second call, smaller (skewed buckets, one empty): the array still holds the first call's counts
     m, K2 = 3001, 128
     ids2 = torch.as_tensor(W.zipf_bucket_ids(m, K2, seed=3)).cuda()
-    rows2 = rows[:m].contiguous()
+    rows2 = W.rectified_gaussian(m, w, seed=m, dtype=dtype, device="cuda")
     ref2 = hmoe.moe_dispatch(ids2, K2, rows=rows2)
     got2 = hmoe.moe_dispatch_noalloc(ids2, K2, rows=rows2)
     torch.cuda.synchronize()
