@@ -316,6 +316,20 @@ struct CfgD {
 // 256 x 256 tiles, eight waves of 128 x 64, a 4-stage ring (128 KB): 3 and 5 stages measured
 // slower for the decoder and expert GEMMs.
 typedef CfgD<bf16, 256, 256, 128, 64, 4> CfgDma;
+// The last row tile of a group with at most 128 rows (the short buckets of skewed routing) runs
+// at half height: 128 x 256, eight waves of 64 x 64, a 5-stage ring (120 KB, inside the
+// 256 x 256 tile's allocation), with half the MFMA work of the padded 256-row tile.  Such a
+// tile streams a whole weight panel for few rows: with one row per bucket, 1024 tiles read
+// their 1.07 GB of panels at ~4 TB/s whether the ring runs 4, 5 or 6 stages.
+typedef CfgD<bf16, 128, 256, 64, 64, 5> CfgDmaShort;
+template <class C>
+struct ShortTile {
+  using type = void;
+};
+template <>
+struct ShortTile<CfgDma> {
+  using type = CfgDmaShort;
+};
 typedef CfgD<float, 256, 256, 128, 64, 4> CfgDmaF32;        // fp32, K-contiguous operands
 // fp32 with at most 64 columns (the gater's assignment, K <= 64): 128 x 64 tiles of four waves
 // and a 3-stage ring (36 KB), four workgroups per CU -- measured against 256 x 64 (4 stages:

@@ -37,16 +37,12 @@ struct Ident {
 
 // LAYER 1: H1s[m] = relu(Xs[m] W1_e^T + b1_e).   LAYER 2: H[perm[m]] = H1s[m] W2_e^T + b2_e.
 template <class C, int LAYER>
-__global__ void __launch_bounds__(C::THREADS)
-    k_expert_fwd(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
-                 const typename C::type* __restrict__ bias, const int32_t* __restrict__ seg,
-                 const int32_t* __restrict__ tile_start, int G, int N, int Kd, const int32_t* __restrict__ perm,
-                 typename C::type* __restrict__ out) {
+__device__ __forceinline__ void expert_fwd_tile(const TileCoord& tc, const typename C::type* __restrict__ A,
+                                                const typename C::type* __restrict__ W,
+                                                const typename C::type* __restrict__ bias, int N, int Kd,
+                                                const int32_t* __restrict__ perm, typename C::type* __restrict__ out,
+                                                lds<char>* smem) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
-  lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
-  if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, true>(A + tc.m0 * Kd, Kd, tc.m_rows, W + ((int64_t)tc.group * N + tc.n0) * Kd, Kd,
                            tc.n_cols, Kd, smem, acc);
@@ -67,6 +63,36 @@ __global__ void __launch_bounds__(C::THREADS)
     store_out<C, T>(tc, acc, smem, out, N, elem, RowId{tc.m0}, NoVec{});
   else
     store_out<C, T>(tc, acc, smem, out, N, elem, RowVia{perm, tc.m0}, NoVec{});
+}
+
+// A group's last row tile with few enough rows runs the half-height configuration when C has
+// one (the workgroup size and the LDS allocation are C's).
+template <class C, class Body>
+__device__ __forceinline__ void by_tile_height(const TileCoord& tc, Body body) {
+  using S = typename ShortTile<C>::type;
+  if constexpr (!std::is_void<S>::value) {
+    static_assert(S::THREADS == C::THREADS && S::LDS <= C::LDS, "short tile inside the workgroup");
+    if (tc.m_rows <= S::BM) {
+      body(S{});
+      return;
+    }
+  }
+  body(C{});
+}
+
+template <class C, int LAYER>
+__global__ void __launch_bounds__(C::THREADS)
+    k_expert_fwd(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
+                 const typename C::type* __restrict__ bias, const int32_t* __restrict__ seg,
+                 const int32_t* __restrict__ tile_start, int G, int N, int Kd, const int32_t* __restrict__ perm,
+                 typename C::type* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  const TileCoord tc = tile_group_m<C>(seg, tile_start, G, N, Kd);
+  if (!tc.valid) return;
+  by_tile_height<C>(tc, [&](auto cfg) {
+    expert_fwd_tile<decltype(cfg), LAYER>(tc, A, W, bias, N, Kd, perm, out, smem);
+  });
 }
 
 // ------------------------------------------------------------------ decoder forward
@@ -992,17 +1018,13 @@ struct ReluMask {
 // order.  !MASK: dX[perm[m]] = dZ[m] W1_e, stored in sample order (in slot order, row m, when
 // perm is NULL: the per-expert decoders' dH = g D_e).
 //   A: [rows][Kd] (ld Kd), W: [G][Kd][N] (the layer's [out][in] weights seen as [K][N]).
-template <class C, bool MASK, bool XCD = false>
-__global__ void __launch_bounds__(C::THREADS)
-    k_expert_dgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
-                   const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
-                   const typename C::type* __restrict__ H1s, const int32_t* __restrict__ perm,
-                   typename C::type* __restrict__ out) {
+template <class C, bool MASK>
+__device__ __forceinline__ void expert_dgrad_tile(const TileCoord& tc, const typename C::type* __restrict__ A,
+                                                  const typename C::type* __restrict__ W, int N, int Kd,
+                                                  const typename C::type* __restrict__ H1s,
+                                                  const int32_t* __restrict__ perm,
+                                                  typename C::type* __restrict__ out, lds<char>* smem) {
   using T = typename C::type;
-  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
-  lds<char>* smem = (lds<char>*)smem_raw;
-  const TileCoord tc = tile_group_m<C, XCD>(seg, tile_start, G, N, Kd);
-  if (!tc.valid) return;
   floatx4 acc[C::MI][C::NJ];
   gemm_tile<C, true, false>(A + tc.m0 * Kd, Kd, tc.m_rows, W + (int64_t)tc.group * Kd * N + tc.n0, N, tc.n_cols,
                             Kd, smem, acc);
@@ -1012,6 +1034,21 @@ __global__ void __launch_bounds__(C::THREADS)
     store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowVia{perm, tc.m0}, NoVec{});
   else
     store_out<C, T>(tc, acc, smem, out, N, Ident{}, RowId{tc.m0}, NoVec{});
+}
+
+template <class C, bool MASK, bool XCD = false>
+__global__ void __launch_bounds__(C::THREADS)
+    k_expert_dgrad(const typename C::type* __restrict__ A, const typename C::type* __restrict__ W,
+                   const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_start, int G, int N, int Kd,
+                   const typename C::type* __restrict__ H1s, const int32_t* __restrict__ perm,
+                   typename C::type* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds<char>* smem = (lds<char>*)smem_raw;
+  const TileCoord tc = tile_group_m<C, XCD>(seg, tile_start, G, N, Kd);
+  if (!tc.valid) return;
+  by_tile_height<C>(tc, [&](auto cfg) {
+    expert_dgrad_tile<decltype(cfg), MASK>(tc, A, W, N, Kd, H1s, perm, out, smem);
+  });
 }
 
 // ------------------------------------------------------------------ launchers
@@ -1088,7 +1125,8 @@ static int forward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const i
   HMOE_LAUNCH("expert layer 1", (k_expert_fwd<C, 1>), dim3((unsigned)(mt_bound * cdiv(s.h, C::BN))),
               dim3(C::THREADS), C::LDS, st, Xs, W1, (const T*)p->b1, offsets, ts, s.K, s.h, s.d, perm, H1s);
   HMOE_LAUNCH("expert layer 2", (k_expert_fwd<C, 2>), dim3((unsigned)(mt_bound * cdiv(s.o, C::BN))),
-              dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h, perm, H);
+              dim3(C::THREADS), C::LDS, st, (const T*)H1s, W2, (const T*)p->b2, offsets, ts, s.K, s.o, s.h,
+              perm, H);
   if (s.nd > 1) {
     // one decoder per expert: decode in slot order
     HMOE_TRY(launch_permute(H, Hs, perm, n, s.o, p->dt, st));
@@ -1212,8 +1250,8 @@ static int backward_t(const hmoe_moe_params_t* p, int64_t n, const T* Xs, const 
               dim3(C::THREADS), C::LDS, st, (const T*)dZ, Xs, offsets, order, s.K, s.h, s.d, dW1);
   if (dX)
     HMOE_LAUNCH("expert dX", (k_expert_dgrad<C, false>), dim3((unsigned)(mt_bound * cdiv(s.d, C::BN))),
-                dim3(C::THREADS), C::LDS, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h, (const T*)nullptr, perm,
-                dX);
+                dim3(C::THREADS), C::LDS, st, (const T*)dZ, W1, offsets, ts, s.K, s.d, s.h,
+                (const T*)nullptr, perm, dX);
   return HMOE_OK;
 }
 

@@ -81,6 +81,21 @@ def test_skewed_routing_with_empty_experts():
         assert torch.count_nonzero(g[k][torch.as_tensor(empty).cuda()]) == 0, k
 
 
+def test_bucket_sizes_around_the_half_height_tile():
+    # a group's last row tile runs at half height (128 rows) when it holds at most 128 rows:
+    # buckets on both sides of that boundary and of the 256-row tile, next to empty and
+    # one-sample experts, through every row-grouped GEMM (layers 1 and 2, dH1 and dX)
+    sizes = [128, 1, 129, 0, 256, 127, 257, 64, 384, 255, 385]
+    n, K = sum(sizes), len(sizes)
+    ids = np.repeat(np.arange(K, dtype=np.int32), sizes)
+    ids = ids[np.random.default_rng(11).permutation(n)]
+    inp = W.skewed_inputs(device="cuda", seed=12, n=n, d=256, h=384, o=136, V=600, K=K, bias=True)
+    g, counts = _check_step(inp["X"], ids, K, inp["params"], inp["row_ptr"], inp["tag"], saved=True)
+    assert counts.tolist() == sizes
+    for k in ("dW1", "db1", "dW2", "db2"):
+        assert torch.count_nonzero(g[k][3]) == 0, k
+
+
 def test_single_expert():
     inp = W.skewed_inputs(device="cuda", seed=6, n=300, d=64, h=128, o=64, V=256, K=1)
     ids = np.zeros(300, np.int32)
