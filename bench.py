@@ -502,7 +502,11 @@ def leg_inference(steps, warmup, m=10, draws=100000):
                        f"then top-{m} per row and p@m / q@m counts ({draws} q draws)",
            "samples_per_s": round(s["n"] / (ms * 1e-3), 1), "ms_per_batch": round(ms, 3),
            "topm_ms": round(tk, 4),
-           "topm_frac_hbm_peak": round(s["n"] * s["V"] * 2 / (tk * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           # the anchored top-m reads the anchors (4 bytes per 64 columns) and about m blocks of
+           # 64 bf16 logits per row, not the whole row: the rate of the whole-row scan it replaces
+           # is quoted as the logits it did not have to read
+           "topm_logits_gb_per_s_equiv": round(s["n"] * s["V"] * 2 / (tk * 1e-3) / 1e9, 1),
+           "topm_anchor_bytes": int(s["n"] * -(-s["V"] // 256) * 16),
            "p_at_m": [round(float(x) / nnz, 6) for x in h[0]],
            "q_at_m": [round(float(x) / draws, 6) for x in h[1]],
            "kernels": k}

@@ -266,10 +266,13 @@ int hmoe_sgd_step(float* w, const float* g, float* v, void* w_lo, hmoe_dtype_t d
  * order, so these are the m most probable tags), the indices of its m largest entries in
  * decreasing order, equal values in increasing index order.  With anchor (float, the layout of
  * HMOE_ANCHOR_*, as written by hmoe_moe_forward) an entry is anchor + stored value, formed in
- * fp32; with anchor NULL it is the stored value.  idx int32[n][m] out; val float[n][m] out or
- * NULL (the entries at those indices).  1 <= m <= 16, m <= vocab; the entries are assumed
- * finite or -inf.  One wave per row; the logits are read once.  Errors: HMOE_EINVAL (m out of
- * range, NULL logits or idx), HMOE_ESHAPE (vocab not a multiple of 8). */
+ * fp32, and every stored value must be <= 0 (each anchor at least every entry of its
+ * HMOE_ANCHOR_COLS-column block, as hmoe_moe_forward writes them): the kernel then reads the
+ * anchors and only the blocks whose anchor can reach the row's m-th entry.  With anchor NULL an
+ * entry is the stored value and each row is read once.  idx int32[n][m] out; val float[n][m]
+ * out or NULL (the entries at those indices).  1 <= m <= 16, m <= vocab; the entries are
+ * assumed finite or -inf.  One wave per row.  Errors: HMOE_EINVAL (m out of range, NULL
+ * logits or idx), HMOE_ESHAPE (vocab not a multiple of 8). */
 int hmoe_topm(const void* logits, const float* anchor, hmoe_dtype_t dt, int64_t n, int32_t vocab,
               int32_t m, int32_t* idx, float* val, void* stream);
 

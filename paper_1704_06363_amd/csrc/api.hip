@@ -503,7 +503,7 @@ int hmoe_topm(const void* logits, const float* anchor, hmoe_dtype_t dt, int64_t 
   if (n == 0) return HMOE_OK;
   HMOE_TRY(check_ptr("logits", logits));
   HMOE_TRY(check_ptr("idx", idx, false));
-  if (anchor) HMOE_TRY(check_ptr("anchor", anchor, false));
+  if (anchor) HMOE_TRY(check_ptr("anchor", anchor));
   return launch_topm(logits, anchor, dt, n, vocab, m, idx, val, (hipStream_t)stream);
 }
 

@@ -484,7 +484,7 @@ def topm(logits, m: int, out=None, want_values=False, anchor=None):
     """t_m (Section 4.4): the indices [n, m] of each row's m largest logits, decreasing, equal
     values by increasing index (and their values, fp32, with want_values).  anchor: the
     forward's logit_anchor when logits are its stored offsets (an entry is then anchor +
-    offset in fp32)."""
+    offset in fp32; every offset must be <= 0, as the forward writes them)."""
     n, V = logits.shape
     dev = logits.device
     o = out or {}

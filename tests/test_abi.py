@@ -102,6 +102,8 @@ def test_argument_errors_are_reported_before_launch(lib):
     assert rc == -1 and "m = 17" in hmoe.last_error()
     rc = lib.hmoe_topm(16, None, 1, 10, 60, 5, 16, None, None)
     assert rc == -3 and "vocab" in hmoe.last_error()
+    rc = lib.hmoe_topm(16, 20, 1, 10, 64, 5, 16, None, None)  # anchors are read as 16-byte vectors
+    assert rc == -3 and "anchor" in hmoe.last_error()
     rc = lib.hmoe_topm_hits(16, 10, 0, ctypes.byref(lab), None, None, 0, 16, None)
     assert rc == -1 and "m = 0" in hmoe.last_error()
     # PCA: more components than dimensions, one sample

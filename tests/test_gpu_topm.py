@@ -11,7 +11,7 @@ import torch
 from oracle import oracle as O
 from paper_1704_06363_amd import hmoe
 from paper_1704_06363_amd import workloads as W
-from tests.parity import anchor_of_columns, np64, npi
+from tests.parity import anchor_of_columns, anchored, np64, npi, unanchored
 
 pytestmark = pytest.mark.gpu
 
@@ -51,6 +51,41 @@ def test_topm_anchored_bit_exact(dtype, n, V, m):
     L, A = off.to(tdt).cuda(), anc.cuda()
     idx, val = hmoe.topm(L, m, want_values=True, anchor=A)
     full = (anchor_of_columns(A, V) + np64(L).astype(np.float32)).astype(np.float32)
+    ref = O.topm(full, m)
+    assert np.array_equal(npi(idx), ref)
+    np.testing.assert_array_equal(np64(val), np.take_along_axis(full, ref.astype(np.int64), axis=1))
+
+
+@pytest.mark.parametrize("dtype,n,V,m,top", [("bf16", 300, 1000, 10, -0.25), ("bf16", 40, 50000, 16, -0.5),
+                                              ("f32", 100, 520, 7, -0.25), ("bf16", 90, 64, 16, 0.0),
+                                              ("bf16", 50, 136, 16, -0.25), ("f32", 64, 8, 8, 0.0)])
+def test_topm_anchored_unattained_anchors(dtype, n, V, m, top):
+    """Anchors that only bound their blocks (every offset at most `top` < 0), so a block with a
+    high anchor may hold only lower entries, and the blocks whose anchor lies between the row's
+    m-th entry and the m-th largest anchor must be read as well; plus rows with fewer 64-column
+    blocks than m (V = 64, 136, 8)."""
+    g = torch.Generator(device="cpu").manual_seed(7 * n + V)
+    nt = (V + 255) // 256
+    anc = torch.randint(-4, 5, (nt, n, 4), generator=g).float() * 0.5
+    off = torch.randint(-16, 1, (n, V), generator=g).float() * 0.25 + top
+    off = torch.minimum(off, torch.tensor(top))
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    L, A = off.to(tdt).cuda(), anc.cuda()
+    idx, val = hmoe.topm(L, m, want_values=True, anchor=A)
+    full = (anchor_of_columns(A, V) + np64(L).astype(np.float32)).astype(np.float32)
+    ref = O.topm(full, m)
+    assert np.array_equal(npi(idx), ref)
+    np.testing.assert_array_equal(np64(val), np.take_along_axis(full, ref.astype(np.int64), axis=1))
+
+
+@pytest.mark.parametrize("n,V,m", [(64, 50000, 10), (200, 4000, 16), (128, 1000, 1)])
+def test_topm_anchored_forward_layout(n, V, m):
+    """The forward's own layout (each anchor its block's maximum, offsets rounded to bf16) from
+    Gaussian logits of the trained-tagger scale."""
+    Lf = np.random.default_rng(n + V).standard_normal((n, V)) * 6.0
+    L, A = anchored(Lf, torch.bfloat16)
+    idx, val = hmoe.topm(L, m, want_values=True, anchor=A)
+    full = unanchored(L, A)
     ref = O.topm(full, m)
     assert np.array_equal(npi(idx), ref)
     np.testing.assert_array_equal(np64(val), np.take_along_axis(full, ref.astype(np.int64), axis=1))
