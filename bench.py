@@ -138,6 +138,8 @@ def step_bytes(s, nnz):
         "assign": n * d * b + K * d * b + n * (i + f),
         "dispatch hist": n * i + nb * (K + 1) * i,
         "dispatch colscan": 2 * nb * (K + 1) * i + K * i,
+        "dispatch offsets": K * i + (K + 1) * i,
+        "dispatch scan": 2 * nb * (K + 1) * i + K * i + (K + 1) * i,  # colscan + offsets in one launch
         "dispatch scatter": n * i + nb * (K + 1) * i + 2 * n * i,
         "permute rows": 2 * n * d * b + n * i,
         "expert layer 1": n * d * b + K * h * d * b + n * h * b,
@@ -672,6 +674,7 @@ def main():
         # second expert layer's epilogue, which writes rows back to sample order); reduction =
         # the experts' bias-gradient segmented sums (the centre update's is in legs.gater_fit)
         "hbm": {"dispatch": hbm_summary(rep, nby, args.steps, ["dispatch hist", "dispatch colscan",
+                                                               "dispatch offsets", "dispatch scan",
                                                                "dispatch scatter", "permute rows"]),
                 "dispatch_row_gather": hbm_summary(rep, nby, args.steps, ["permute rows"]),
                 "reduction_bias_grads": hbm_summary(rep, nby, args.steps, ["segsum partial"]),

@@ -8,6 +8,7 @@
 //   colscan per expert (one wave each), exclusive prefix of block_counts[k][*] over blocks
 //           -> counts[k];
 //   offsets exclusive scan of counts (one block);
+//           (for small problems colscan and offsets run as one single-workgroup kernel);
 //   scatter recomputes the peer masks and writes each id's slot = offsets[k] + earlier blocks
 //           + earlier waves + earlier chunks + rank among earlier peer lanes: the order of
 //           equal ids is the sample order, so the permutation is unique.
@@ -69,16 +70,11 @@ __global__ void __launch_bounds__(256) k_dispatch_hist(const int32_t* __restrict
         hist[k] + hist[KB + k] + hist[2 * KB + k] + hist[3 * KB + k];
 }
 
-// One wave per expert k: exclusive prefix over the blocks of block_counts[k][*] (in place) and
-// counts[k] = its total.  Lane l scans a contiguous run of the blocks, the runs are combined by
-// a wave scan.
-// Buckets 0 .. K (K: the out-of-range ids); counts[k] is written for the K experts only.
-__global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ block_counts, int nb, int K,
-                                                          int32_t* __restrict__ counts) {
-  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+// Exclusive prefix over the blocks of block_counts[k][*] (in place) by one wave; returns the
+// column's total (in every lane).  Lane l scans a contiguous run of the blocks, the runs are
+// combined by a wave scan.
+__device__ __forceinline__ int32_t wave_colscan(int32_t* __restrict__ col, int nb) {
   const int l = threadIdx.x & 63;
-  if (k > K) return;
-  int32_t* col = block_counts + (int64_t)k * nb;
   const int per = (nb + 63) / 64;
   const int b0 = l * per;
   int32_t loc = 0;
@@ -98,7 +94,17 @@ __global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ 
       col[b0 + q] = run;
       run += t;
     }
-  if (l == 63 && k < K) counts[k] = inc;
+  return __shfl(inc, 63, 64);
+}
+
+// One wave per expert k: the column scan of block_counts[k][*] and counts[k] = its total.
+// Buckets 0 .. K (K: the out-of-range ids); counts[k] is written for the K experts only.
+__global__ void __launch_bounds__(256) k_dispatch_colscan(int32_t* __restrict__ block_counts, int nb, int K,
+                                                          int32_t* __restrict__ counts) {
+  const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (k > K) return;
+  const int32_t total = wave_colscan(block_counts + (int64_t)k * nb, nb);
+  if ((threadIdx.x & 63) == 0 && k < K) counts[k] = total;
 }
 
 __global__ void __launch_bounds__(1024) k_dispatch_offsets(const int32_t* __restrict__ counts, int K,
@@ -115,6 +121,39 @@ __global__ void __launch_bounds__(1024) k_dispatch_offsets(const int32_t* __rest
     if (k0 + q < K) {
       offsets[k0 + q] = ex;
       ex += counts[k0 + q];
+    }
+  if (threadIdx.x == 0) offsets[K] = total;
+}
+
+// The column scans and the offsets in one workgroup, for small problems ((K + 1) nb <=
+// kScanSmall): wave j scans the columns k = j, j + 16, ..., the totals meet in LDS, and the
+// workgroup's exclusive scan of them gives the offsets -- one launch instead of two.
+constexpr int64_t kScanSmall = 1 << 16;
+__global__ void __launch_bounds__(1024) k_dispatch_scan_small(int32_t* __restrict__ block_counts, int nb, int K,
+                                                              int32_t* __restrict__ counts,
+                                                              int32_t* __restrict__ offsets) {
+  __shared__ int32_t s_cnt[4096];
+  __shared__ int32_t sh[17];
+  for (int k = threadIdx.x >> 6; k < K; k += 16) {
+    const int32_t total = wave_colscan(block_counts + (int64_t)k * nb, nb);
+    if ((threadIdx.x & 63) == 0) {
+      counts[k] = total;
+      s_cnt[k] = total;
+    }
+  }
+  if ((threadIdx.x >> 6) == K % 16) wave_colscan(block_counts + (int64_t)K * nb, nb);  // the out-of-range bucket
+  __syncthreads();
+  const int per = (K + 1023) / 1024;
+  const int k0 = threadIdx.x * per;
+  int32_t s = 0;
+  for (int q = 0; q < per; ++q)
+    if (k0 + q < K) s += s_cnt[k0 + q];
+  int32_t total;
+  int32_t ex = block_excl_scan<int32_t>(s, sh, &total);
+  for (int q = 0; q < per; ++q)
+    if (k0 + q < K) {
+      offsets[k0 + q] = ex;
+      ex += s_cnt[k0 + q];
     }
   if (threadIdx.x == 0) offsets[K] = total;
 }
@@ -184,9 +223,13 @@ int launch_dispatch(const int32_t* e, int64_t n, int32_t K, int32_t* counts, int
     HMOE_LAUNCH("dispatch hist", k_dispatch_hist, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        (int32_t*)nullptr);
   }
-  HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K + 1, 4)), dim3(256), 0, st, bc, (int)nb,
-              K, counts);
-  HMOE_LAUNCH("dispatch offsets", k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
+  if ((int64_t)(K + 1) * nb <= kScanSmall) {
+    HMOE_LAUNCH("dispatch scan", k_dispatch_scan_small, dim3(1), dim3(1024), 0, st, bc, (int)nb, K, counts, offsets);
+  } else {
+    HMOE_LAUNCH("dispatch colscan", k_dispatch_colscan, dim3((unsigned)cdiv(K + 1, 4)), dim3(256), 0, st, bc,
+                (int)nb, K, counts);
+    HMOE_LAUNCH("dispatch offsets", k_dispatch_offsets, dim3(1), dim3(1024), 0, st, counts, K, offsets);
+  }
   if (nb > 0) {
     HMOE_LAUNCH("dispatch scatter", k_dispatch_scatter, dim3((unsigned)nb), dim3(256), lds, st, e, n, K, bits, bc,
                        offsets, perm, inv);
