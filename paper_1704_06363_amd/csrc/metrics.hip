@@ -183,19 +183,31 @@ __device__ __forceinline__ void topm_block(const T* __restrict__ r, int V, int b
   for (int v = 0; v < VPB; ++v)
     if (take && c0 + v * EPV < V) raw[v] = *reinterpret_cast<const i32x4*>(r + c0 + v * EPV);
   if (!take) return;
+  auto offer = [&](const i32x4& x, int cv0) {
+    const T* e = reinterpret_cast<const T*>(&x);
 #pragma unroll
-  for (int v = 0; v < VPB; ++v) {
-    const int cv0 = c0 + v * EPV;
-    if (cv0 < V) {  // V is a multiple of 8: vectors are whole
-      const T* e = reinterpret_cast<const T*>(&raw[v]);
-#pragma unroll
-      for (int z = 0; z < EPV; ++z) {
-        const float cv = a + to_f32(e[z]);
-        if (cv >= lo && (cv > lv[M - 1] || (cv == lv[M - 1] && cv0 + z < li[M - 1]))) {
-          list_carry(lv, li, cv, cv0 + z);
-          ++cnt;
-        }
+    for (int z = 0; z < EPV; ++z) {
+      const float cv = a + to_f32(e[z]);
+      if (cv >= lo && (cv > lv[M - 1] || (cv == lv[M - 1] && cv0 + z < li[M - 1]))) {
+        list_carry(lv, li, cv, cv0 + z);
+        ++cnt;
       }
+    }
+  };
+  if constexpr (M <= 12) {
+#pragma unroll
+    for (int v = 0; v < VPB; ++v)
+      if (c0 + v * EPV < V) offer(raw[v], c0 + v * EPV);  // V is a multiple of 8: vectors are whole
+  } else {
+    // long lists: one vector per trip, picked by selects (fully unrolled, the insertion code
+    // outgrows the unroller, which then indexes the vectors through scratch memory)
+#pragma unroll 1
+    for (int v = 0; v < VPB; ++v) {
+      if (c0 + v * EPV >= V) break;
+      i32x4 x = raw[0];
+#pragma unroll
+      for (int vv = 1; vv < VPB; ++vv) x = v == vv ? raw[vv] : x;
+      offer(x, c0 + v * EPV);
     }
   }
 }
@@ -321,16 +333,20 @@ __global__ void __launch_bounds__(256) k_topm_anchored(const T* __restrict__ L, 
     li[k] = 0x7fffffff;
   }
   int cnt = 0;  // entries >= a_m that entered this lane's list (each entry enters at most once)
-  // pass 2: the listed blocks with anchor >= a_m (a prefix of the sorted list), two at a time;
+  // pass 2: the listed blocks with anchor >= a_m (a prefix of the sorted list), two at a time
+  // from the head of the list, which then shifts by two (every register index stays static);
   // an unfilled slot (block -1, anchor -inf) is never read, also when a_m is -inf
-#pragma unroll
   for (int k = 0; k < M; k += 2) {
-    const int k1 = k + 1 < M ? k + 1 : k;
-    const bool t0k = !rescan && ab[k] >= 0 && av[k] >= a_m;
-    const bool t1k = k + 1 < M && !rescan && ab[k1] >= 0 && av[k1] >= a_m;
+    const bool t0k = !rescan && ab[0] >= 0 && av[0] >= a_m;
+    const bool t1k = M > 1 && !rescan && ab[M > 1 ? 1 : 0] >= 0 && av[M > 1 ? 1 : 0] >= a_m;
     if (!__any(t0k)) break;  // wave-uniform: the lists are sorted, nothing further qualifies
-    topm_block<T, M>(r, V, ab[k], av[k], a_m, t0k, lv, li, cnt);
-    if (k + 1 < M) topm_block<T, M>(r, V, ab[k1], av[k1], a_m, t1k, lv, li, cnt);
+    topm_block<T, M>(r, V, ab[0], av[0], a_m, t0k, lv, li, cnt);
+    if (M > 1) topm_block<T, M>(r, V, ab[M > 1 ? 1 : 0], av[M > 1 ? 1 : 0], a_m, t1k, lv, li, cnt);
+#pragma unroll
+    for (int q = 0; q < M; ++q) {
+      av[q] = q + 2 < M ? av[q + 2 < M ? q + 2 : q] : -INFINITY;
+      ab[q] = q + 2 < M ? ab[q + 2 < M ? q + 2 : q] : -1;
+    }
   }
   if (__any(rescan)) topm_scan<T, M, TU>(r, arow, n, V, nb, nt, w, a_m, rescan, lv, li, cnt);
   // pass 3 for the rows with fewer than m entries >= a_m
