@@ -91,6 +91,36 @@ def test_topm_anchored_forward_layout(n, V, m):
     np.testing.assert_array_equal(np64(val), np.take_along_axis(full, ref.astype(np.int64), axis=1))
 
 
+def test_topm_anchored_full_size_sampled_rows():
+    """The inference workload's shape and launch (65,536 x 50,000 bf16 logits in the forward's
+    anchored layout, m = 10): 512 seeded rows against the oracle on their own entries, plus
+    every row's list checked for validity (m distinct in-range indices, values non-increasing
+    and equal to the entries they name)."""
+    n, V, m = 65536, 50000, 10
+    g = torch.Generator(device="cuda").manual_seed(21)
+    nt = (V + 255) // 256
+    Lp = torch.full((n, nt * 256), -float("inf"), device="cuda")
+    Lp[:, :V] = torch.randn(n, V, device="cuda", generator=g) * 6.0
+    bm = Lp.view(n, nt, 4, 64).amax(dim=3)  # each 64-column block's maximum: the anchor
+    A = bm.permute(1, 0, 2).contiguous()
+    L = (Lp.view(n, nt, 4, 64) - bm[..., None]).view(n, nt * 256)[:, :V].to(torch.bfloat16).contiguous()
+    del Lp, bm
+    idx, val = hmoe.topm(L, m, want_values=True, anchor=A)
+    rows = np.sort(np.random.default_rng(22).choice(n, 512, replace=False))
+    ri = torch.as_tensor(rows, device="cuda")
+    full = (anchor_of_columns(A[:, ri].contiguous(), V) + np64(L[ri]).astype(np.float32)).astype(np.float32)
+    ref = O.topm(full, m)
+    assert np.array_equal(npi(idx)[rows], ref)
+    np.testing.assert_array_equal(np64(val)[rows], np.take_along_axis(full, ref.astype(np.int64), axis=1))
+    # every row: distinct in-range indices, non-increasing values equal to anchor + offset there
+    it = idx.long()
+    assert int(it.min()) >= 0 and int(it.max()) < V
+    assert bool((it.sort(dim=1).values.diff(dim=1) > 0).all())
+    assert bool((val.diff(dim=1) <= 0).all())
+    anc_at = A.permute(1, 0, 2).reshape(n, nt * 4).gather(1, it // 64)
+    assert torch.equal(anc_at + L.gather(1, it).float(), val)
+
+
 def test_hits_exact():
     n, V, m = 3000, 2000, 10
     L = _logits(n, V, "bf16", seed=5, ties=False)
