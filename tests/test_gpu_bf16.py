@@ -176,6 +176,29 @@ def test_empty_batch():
         assert torch.count_nonzero(g[k]) == 0
 
 
+@pytest.mark.parametrize("K,n,bad", [(63, 1024 * 1024, 0), (63, 1024 * 1024 + 1, 0), (15, 4096 * 1024, 7),
+                                     (15, 4096 * 1024 + 1, 7)])
+def test_dispatch_around_the_fused_scan_size(K, n, bad):
+    # the column scans and offsets run as one workgroup while (K + 1) ceil(n / 1024) <= 2^16 and
+    # as two launches above: both sides of that size, bit-exact against the oracle (with a few
+    # out-of-range ids in the last two cases)
+    rs = np.random.default_rng(K + n)
+    ids = rs.integers(0, K, n).astype(np.int32)
+    if bad:
+        ids[rs.choice(n, bad, replace=False)] = K + 3
+    d = hmoe.moe_dispatch(torch.as_tensor(ids).cuda(), K)
+    good = ids[ids < K]
+    counts, offsets, perm, inv = O.dispatch(good, K)
+    assert npi(d["counts"]).tolist() == counts.tolist()
+    assert npi(d["offsets"]).tolist() == offsets.tolist()
+    # the in-range rows in expert order match the oracle's order over the same rows
+    rows = np.flatnonzero(ids < K)
+    assert np.array_equal(npi(d["perm"])[:len(good)], rows[perm])
+    assert np.array_equal(np.sort(npi(d["perm"])[len(good):]), np.flatnonzero(ids >= K))
+    pv = npi(d["perm"])
+    assert np.array_equal(npi(d["inv"])[pv], np.arange(n))
+
+
 def test_dispatch_out_of_range_ids():
     # ids outside [0, K) are the caller's error: their rows go after every expert's, in sample
     # order, the counts exclude them, and perm / inv stay permutations of all rows
