@@ -194,13 +194,14 @@ __device__ __forceinline__ void topm_block(const T* __restrict__ r, int V, int b
       }
     }
   };
-  if constexpr (M <= 12) {
+  if constexpr (M <= 4) {
 #pragma unroll
     for (int v = 0; v < VPB; ++v)
       if (c0 + v * EPV < V) offer(raw[v], c0 + v * EPV);  // V is a multiple of 8: vectors are whole
   } else {
-    // long lists: one vector per trip, picked by selects (fully unrolled, the insertion code
-    // outgrows the unroller, which then indexes the vectors through scratch memory)
+    // longer lists: one vector per trip, picked by selects.  Fully unrolled, the insertion code
+    // of a block is (64 entries x M steps) long: it compiled for minutes per list length, and
+    // past 12 entries the unroller gave up and indexed the vectors through scratch memory.
 #pragma unroll 1
     for (int v = 0; v < VPB; ++v) {
       if (c0 + v * EPV >= V) break;
@@ -422,37 +423,48 @@ __global__ void __launch_bounds__(256) k_topm_hits(const int32_t* __restrict__ i
 }
 
 template <typename T, int M>
-static int topm_launch(const T* L, const float* anc, int64_t n, int V, int m, int32_t* idx, float* val,
-                       hipStream_t st) {
-  if (anc)
-    HMOE_LAUNCH("top-m", (k_topm_anchored<T, M>), dim3((unsigned)cdiv(n, kTopmRows)), dim3(256), 0, st, L, anc, n,
-                V, m, idx, val);
-  else
-    HMOE_LAUNCH("top-m", (k_topm<T, M>), dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, L, n, V, m, idx, val);
+static int topm_launch(const T* L, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
+  HMOE_LAUNCH("top-m", (k_topm<T, M>), dim3((unsigned)cdiv(n, 4)), dim3(256), 0, st, L, n, V, m, idx, val);
   return HMOE_OK;
 }
 
-// The register lists hold exactly m entries (the insertion and the registers scale with the
-// list length: a 16-entry list for m = 10 ran 25% slower than a 12-entry one).
+// The anchored kernel keeps M >= m entries per list (it takes the m-th of the merged lists), so
+// four list lengths cover m = 1 .. 16.
+template <typename T, int M>
+static int topm_launch_anchored(const T* L, const float* anc, int64_t n, int V, int m, int32_t* idx, float* val,
+                                hipStream_t st) {
+  HMOE_LAUNCH("top-m", (k_topm_anchored<T, M>), dim3((unsigned)cdiv(n, kTopmRows)), dim3(256), 0, st, L, anc, n, V,
+              m, idx, val);
+  return HMOE_OK;
+}
+
+// The plain kernel's register lists hold exactly m entries (the insertion and the registers
+// scale with the list length: a 16-entry list for m = 10 ran 25% slower than a 12-entry one).
 template <typename T>
 static int topm_t(const T* L, const float* anc, int64_t n, int V, int m, int32_t* idx, float* val, hipStream_t st) {
+  if (anc) {
+    if (m <= 4) return topm_launch_anchored<T, 4>(L, anc, n, V, m, idx, val, st);
+    if (m <= 8) return topm_launch_anchored<T, 8>(L, anc, n, V, m, idx, val, st);
+    if (m <= 12) return topm_launch_anchored<T, 12>(L, anc, n, V, m, idx, val, st);
+    return topm_launch_anchored<T, 16>(L, anc, n, V, m, idx, val, st);
+  }
   switch (m) {
-    case 1: return topm_launch<T, 1>(L, anc, n, V, m, idx, val, st);
-    case 2: return topm_launch<T, 2>(L, anc, n, V, m, idx, val, st);
-    case 3: return topm_launch<T, 3>(L, anc, n, V, m, idx, val, st);
-    case 4: return topm_launch<T, 4>(L, anc, n, V, m, idx, val, st);
-    case 5: return topm_launch<T, 5>(L, anc, n, V, m, idx, val, st);
-    case 6: return topm_launch<T, 6>(L, anc, n, V, m, idx, val, st);
-    case 7: return topm_launch<T, 7>(L, anc, n, V, m, idx, val, st);
-    case 8: return topm_launch<T, 8>(L, anc, n, V, m, idx, val, st);
-    case 9: return topm_launch<T, 9>(L, anc, n, V, m, idx, val, st);
-    case 10: return topm_launch<T, 10>(L, anc, n, V, m, idx, val, st);
-    case 11: return topm_launch<T, 11>(L, anc, n, V, m, idx, val, st);
-    case 12: return topm_launch<T, 12>(L, anc, n, V, m, idx, val, st);
-    case 13: return topm_launch<T, 13>(L, anc, n, V, m, idx, val, st);
-    case 14: return topm_launch<T, 14>(L, anc, n, V, m, idx, val, st);
-    case 15: return topm_launch<T, 15>(L, anc, n, V, m, idx, val, st);
-    default: return topm_launch<T, 16>(L, anc, n, V, m, idx, val, st);
+    case 1: return topm_launch<T, 1>(L, n, V, m, idx, val, st);
+    case 2: return topm_launch<T, 2>(L, n, V, m, idx, val, st);
+    case 3: return topm_launch<T, 3>(L, n, V, m, idx, val, st);
+    case 4: return topm_launch<T, 4>(L, n, V, m, idx, val, st);
+    case 5: return topm_launch<T, 5>(L, n, V, m, idx, val, st);
+    case 6: return topm_launch<T, 6>(L, n, V, m, idx, val, st);
+    case 7: return topm_launch<T, 7>(L, n, V, m, idx, val, st);
+    case 8: return topm_launch<T, 8>(L, n, V, m, idx, val, st);
+    case 9: return topm_launch<T, 9>(L, n, V, m, idx, val, st);
+    case 10: return topm_launch<T, 10>(L, n, V, m, idx, val, st);
+    case 11: return topm_launch<T, 11>(L, n, V, m, idx, val, st);
+    case 12: return topm_launch<T, 12>(L, n, V, m, idx, val, st);
+    case 13: return topm_launch<T, 13>(L, n, V, m, idx, val, st);
+    case 14: return topm_launch<T, 14>(L, n, V, m, idx, val, st);
+    case 15: return topm_launch<T, 15>(L, n, V, m, idx, val, st);
+    default: return topm_launch<T, 16>(L, n, V, m, idx, val, st);
   }
 }
 
